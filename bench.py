@@ -1,0 +1,276 @@
+#!/usr/bin/env python3
+"""Benchmark of the hot path on one MI355X: jagged dynamic-mask HSTU attention with the
+gate + Group-LayerNorm that follows it (MTGR, arXiv 2505.18654, Sec. 4.2), fwd + bwd.
+
+One step = plan (tile summaries + work list) -> attention fwd -> gate + Group-LN fwd ->
+Group-LN bwd -> attention bwd (dQ kernel, then dK/dV kernel), on one synthetic batch of
+the MTGR-large shape (64 users, 16 user tokens, lognormal history, 8 heads x 128) whose
+inputs are resident in HBM before the timed region.  Prints ONE JSON line.
+
+    python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--workload mtgr_large]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16 = 2.5e15        # MI355X dense bf16 MFMA, FLOP/s
+PEAK_FP32 = 157.3e12      # MI355X fp32 vector, FLOP/s
+PEAK_HBM = 8.0e12         # MI355X HBM3E, B/s
+METRIC = "jagged HSTU attn fwd+bwd tokens/s and TFLOP/s (% bf16 MFMA peak), 1 MI355X"
+CSRC = os.path.join(ROOT, "paper_2505_18654_amd", "csrc")
+
+
+def visible_pairs(layout) -> np.ndarray:
+    """Mask-visible (i, j) pairs per user, counted segment by segment (Sec. 4.2 rules)."""
+    out = np.zeros(layout.num_users, np.int64)
+    for b in range(layout.num_users):
+        sl = layout.user_slice(b)
+        seg, ts = layout.seg[sl], layout.ts[sl].astype(np.int64)
+        n = len(seg)
+        n_s = int(np.sum(seg <= 1))
+        rt = np.sort(ts[seg == 2])
+        rt_q = ts[seg == 2]
+        cand = ts[seg == 3]
+        earlier_rt = np.searchsorted(rt, rt_q, side="left").sum() + np.searchsorted(rt, cand, side="left").sum()
+        dyn = n - n_s
+        out[b] = n_s * n_s + dyn * n_s + earlier_rt + dyn
+    return out
+
+
+def source_hash() -> str:
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(CSRC)):
+        with open(os.path.join(CSRC, name), "rb") as f:
+            h.update(name.encode() + f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch from the committed rocprofv3 counter runs, if they were taken
+    on the current kernel sources (else None)."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    try:
+        with open(path) as f:
+            data = json.load(f)
+    except (OSError, ValueError):
+        return None
+    entry = data.get(f"{kernel}@{workload}")
+    if not entry or entry.get("source_hash") != source_hash():
+        return None
+    return entry.get("bytes_per_launch")
+
+
+def cpu_baseline(layout, budget_s: float):
+    """The oracle (plain fp64 C, OpenMP) on a bounded sample of the same batch: the users
+    with the smallest visible-pair count first, until about `budget_s` seconds of work."""
+    import oracle
+    from synth import make_values
+    pairs = visible_pairs(layout)
+    H, dh = layout.spec.heads, layout.spec.head_dim
+    order = list(np.argsort(pairs, kind="stable"))
+    # calibrate the oracle's pair rate on one small user
+    probe = [int(order[len(order) // 4])]
+    t_probe = _oracle_step(layout, probe)
+    rate = max(pairs[probe[0]] * H / max(t_probe, 1e-6), 1.0)      # (pair * head) / s
+    chosen, work = [], 0.0
+    for b in order[::-1]:                                             # mix: largest first
+        cost = pairs[b] * H / rate
+        if work + cost > budget_s and chosen:
+            continue
+        chosen.append(int(b))
+        work += cost
+        if work >= 0.6 * budget_s:
+            break
+    t = _oracle_step(layout, chosen)
+    tokens = int(sum(layout.offsets[b + 1] - layout.offsets[b] for b in chosen))
+    threads = int(os.environ.get("OMP_NUM_THREADS", 0)) or len(os.sched_getaffinity(0))
+    return {"value": tokens / t, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"{len(chosen)} of {layout.num_users} users ({tokens} tokens, "
+                      f"{int(pairs[chosen].sum())} visible pairs x {H} heads), same path fwd+bwd, "
+                      f"fp64, {t:.1f} s",
+            "seconds": round(t, 2)}
+
+
+def _oracle_step(layout, users) -> float:
+    import oracle
+    from synth import make_values
+    sub = layout.subset(users)
+    vals = make_values(sub)
+    H, dh = layout.spec.heads, layout.spec.head_dim
+    T = sub.total_tokens
+    t0 = time.perf_counter()
+    o = oracle.attn_fwd(sub.offsets, sub.seg, sub.ts, vals["q"], vals["k"], vals["v"], vals["rab"])
+    x = o.reshape(T, H * dh)
+    oracle.gln_fwd(x, vals["u"], sub.seg, vals["gamma"], vals["beta"])
+    dx, _, _, _ = oracle.gln_bwd(x, vals["u"], sub.seg, vals["gamma"], vals["dy"])
+    oracle.attn_bwd(sub.offsets, sub.seg, sub.ts, vals["q"], vals["k"], vals["v"], dx.reshape(T, H, dh),
+                    vals["rab"])
+    return time.perf_counter() - t0
+
+
+def sampled_parity(layout, inp, res, users):
+    """Forward attention output of a few users against the oracle (max-abs / RMS)."""
+    import oracle
+    from synth import make_values
+    sub = layout.subset(users)
+    vals = make_values(sub, tensors=("q", "k", "v"))
+    ref = oracle.attn_fwd(sub.offsets, sub.seg, sub.ts, vals["q"], vals["k"], vals["v"], inp["rab_np"])
+    rows = np.concatenate([np.arange(layout.offsets[b], layout.offsets[b + 1]) for b in users])
+    got = res["o"].float().cpu().numpy()[rows]
+    worst, row = 0.0, 0
+    for b in users:
+        n = int(layout.offsets[b + 1] - layout.offsets[b])
+        g, w = got[row:row + n], ref[row:row + n]
+        row += n
+        rms = float(np.sqrt(np.mean(w ** 2)))
+        excess = float(np.max(np.maximum(np.abs(g - w) - 2.0 ** -8 * np.abs(w), 0.0)))
+        worst = max(worst, excess / rms if rms else 0.0)
+    return worst
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="mtgr_large",
+                    choices=["tiny", "small", "mtgr_small", "mtgr_large", "serving"])
+    ap.add_argument("--cpu-seconds", type=float, default=20.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build measures one GPU; --gpus {args.gpus} is not supported "
+              "(the hot path shards by user across GPUs with no forward exchange; see DESIGN.md)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2505_18654_amd import ops
+    from synth import make_layout
+    from synth.torch_inputs import device_inputs
+
+    layout = make_layout(args.workload)
+    spec = layout.spec
+    H, dh = spec.heads, spec.head_dim
+    d = H * dh
+    T = layout.total_tokens
+    lens = np.diff(layout.offsets)
+    check_users = sorted({int(np.argmin(lens)), int(np.argsort(lens)[len(lens) // 2])})
+    fwd_only = spec.fwd_only
+    tensors = ("q", "k", "v", "u") if fwd_only else ("q", "k", "v", "u", "dy")
+    inp = device_inputs(layout, "cuda", exact_users=check_users, tensors=tensors)
+    jag = ops.Jagged(inp["offsets"], inp["seg"], inp["ts"], inp["max_seqlen"])
+    q, k, v, u = inp["q"], inp["k"], inp["v"], inp["u"]
+    rab, gamma, beta, seg = inp["rab"], inp["gamma"], inp["beta"], inp["seg"]
+
+    # preallocated outputs and workspace: nothing is allocated inside the timed region
+    o = torch.empty_like(q)
+    y = torch.empty((T, d), dtype=q.dtype, device="cuda")
+    mean = torch.empty(T, dtype=torch.float32, device="cuda")
+    rstd = torch.empty(T, dtype=torch.float32, device="cuda")
+    dx = torch.empty((T, d), dtype=q.dtype, device="cuda")
+    du = torch.empty((T, d), dtype=q.dtype, device="cuda")
+    dg = torch.empty_like(gamma)
+    db = torch.empty_like(gamma)
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    drab = torch.empty_like(rab) if rab is not None else None
+    ws = ops.workspace_for(ops.attn_problem(jag, q, k, v, o, rab), "cuda")
+
+    stages = ["plan", "attn_fwd", "gln_fwd"] + ([] if fwd_only else ["gln_bwd", "attn_bwd_dq", "attn_bwd_dkdv"])
+
+    def run(name):
+        if name == "plan":
+            ops.attn_plan(q, jag, workspace=ws, rab=rab)
+        elif name == "attn_fwd":
+            ops.attn_fwd(q, k, v, jag, rab, out=o, workspace=ws, planned=True)
+        elif name == "gln_fwd":
+            ops.gln_fwd(o.view(T, d), u, seg, gamma, beta, y=y, stats=(mean, rstd))
+        elif name == "gln_bwd":
+            ops.gln_bwd(inp["dy"], o.view(T, d), u, seg, gamma, mean, rstd, grads=(dx, du, dg, db))
+        elif name == "attn_bwd_dq":
+            ops.attn_bwd(q, k, v, dx.view(T, H, dh), jag, rab, grads=(dq, dk, dv, drab), workspace=ws,
+                         planned=True, parts="dq")
+        elif name == "attn_bwd_dkdv":
+            ops.attn_bwd(q, k, v, dx.view(T, H, dh), jag, rab, grads=(dq, dk, dv, drab), workspace=ws,
+                         planned=True, parts="dkdv")
+
+    for _ in range(args.warmup):
+        for s in stages:
+            run(s)
+    torch.cuda.synchronize()
+
+    ev = {s: [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(args.steps)] for s in stages}
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        for s in stages:
+            ev[s][i][0].record()
+            run(s)
+            ev[s][i][1].record()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    stage_ms = {s: float(np.mean([a.elapsed_time(b) for a, b in ev[s]])) for s in stages}
+
+    pairs = int(visible_pairs(layout).sum())
+    f_fwd = 4.0 * dh * H * pairs
+    f_bwd = 0.0 if fwd_only else 8.0 * dh * H * pairs
+    ms_step = elapsed * 1e3 / args.steps
+    tflops = (f_fwd + f_bwd) / (ms_step * 1e-3) / 1e12
+
+    # dominant kernel and its roofline (algorithmic flops per launch / event-timed duration)
+    kflops = {"attn_fwd": f_fwd, "attn_bwd_dq": f_bwd / 2, "attn_bwd_dkdv": f_bwd / 2}
+    kname = {"attn_fwd": "attn_fwd_bf16_kernel", "attn_bwd_dq": "attn_bwd_dq_bf16_kernel",
+             "attn_bwd_dkdv": "attn_bwd_dkdv_bf16_kernel"}
+    dom = max((s for s in kflops if s in stage_ms), key=lambda s: stage_ms[s])
+    achieved = kflops[dom] / (stage_ms[dom] * 1e-3)
+    roofline = {"bound": "mfma", "kernel": kname[dom], "achieved": achieved / 1e12, "peak": PEAK_BF16 / 1e12,
+                "unit": "TFLOP/s", "frac": achieved / PEAK_BF16,
+                "traffic": measured_traffic(kname[dom], args.workload)}
+    gln_bytes = T * (3 * d * 2 + 8) + (0 if fwd_only else T * (5 * d * 2 + 8))
+    gln_ms = stage_ms["gln_fwd"] + stage_ms.get("gln_bwd", 0.0)
+
+    res = {"o": o}
+    err = sampled_parity(layout, inp, res, check_users)
+
+    line = {
+        "metric": METRIC,
+        "value": T * args.steps / elapsed,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if spec.dtype == "bf16" else "f32",
+        "data": "synthetic",
+        "config": {"workload": args.workload, "users": layout.num_users, "tokens": T,
+                   "max_seqlen": layout.max_seqlen, "heads": H, "head_dim": dh, "d": d,
+                   "rab_buckets": spec.rab_buckets, "pass": "fwd" if fwd_only else "fwd+bwd"},
+        "tflops": tflops,
+        "pct_bf16_peak": 100.0 * tflops * 1e12 / PEAK_BF16,
+        "visible_pairs": pairs,
+        "stage_ms": {s: round(v, 4) for s, v in stage_ms.items()},
+        "gln": {"bound": "hbm", "achieved_GBps": gln_bytes / (gln_ms * 1e-3) / 1e9, "peak_GBps": PEAK_HBM / 1e9},
+        "roofline": roofline,
+        "parity_sampled_fwd": {"users": check_users, "max_err_over_rms": err},
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(layout, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,200 @@
+/*
+ * mtgr_hstu.h — C ABI of the MI355X (gfx950) implementation of MTGR's jagged
+ * dynamic-mask HSTU attention and the gated Group-LayerNorm that follows it
+ * (MTGR, arXiv 2505.18654, Sec. 4.2, Eq. 5 and Eq. 6).
+ *
+ * Conventions shared by every entry point
+ *   - Every tensor pointer is DEVICE memory owned by the caller (borrowed; the
+ *     library keeps no reference after the call returns).  The library never
+ *     allocates device memory and never synchronises the stream.
+ *   - Calls are asynchronous on `stream` (a hipStream_t; NULL = the null stream).
+ *   - Outputs are overwritten, never accumulated into (this includes the
+ *     parameter gradients dgamma, dbeta and drab).
+ *   - On any status other than MTGR_SUCCESS nothing has been launched and every
+ *     output is untouched, except MTGR_ERROR_DEVICE, which reports a failed
+ *     launch (outputs then undefined).  mtgr_last_error_message() names the
+ *     offending argument.
+ *   - Jagged batches: user b owns tokens offsets[b] .. offsets[b+1]-1 of a
+ *     [T, ...] tensor.  offsets (int32, B+1 entries, device) must satisfy
+ *     offsets[0] = 0, offsets[b] <= offsets[b+1], offsets[B] = total_tokens and
+ *     offsets[b+1] - offsets[b] <= max_seqlen; seg[t] must lie in 0..3 and
+ *     group ids in 0..G-1.  These device-resident preconditions are not checked
+ *     (checking them would need a synchronisation); violating them is undefined.
+ *   - B = 0 or T = 0 is a successful no-op (outputs of size zero; parameter
+ *     gradients are zero-filled).
+ *   - Every function is stateless and may be called concurrently from several
+ *     host threads.
+ */
+#ifndef MTGR_HSTU_H
+#define MTGR_HSTU_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MTGR_HSTU_VERSION 100           /* major * 100 + minor */
+
+typedef enum {
+    MTGR_SUCCESS = 0,
+    MTGR_ERROR_NULL_POINTER = 1,        /* a required pointer is NULL */
+    MTGR_ERROR_INVALID_ARGUMENT = 2,    /* a size, stride or alignment is invalid */
+    MTGR_ERROR_UNSUPPORTED = 3,         /* valid but not implemented (head_dim, dtype, ...) */
+    MTGR_ERROR_WORKSPACE_TOO_SMALL = 4, /* workspace_bytes below the queried size */
+    MTGR_ERROR_DEVICE = 5               /* a HIP call or kernel launch failed */
+} mtgr_status_t;
+
+typedef enum {
+    MTGR_DTYPE_BF16 = 0,                /* bf16 storage, fp32 accumulation */
+    MTGR_DTYPE_FP32 = 1                 /* fp32 storage and arithmetic (parity mode) */
+} mtgr_dtype_t;
+
+/* Token segments of the sequence [U | S | R | I] (Sec. 4.1, Eq. 4). */
+enum {
+    MTGR_SEG_USER = 0,                  /* user-feature token (static) */
+    MTGR_SEG_HIST = 1,                  /* history item (static) */
+    MTGR_SEG_RT = 2,                    /* real-time item (dynamic) */
+    MTGR_SEG_CAND = 3                   /* candidate (cross + item features) */
+};
+
+/* Bits of mtgr_hstu_problem_t.flags. */
+#define MTGR_ATTN_PLANNED 1u   /* the workspace already holds this batch's plan
+                                  (mtgr_hstu_attn_plan); skip rebuilding it */
+#define MTGR_BWD_SKIP_DQ 2u    /* backward: do not form dq (dq may be NULL) */
+#define MTGR_BWD_SKIP_DKDV 4u  /* backward: do not form dk, dv (both may be NULL) */
+
+#define MTGR_MAX_RAB_BUCKETS 64
+#define MTGR_MAX_HEADS 255
+#define MTGR_MAX_GROUPS 127
+
+typedef void* mtgr_stream_t;            /* hipStream_t */
+
+/* Shape of one attention call.
+ *   num_users B >= 0, total_tokens T >= 0 (T < 2^31), max_seqlen >= every user's length.
+ *   num_heads H in 1..255; head_dim dh: bf16 {32, 64, 128}, fp32 {16, 32, 64, 128}.
+ *   alpha: multiplier of q.k inside the SiLU (Eq. 5 has none: pass 1.0).
+ *   num_rab_buckets: 0 = no relative bias, else 1..64 (rab is [H][num_rab_buckets] fp32;
+ *     a gap whose log-time bucket is >= num_rab_buckets uses the last bucket).
+ *   ld_*: token strides in ELEMENTS (>= H*dh); q, k, v may be views into one fused
+ *     projection output.  Gradients share the layout of their primal:
+ *     dq uses ld_q, dk ld_k, dv ld_v, and dout uses ld_o.
+ *   flags: see MTGR_ATTN_PLANNED and MTGR_BWD_SKIP_*.
+ * Alignment: every tensor pointer 16-byte aligned; every ld a multiple of 16 bytes. */
+typedef struct {
+    int32_t num_users;
+    int32_t max_seqlen;
+    int64_t total_tokens;
+    int32_t num_heads;
+    int32_t head_dim;
+    int32_t dtype;                      /* mtgr_dtype_t */
+    float alpha;
+    int32_t num_rab_buckets;
+    uint32_t flags;                     /* MTGR_ATTN_PLANNED | MTGR_BWD_SKIP_* (0 = none) */
+    int64_t ld_q, ld_k, ld_v, ld_o;
+} mtgr_hstu_problem_t;
+
+/* Shape of one gate + Group-LN call.
+ *   num_tokens T >= 0, dim d (bf16: multiple of 8 and <= 4096; fp32: multiple of 4 and <= 2048),
+ *   num_groups G in 1..127, eps > 0.
+ *   ld_*: token strides in elements (>= d).  Gradients share the layout of their
+ *   primal: dx uses ld_x, du ld_u, dy ld_y. */
+typedef struct {
+    int64_t num_tokens;
+    int32_t dim;
+    int32_t num_groups;
+    int32_t dtype;                      /* mtgr_dtype_t */
+    float eps;
+    int64_t ld_x, ld_u, ld_y;
+} mtgr_gln_problem_t;
+
+/* Bytes of device workspace needed by mtgr_hstu_attn_fwd (backward = 0) or
+ * mtgr_hstu_attn_bwd (backward = 1) for problem `p`.  Pure host arithmetic. */
+mtgr_status_t mtgr_hstu_attn_workspace_size(const mtgr_hstu_problem_t* p, int backward,
+                                            size_t* bytes);
+
+/* Builds the batch plan into `workspace`: per 64-token tile of every user, the segment
+ * flags and time range that classify each (query tile, key tile) pair as fully visible,
+ * partially visible or fully masked under the dynamic mask (Sec. 4.2), and a work list of
+ * (user, head, tile) items ordered longest user first.  The plan depends only on
+ * offsets, seg, ts and the problem shape, so one plan serves every forward and backward
+ * call on the same batch (all layers of the encoder) when they pass MTGR_ATTN_PLANNED.
+ * Without that flag, mtgr_hstu_attn_fwd/bwd rebuild the plan themselves. */
+mtgr_status_t mtgr_hstu_attn_plan(const mtgr_hstu_problem_t* p, const int32_t* offsets,
+                                  const int8_t* seg, const int32_t* ts, void* workspace,
+                                  size_t workspace_bytes, mtgr_stream_t stream);
+
+/* Forward of Eq. 5 (Sec. 4.2) for every user b, head h and token i of b:
+ *   out[i,h,:] = sum over tokens j of b with M_ij = 1 of
+ *                silu(alpha * q[i,h,:].k[j,h,:] + rab[h, bucket(|ts_i - ts_j|)]) / n_b * v[j,h,:]
+ * where n_b is the user's token count (candidates included) and M is the
+ * dynamic mask of Sec. 4.2 ("Dynamic Masking"), evaluated from seg and ts:
+ *   M_ij = 1 iff i == j, or seg_j is USER/HIST (static, rule 1), or seg_j is RT and
+ *   seg_i is RT/CAND and ts_j < ts_i (rule 2); candidates are seen only by
+ *   themselves (rule 3).
+ * The bias term is present only when rab != NULL (requires num_rab_buckets > 0);
+ * bucket(g) = g for g < 2, else 2e + [g >= 1.5 * 2^e] with e = floor(log2 g), g as uint32.
+ *   offsets [B+1] int32, seg [T] int8, ts [T] int32 (seconds; any epoch).
+ *   q, k, v [T, H, dh] (dtype), out [T, H, dh] (dtype, stride ld_o).
+ *   workspace: at least mtgr_hstu_attn_workspace_size(p, 0) bytes, 256-byte aligned. */
+mtgr_status_t mtgr_hstu_attn_fwd(const mtgr_hstu_problem_t* p, const int32_t* offsets,
+                                 const int8_t* seg, const int32_t* ts, const void* q,
+                                 const void* k, const void* v, const float* rab, void* out,
+                                 void* workspace, size_t workspace_bytes, mtgr_stream_t stream);
+
+/* Backward of Eq. 5: given dout = dL/dout, writes dq, dk, dv (same dtype and
+ * layout as q, k, v) and, when drab != NULL, drab = dL/drab ([H][num_rab_buckets]
+ * fp32; requires rab != NULL).  With s = alpha q.k + rab, sg = sigmoid(s):
+ *   dS_ij = M_ij (dout_i . v_j) sg (1 + s (1 - sg)) / n_b,
+ *   dv_j = sum_i M_ij silu(s_ij)/n_b dout_i,  dq_i = alpha sum_j dS_ij k_j,
+ *   dk_j = alpha sum_i dS_ij q_i,  drab[h, x] = sum over pairs in bucket x of dS_ij.
+ * The forward saves nothing (no softmax statistics), so the same inputs are passed.
+ * dq and (dk, dv) come from two independent kernels; MTGR_BWD_SKIP_DQ / _DKDV launch
+ * only one of them (drab is formed with dq).  The workspace is the forward's. */
+mtgr_status_t mtgr_hstu_attn_bwd(const mtgr_hstu_problem_t* p, const int32_t* offsets,
+                                 const int8_t* seg, const int32_t* ts, const void* q,
+                                 const void* k, const void* v, const float* rab,
+                                 const void* dout, void* dq, void* dk, void* dv, float* drab,
+                                 void* workspace, size_t workspace_bytes, mtgr_stream_t stream);
+
+/* Bytes of device workspace for the Group-LN calls (currently always 0). */
+mtgr_status_t mtgr_group_layernorm_workspace_size(const mtgr_gln_problem_t* p, int backward,
+                                                  size_t* bytes);
+
+/* Eq. 6 up to the MLP (Sec. 4.2): y = GroupLN(x (*) u) per token t:
+ *   z = x[t] (*) u[t]  (u == NULL: z = x[t], the input Group-LN before the projections)
+ *   mean[t] = mean(z), rstd[t] = 1/sqrt(mean((z - mean)^2) + eps)  (biased variance)
+ *   y[t] = gamma[g] (*) (z - mean[t]) rstd[t] + beta[g],  g = group_ids[t].
+ *   x, u, y [T, d] (dtype); group_ids [T] int8; gamma, beta [G][d] fp32;
+ *   mean, rstd [T] fp32 (may be NULL when not needed for a backward). */
+mtgr_status_t mtgr_group_layernorm_fwd(const mtgr_gln_problem_t* p, const void* x, const void* u,
+                                       const int8_t* group_ids, const float* gamma,
+                                       const float* beta, void* y, float* mean, float* rstd,
+                                       mtgr_stream_t stream);
+
+/* Backward of mtgr_group_layernorm_fwd, using its saved mean and rstd:
+ *   with zhat = (z - mean) rstd and g = dy (*) gamma[g_t]:
+ *   dz = rstd (g - mean(g) - zhat mean(g (*) zhat)),  dx = dz (*) u,  du = dz (*) x,
+ *   dgamma[g] = sum over tokens of group g of dy (*) zhat,  dbeta[g] = sum of dy.
+ *   du must be non-NULL iff u is non-NULL.  dgamma, dbeta [G][d] fp32 are
+ *   overwritten; their summation order is not fixed (fp32 atomics). */
+mtgr_status_t mtgr_group_layernorm_bwd(const mtgr_gln_problem_t* p, const void* dy, const void* x,
+                                       const void* u, const int8_t* group_ids, const float* gamma,
+                                       const float* mean, const float* rstd, void* dx, void* du,
+                                       float* dgamma, float* dbeta, void* workspace,
+                                       size_t workspace_bytes, mtgr_stream_t stream);
+
+/* Static string for a status code. */
+const char* mtgr_status_string(mtgr_status_t status);
+
+/* Message of the last failing call on the calling host thread ("" if none). */
+const char* mtgr_last_error_message(void);
+
+/* MTGR_HSTU_VERSION of the loaded library. */
+int32_t mtgr_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MTGR_HSTU_H */

@@ -1,0 +1,434 @@
+// C ABI of the library: argument validation (pure host code, before any HIP call),
+// workspace layout and kernel launches.  See include/mtgr_hstu.h for the contract.
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+
+#include "../../include/mtgr_hstu.h"
+#include "mtgr_internal.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+mtgr_status_t fail(mtgr_status_t st, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+mtgr_status_t fail(mtgr_status_t st, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return st;
+}
+
+mtgr_status_t ok() {
+    g_last_error.clear();
+    return MTGR_SUCCESS;
+}
+
+mtgr_status_t device_fail(hipError_t e, const char* where) {
+    return fail(MTGR_ERROR_DEVICE, "%s: %s", where, hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+constexpr int MAX_SEQLEN = (mtgr::SCHED_BUCKETS - 1) * 64;
+
+struct AttnLayout {
+    int tile;            // rows per work item
+    int ntile;           // 64-token summary tiles per user
+    long long slots;     // physical work-list entries (= grid size)
+    size_t off_summ, off_items, off_sorted, total;
+};
+
+AttnLayout attn_layout(const mtgr_hstu_problem_t* p) {
+    AttnLayout L{};
+    L.tile = p->dtype == MTGR_DTYPE_BF16 ? mtgr::ATTN_TILE_BF16 : mtgr::ATTN_TILE_F32;
+    L.ntile = (p->max_seqlen + 63) / 64;
+    L.slots = mtgr::schedule_slots(p->total_tokens, p->num_users, p->max_seqlen, p->num_heads, L.tile);
+    L.off_summ = 0;
+    L.off_items = align256((size_t)p->num_users * L.ntile * sizeof(int4));
+    L.off_sorted = L.off_items + align256((size_t)L.slots * sizeof(int2));
+    L.total = L.off_sorted + align256((size_t)p->num_users * sizeof(int));
+    return L;
+}
+
+mtgr_status_t check_problem(const mtgr_hstu_problem_t* p) {
+    if (!p) return fail(MTGR_ERROR_NULL_POINTER, "problem is NULL");
+    if (p->dtype != MTGR_DTYPE_BF16 && p->dtype != MTGR_DTYPE_FP32)
+        return fail(MTGR_ERROR_UNSUPPORTED, "dtype %d is not supported", p->dtype);
+    if (p->num_users < 0) return fail(MTGR_ERROR_INVALID_ARGUMENT, "num_users %d < 0", p->num_users);
+    if (p->total_tokens < 0 || p->total_tokens >= (1ll << 31))
+        return fail(MTGR_ERROR_INVALID_ARGUMENT, "total_tokens %lld outside [0, 2^31)",
+                    (long long)p->total_tokens);
+    if (p->max_seqlen < 0) return fail(MTGR_ERROR_INVALID_ARGUMENT, "max_seqlen %d < 0", p->max_seqlen);
+    if (p->num_users > 0 && p->total_tokens > 0 && p->max_seqlen == 0)
+        return fail(MTGR_ERROR_INVALID_ARGUMENT, "max_seqlen is 0 with tokens present");
+    if (p->total_tokens > 0 && p->num_users == 0)
+        return fail(MTGR_ERROR_INVALID_ARGUMENT, "total_tokens > 0 with no users");
+    if (p->max_seqlen > MAX_SEQLEN)
+        return fail(MTGR_ERROR_UNSUPPORTED, "max_seqlen %d above %d", p->max_seqlen, MAX_SEQLEN);
+    if (p->num_heads < 1 || p->num_heads > MTGR_MAX_HEADS)
+        return fail(MTGR_ERROR_INVALID_ARGUMENT, "num_heads %d outside 1..%d", p->num_heads,
+                    MTGR_MAX_HEADS);
+    const int dh = p->head_dim;
+    const bool dh_ok = p->dtype == MTGR_DTYPE_BF16 ? (dh == 32 || dh == 64 || dh == 128)
+                                                    : (dh == 16 || dh == 32 || dh == 64 || dh == 128);
+    if (!dh_ok)
+        return fail(MTGR_ERROR_UNSUPPORTED, "head_dim %d not supported for %s", dh,
+                    p->dtype == MTGR_DTYPE_BF16 ? "bf16" : "fp32");
+    if (p->num_rab_buckets < 0 || p->num_rab_buckets > MTGR_MAX_RAB_BUCKETS)
+        return fail(MTGR_ERROR_INVALID_ARGUMENT, "num_rab_buckets %d outside 0..%d",
+                    p->num_rab_buckets, MTGR_MAX_RAB_BUCKETS);
+    if (p->flags & ~(MTGR_ATTN_PLANNED | MTGR_BWD_SKIP_DQ | MTGR_BWD_SKIP_DKDV))
+        return fail(MTGR_ERROR_INVALID_ARGUMENT, "unknown flags 0x%x", p->flags);
+    if (!std::isfinite(p->alpha)) return fail(MTGR_ERROR_INVALID_ARGUMENT, "alpha is not finite");
+    const long long row = (long long)p->num_heads * dh;
+    const int esz = p->dtype == MTGR_DTYPE_BF16 ? 2 : 4;
+    const long long lds[4] = {p->ld_q, p->ld_k, p->ld_v, p->ld_o};
+    const char* names[4] = {"ld_q", "ld_k", "ld_v", "ld_o"};
+    for (int i = 0; i < 4; i++) {
+        if (lds[i] < row)
+            return fail(MTGR_ERROR_INVALID_ARGUMENT, "%s %lld below num_heads*head_dim %lld", names[i],
+                        lds[i], row);
+        if ((lds[i] * esz) % 16 != 0)
+            return fail(MTGR_ERROR_INVALID_ARGUMENT, "%s %lld is not a multiple of 16 bytes", names[i],
+                        lds[i]);
+    }
+    if (mtgr::schedule_slots(p->total_tokens, p->num_users, p->max_seqlen, p->num_heads,
+                             mtgr::ATTN_TILE_F32) >= (1ll << 31))
+        return fail(MTGR_ERROR_UNSUPPORTED, "problem too large for one launch");
+    return MTGR_SUCCESS;
+}
+
+#define REQUIRE_PTR(ptr, name)                                                        \
+    do {                                                                              \
+        if (!(ptr)) return fail(MTGR_ERROR_NULL_POINTER, "%s is NULL", name);         \
+        if (!aligned16(ptr))                                                          \
+            return fail(MTGR_ERROR_INVALID_ARGUMENT, "%s is not 16-byte aligned", name); \
+    } while (0)
+
+mtgr_status_t check_attn_common(const mtgr_hstu_problem_t* p, const int32_t* offsets,
+                                const int8_t* seg, const int32_t* ts, const float* rab,
+                                void* workspace, size_t ws_bytes) {
+    mtgr_status_t st = check_problem(p);
+    if (st != MTGR_SUCCESS) return st;
+    if (rab && p->num_rab_buckets == 0)
+        return fail(MTGR_ERROR_INVALID_ARGUMENT, "rab given but num_rab_buckets is 0");
+    if (p->num_users > 0) {
+        if (!offsets) return fail(MTGR_ERROR_NULL_POINTER, "offsets is NULL");
+        if (((uintptr_t)offsets & 3u) != 0)
+            return fail(MTGR_ERROR_INVALID_ARGUMENT, "offsets is not 4-byte aligned");
+    }
+    if (p->total_tokens > 0) {
+        if (!seg) return fail(MTGR_ERROR_NULL_POINTER, "seg is NULL");
+        if (!ts) return fail(MTGR_ERROR_NULL_POINTER, "ts is NULL");
+        if (((uintptr_t)ts & 3u) != 0) return fail(MTGR_ERROR_INVALID_ARGUMENT, "ts is not 4-byte aligned");
+    }
+    if (rab && ((uintptr_t)rab & 3u) != 0)
+        return fail(MTGR_ERROR_INVALID_ARGUMENT, "rab is not 4-byte aligned");
+    const AttnLayout L = attn_layout(p);
+    if (p->num_users > 0 && p->total_tokens > 0) {
+        if (ws_bytes < L.total)
+            return fail(MTGR_ERROR_WORKSPACE_TOO_SMALL, "workspace %zu bytes, need %zu", ws_bytes,
+                        L.total);
+        if (!workspace) return fail(MTGR_ERROR_NULL_POINTER, "workspace is NULL");
+        if (((uintptr_t)workspace & 255u) != 0)
+            return fail(MTGR_ERROR_INVALID_ARGUMENT, "workspace is not 256-byte aligned");
+    }
+    return MTGR_SUCCESS;
+}
+
+mtgr::AttnArgs make_args(const mtgr_hstu_problem_t* p, const AttnLayout& L, const int32_t* offsets,
+                         const int8_t* seg, const int32_t* ts, void* workspace) {
+    mtgr::AttnArgs a{};
+    a.offsets = offsets;
+    a.seg = seg;
+    a.ts = ts;
+    a.ld_q = p->ld_q;
+    a.ld_k = p->ld_k;
+    a.ld_v = p->ld_v;
+    a.ld_o = p->ld_o;
+    char* ws = (char*)workspace;
+    a.summ = (const int4*)(ws + L.off_summ);
+    a.items = (const int2*)(ws + L.off_items);
+    a.ntile = L.ntile;
+    a.heads = p->num_heads;
+    a.alpha = p->alpha;
+    a.nbuckets = p->num_rab_buckets;
+    return a;
+}
+
+// Tile summaries + work list into the workspace.
+mtgr_status_t schedule(const mtgr_hstu_problem_t* p, const AttnLayout& L, const int32_t* offsets,
+                       const int8_t* seg, const int32_t* ts, void* workspace, hipStream_t s) {
+    char* ws = (char*)workspace;
+    hipError_t e = mtgr::launch_tile_summaries(offsets, seg, ts, p->num_users, L.ntile,
+                                               (int4*)(ws + L.off_summ), s);
+    if (e != hipSuccess) return device_fail(e, "tile summaries");
+    e = mtgr::launch_build_schedule(offsets, p->num_users, p->num_heads, L.tile,
+                                    (int2*)(ws + L.off_items), (int)L.slots, (int*)(ws + L.off_sorted), s);
+    if (e != hipSuccess) return device_fail(e, "schedule");
+    return MTGR_SUCCESS;
+}
+
+}  // namespace
+
+extern "C" {
+
+mtgr_status_t mtgr_hstu_attn_plan(const mtgr_hstu_problem_t* p, const int32_t* offsets,
+                                  const int8_t* seg, const int32_t* ts, void* workspace,
+                                  size_t workspace_bytes, mtgr_stream_t stream) {
+    mtgr_status_t st = check_attn_common(p, offsets, seg, ts, nullptr, workspace, workspace_bytes);
+    if (st != MTGR_SUCCESS) return st;
+    if (p->num_users == 0 || p->total_tokens == 0) return ok();
+    st = schedule(p, attn_layout(p), offsets, seg, ts, workspace, (hipStream_t)stream);
+    if (st != MTGR_SUCCESS) return st;
+    return ok();
+}
+
+mtgr_status_t mtgr_hstu_attn_workspace_size(const mtgr_hstu_problem_t* p, int backward, size_t* bytes) {
+    (void)backward;
+    if (!bytes) return fail(MTGR_ERROR_NULL_POINTER, "bytes is NULL");
+    mtgr_status_t st = check_problem(p);
+    if (st != MTGR_SUCCESS) return st;
+    *bytes = (p->num_users > 0 && p->total_tokens > 0) ? attn_layout(p).total : 0;
+    return ok();
+}
+
+mtgr_status_t mtgr_hstu_attn_fwd(const mtgr_hstu_problem_t* p, const int32_t* offsets,
+                                 const int8_t* seg, const int32_t* ts, const void* q, const void* k,
+                                 const void* v, const float* rab, void* out, void* workspace,
+                                 size_t workspace_bytes, mtgr_stream_t stream) {
+    mtgr_status_t st = check_attn_common(p, offsets, seg, ts, rab, workspace, workspace_bytes);
+    if (st != MTGR_SUCCESS) return st;
+    if (p->num_users == 0 || p->total_tokens == 0) return ok();
+    REQUIRE_PTR(q, "q");
+    REQUIRE_PTR(k, "k");
+    REQUIRE_PTR(v, "v");
+    REQUIRE_PTR(out, "out");
+    hipStream_t s = (hipStream_t)stream;
+    const AttnLayout L = attn_layout(p);
+    if (!(p->flags & MTGR_ATTN_PLANNED)) {
+        st = schedule(p, L, offsets, seg, ts, workspace, s);
+        if (st != MTGR_SUCCESS) return st;
+    }
+    mtgr::AttnArgs a = make_args(p, L, offsets, seg, ts, workspace);
+    a.q = q;
+    a.k = k;
+    a.v = v;
+    a.rab = rab;
+    a.out = out;
+    hipError_t e = p->dtype == MTGR_DTYPE_BF16
+                       ? mtgr::launch_attn_fwd_bf16(a, p->head_dim, (int)L.slots, s)
+                       : mtgr::launch_attn_fwd_f32(a, p->head_dim, (int)L.slots, s);
+    if (e != hipSuccess) return device_fail(e, "attention forward");
+    return ok();
+}
+
+mtgr_status_t mtgr_hstu_attn_bwd(const mtgr_hstu_problem_t* p, const int32_t* offsets,
+                                 const int8_t* seg, const int32_t* ts, const void* q, const void* k,
+                                 const void* v, const float* rab, const void* dout, void* dq,
+                                 void* dk, void* dv, float* drab, void* workspace,
+                                 size_t workspace_bytes, mtgr_stream_t stream) {
+    mtgr_status_t st = check_attn_common(p, offsets, seg, ts, rab, workspace, workspace_bytes);
+    if (st != MTGR_SUCCESS) return st;
+    if (drab && !rab) return fail(MTGR_ERROR_INVALID_ARGUMENT, "drab given without rab");
+    if (drab && ((uintptr_t)drab & 3u) != 0)
+        return fail(MTGR_ERROR_INVALID_ARGUMENT, "drab is not 4-byte aligned");
+    hipStream_t s = (hipStream_t)stream;
+    if (p->num_users == 0 || p->total_tokens == 0) {
+        if (drab) {
+            hipError_t e = mtgr::launch_fill_f32(drab, (long long)p->num_heads * p->num_rab_buckets, 0.f, s);
+            if (e != hipSuccess) return device_fail(e, "drab fill");
+        }
+        return ok();
+    }
+    const bool want_dq = !(p->flags & MTGR_BWD_SKIP_DQ);
+    const bool want_dkdv = !(p->flags & MTGR_BWD_SKIP_DKDV);
+    REQUIRE_PTR(q, "q");
+    REQUIRE_PTR(k, "k");
+    REQUIRE_PTR(v, "v");
+    REQUIRE_PTR(dout, "dout");
+    if (want_dq) REQUIRE_PTR(dq, "dq");
+    if (want_dkdv) {
+        REQUIRE_PTR(dk, "dk");
+        REQUIRE_PTR(dv, "dv");
+    }
+    const AttnLayout L = attn_layout(p);
+    if (!(p->flags & MTGR_ATTN_PLANNED)) {
+        st = schedule(p, L, offsets, seg, ts, workspace, s);
+        if (st != MTGR_SUCCESS) return st;
+    }
+    float* drab_out = want_dq ? drab : nullptr;
+    if (drab_out) {
+        hipError_t e = mtgr::launch_fill_f32(drab_out, (long long)p->num_heads * p->num_rab_buckets, 0.f, s);
+        if (e != hipSuccess) return device_fail(e, "drab fill");
+    }
+    mtgr::AttnArgs a = make_args(p, L, offsets, seg, ts, workspace);
+    a.q = q;
+    a.k = k;
+    a.v = v;
+    a.rab = rab;
+    a.dout = dout;
+    a.dq = dq;
+    a.dk = dk;
+    a.dv = dv;
+    a.drab = drab_out;
+    hipError_t e = p->dtype == MTGR_DTYPE_BF16
+                       ? mtgr::launch_attn_bwd_bf16(a, p->head_dim, (int)L.slots, want_dq, want_dkdv, s)
+                       : mtgr::launch_attn_bwd_f32(a, p->head_dim, (int)L.slots, want_dq, want_dkdv, s);
+    if (e != hipSuccess) return device_fail(e, "attention backward");
+    return ok();
+}
+
+}  // extern "C"
+
+namespace {
+
+mtgr_status_t check_gln(const mtgr_gln_problem_t* p) {
+    if (!p) return fail(MTGR_ERROR_NULL_POINTER, "problem is NULL");
+    if (p->dtype != MTGR_DTYPE_BF16 && p->dtype != MTGR_DTYPE_FP32)
+        return fail(MTGR_ERROR_UNSUPPORTED, "dtype %d is not supported", p->dtype);
+    if (p->num_tokens < 0) return fail(MTGR_ERROR_INVALID_ARGUMENT, "num_tokens < 0");
+    const int vec = p->dtype == MTGR_DTYPE_BF16 ? 8 : 4;
+    const int dmax = p->dtype == MTGR_DTYPE_BF16 ? 4096 : 2048;
+    if (p->dim <= 0 || p->dim % vec != 0)
+        return fail(MTGR_ERROR_INVALID_ARGUMENT, "dim %d must be a positive multiple of %d", p->dim, vec);
+    if (p->dim > dmax) return fail(MTGR_ERROR_UNSUPPORTED, "dim %d above %d", p->dim, dmax);
+    if (p->num_groups < 1 || p->num_groups > MTGR_MAX_GROUPS)
+        return fail(MTGR_ERROR_INVALID_ARGUMENT, "num_groups %d outside 1..%d", p->num_groups,
+                    MTGR_MAX_GROUPS);
+    if (!(p->eps > 0.f) || !std::isfinite(p->eps))
+        return fail(MTGR_ERROR_INVALID_ARGUMENT, "eps must be positive and finite");
+    const int esz = p->dtype == MTGR_DTYPE_BF16 ? 2 : 4;
+    const long long lds[3] = {p->ld_x, p->ld_u, p->ld_y};
+    const char* names[3] = {"ld_x", "ld_u", "ld_y"};
+    for (int i = 0; i < 3; i++) {
+        if (lds[i] < p->dim)
+            return fail(MTGR_ERROR_INVALID_ARGUMENT, "%s %lld below dim %d", names[i], lds[i], p->dim);
+        if ((lds[i] * esz) % 16 != 0)
+            return fail(MTGR_ERROR_INVALID_ARGUMENT, "%s %lld is not a multiple of 16 bytes", names[i],
+                        lds[i]);
+    }
+    return MTGR_SUCCESS;
+}
+
+mtgr::GlnArgs gln_args(const mtgr_gln_problem_t* p) {
+    mtgr::GlnArgs a{};
+    a.T = p->num_tokens;
+    a.d = p->dim;
+    a.G = p->num_groups;
+    a.eps = p->eps;
+    a.ld_x = p->ld_x;
+    a.ld_u = p->ld_u;
+    a.ld_y = p->ld_y;
+    return a;
+}
+
+}  // namespace
+
+extern "C" {
+
+mtgr_status_t mtgr_group_layernorm_workspace_size(const mtgr_gln_problem_t* p, int backward,
+                                                  size_t* bytes) {
+    (void)backward;
+    if (!bytes) return fail(MTGR_ERROR_NULL_POINTER, "bytes is NULL");
+    mtgr_status_t st = check_gln(p);
+    if (st != MTGR_SUCCESS) return st;
+    *bytes = 0;
+    return ok();
+}
+
+mtgr_status_t mtgr_group_layernorm_fwd(const mtgr_gln_problem_t* p, const void* x, const void* u,
+                                       const int8_t* group_ids, const float* gamma, const float* beta,
+                                       void* y, float* mean, float* rstd, mtgr_stream_t stream) {
+    mtgr_status_t st = check_gln(p);
+    if (st != MTGR_SUCCESS) return st;
+    REQUIRE_PTR(gamma, "gamma");
+    REQUIRE_PTR(beta, "beta");
+    if (p->num_tokens == 0) return ok();
+    REQUIRE_PTR(x, "x");
+    REQUIRE_PTR(y, "y");
+    if (u && !aligned16(u)) return fail(MTGR_ERROR_INVALID_ARGUMENT, "u is not 16-byte aligned");
+    if (!group_ids) return fail(MTGR_ERROR_NULL_POINTER, "group_ids is NULL");
+    if ((mean && ((uintptr_t)mean & 3u)) || (rstd && ((uintptr_t)rstd & 3u)))
+        return fail(MTGR_ERROR_INVALID_ARGUMENT, "mean/rstd not 4-byte aligned");
+    mtgr::GlnArgs a = gln_args(p);
+    a.x = x;
+    a.u = u;
+    a.gid = group_ids;
+    a.gamma = gamma;
+    a.beta = beta;
+    a.y = y;
+    a.mean = mean;
+    a.rstd = rstd;
+    hipError_t e = mtgr::launch_gln_fwd(a, p->dtype == MTGR_DTYPE_BF16, (hipStream_t)stream);
+    if (e != hipSuccess) return device_fail(e, "group layernorm forward");
+    return ok();
+}
+
+mtgr_status_t mtgr_group_layernorm_bwd(const mtgr_gln_problem_t* p, const void* dy, const void* x,
+                                       const void* u, const int8_t* group_ids, const float* gamma,
+                                       const float* mean, const float* rstd, void* dx, void* du,
+                                       float* dgamma, float* dbeta, void* workspace,
+                                       size_t workspace_bytes, mtgr_stream_t stream) {
+    (void)workspace;
+    (void)workspace_bytes;
+    mtgr_status_t st = check_gln(p);
+    if (st != MTGR_SUCCESS) return st;
+    REQUIRE_PTR(gamma, "gamma");
+    REQUIRE_PTR(dgamma, "dgamma");
+    REQUIRE_PTR(dbeta, "dbeta");
+    if ((u == nullptr) != (du == nullptr))
+        return fail(MTGR_ERROR_INVALID_ARGUMENT, "du must be given exactly when u is given");
+    if (p->num_tokens > 0) {
+        REQUIRE_PTR(dy, "dy");
+        REQUIRE_PTR(x, "x");
+        REQUIRE_PTR(dx, "dx");
+        if (u) {
+            REQUIRE_PTR(u, "u");
+            REQUIRE_PTR(du, "du");
+        }
+        if (!group_ids) return fail(MTGR_ERROR_NULL_POINTER, "group_ids is NULL");
+        if (!mean) return fail(MTGR_ERROR_NULL_POINTER, "mean is NULL");
+        if (!rstd) return fail(MTGR_ERROR_NULL_POINTER, "rstd is NULL");
+    }
+    mtgr::GlnArgs a = gln_args(p);
+    a.dy = dy;
+    a.x = x;
+    a.u = u;
+    a.gid = group_ids;
+    a.gamma = gamma;
+    a.mean = const_cast<float*>(mean);
+    a.rstd = const_cast<float*>(rstd);
+    a.dx = dx;
+    a.du = du;
+    a.dgamma = dgamma;
+    a.dbeta = dbeta;
+    hipError_t e = mtgr::launch_gln_bwd(a, p->dtype == MTGR_DTYPE_BF16, (hipStream_t)stream);
+    if (e != hipSuccess) return device_fail(e, "group layernorm backward");
+    return ok();
+}
+
+const char* mtgr_status_string(mtgr_status_t status) {
+    switch (status) {
+        case MTGR_SUCCESS: return "success";
+        case MTGR_ERROR_NULL_POINTER: return "null pointer";
+        case MTGR_ERROR_INVALID_ARGUMENT: return "invalid argument";
+        case MTGR_ERROR_UNSUPPORTED: return "unsupported";
+        case MTGR_ERROR_WORKSPACE_TOO_SMALL: return "workspace too small";
+        case MTGR_ERROR_DEVICE: return "device error";
+        default: return "unknown status";
+    }
+}
+
+const char* mtgr_last_error_message(void) { return g_last_error.c_str(); }
+
+int32_t mtgr_version(void) { return MTGR_HSTU_VERSION; }
+
+}  // extern "C"

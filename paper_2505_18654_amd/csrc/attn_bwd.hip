@@ -1,0 +1,717 @@
+// Backward of the jagged dynamic-mask SiLU attention (chain rule of Eq. 5).
+//
+// With s = alpha q_i.k_j + rab, sg = sigmoid(s), p = silu(s)/n_b and dP = dout_i . v_j:
+//     dS_ij = M_ij dP_ij sg (1 + s (1 - sg)) / n_b
+//     dV_j = sum_i M_ij p_ij dout_i,   dK_j = alpha sum_i dS_ij q_i,
+//     dQ_i = alpha sum_j dS_ij k_j,    drab[h, bucket] += dS_ij.
+// There is no softmax, so nothing is saved by the forward and no row statistic is needed.
+//
+// Two kernels, no atomics on dQ/dK/dV (results are deterministic):
+//   dq kernel (row-parallel, like the forward): per wave 32 queries, Q and dO in VGPRs;
+//     per 64-key tile: S^T = K Q^T, dP^T = V dO^T, dS^T in registers, dQ^T += K^T dS^T.
+//     It also forms drab (LDS histogram, one global atomic per bucket per workgroup).
+//   dkdv kernel (column-parallel): per wave 32 keys, K and V in VGPRs; per 64-query tile:
+//     S = Q K^T, dP = dO V^T (lane = key column), then dV += P^T dO and dK += dS^T Q.
+#include "mtgr_device.h"
+#include "mtgr_internal.h"
+
+namespace mtgr {
+
+namespace {
+constexpr int BM = 128;   // rows (queries or keys) per workgroup
+constexpr int BN = 64;    // columns per inner tile
+__device__ __forceinline__ uint4 ldg16(const uint16_t* p) { return *(const uint4*)p; }
+
+__device__ __forceinline__ void zero(floatx16& x) {
+#pragma unroll
+    for (int r = 0; r < 16; r++) x[r] = 0.f;
+}
+
+// 8 bf16 of a transposed LDS row in the k-slot order of the accumulator layout:
+// slots 0..3 = columns c0 + 4hh + 0..3, slots 4..7 = columns c0 + 8 + 4hh + 0..3.
+__device__ __forceinline__ bf16x8 ld_tr8(const uint16_t* row) {
+    const uint2 lo = *(const uint2*)row;
+    const uint2 hi = *(const uint2*)(row + 8);
+    return as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y));
+}
+
+// Stage `rows` x DH bf16 from registers (uint4 chunks) into a row-major LDS tile and its
+// transpose.  reg[i] holds chunk (tid + 256 i) of the row-major tile for the row-major
+// copy; treg[r] holds row (rg * RPT + r), chunk cc for the transposed copy.
+template <int DH, int RPT>
+__device__ __forceinline__ void store_transposed(uint16_t* sT, int TP, const uint4* treg, int cc,
+                                                 int rg) {
+#pragma unroll
+    for (int e = 0; e < 8; e++) {
+        uint16_t vals[RPT];
+#pragma unroll
+        for (int r = 0; r < RPT; r++) {
+            const uint32_t word = ((const uint32_t*)&treg[r])[e >> 1];
+            vals[r] = (uint16_t)(word >> (16 * (e & 1)));
+        }
+        uint16_t* dst = &sT[(cc * 8 + e) * TP + rg * RPT];
+        if constexpr (RPT == 4) {
+            *(uint2*)dst = make_uint2(vals[0] | ((uint32_t)vals[1] << 16),
+                                      vals[2] | ((uint32_t)vals[3] << 16));
+        } else if constexpr (RPT == 2) {
+            *(uint32_t*)dst = vals[0] | ((uint32_t)vals[1] << 16);
+        } else {
+            dst[0] = vals[0];
+        }
+    }
+}
+}  // namespace
+
+// ------------------------------------------------------------------ dQ (+ drab), bf16
+template <int DH, bool RAB>
+__global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
+    constexpr int KP = DH + 8, TP = BN + 4, OP = DH + 8;
+    constexpr int KSTEPS = DH / 16, DBLK = DH / 32, CPR = DH / 8;
+    constexpr int KCH = BN * CPR / 256, RPT = DH / 32;
+    constexpr int KV_BYTES = 2 * BN * KP * 2 + DH * TP * 2;
+    constexpr int O_BYTES = BM * OP * 2;
+    constexpr int BYTES = KV_BYTES > O_BYTES ? KV_BYTES : O_BYTES;
+    __shared__ __align__(16) char smem[BYTES];
+    __shared__ int sKcode[BN];
+    __shared__ int sKts[BN];
+    __shared__ float sRab[MTGR_RAB_LDS];
+    __shared__ float sHist[MTGR_RAB_LDS];
+    uint16_t* sK = (uint16_t*)smem;
+    uint16_t* sV = sK + BN * KP;
+    uint16_t* sKt = sV + BN * KP;
+
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int2 item = a.items[blockIdx.x];
+    if (item.x < 0) return;
+    const int b = item.x, qt = item.y >> 8, h = item.y & 255;
+    const bool want_drab = RAB && a.drab != nullptr;
+    const int ob = a.offsets[b], nb = a.offsets[b + 1] - ob;
+    const int q0 = qt * BM;
+    const int ntk = (nb + BN - 1) / BN;
+    const float inv_n = 1.0f / (float)nb;
+    const float alpha = a.alpha;
+    const int4* summ = a.summ + (long long)b * a.ntile;
+    TileSummary sq = load_summary(summ, 2 * qt);
+    if (2 * qt + 1 < ntk) sq = combine(sq, load_summary(summ, 2 * qt + 1));
+
+    const int col = lane & 31, hh = lane >> 5;
+    const int qi = q0 + w * 32 + col;
+    const bool qvalid = qi < nb;
+    int qcode = 0, qts = 0;
+    if (qvalid) {
+        qcode = token_code(a.seg[ob + qi]);
+        qts = a.ts[ob + qi];
+    }
+    const uint16_t* Q = (const uint16_t*)a.q;
+    const uint16_t* K = (const uint16_t*)a.k;
+    const uint16_t* V = (const uint16_t*)a.v;
+    const uint16_t* DO = (const uint16_t*)a.dout;
+    bf16x8 qreg[KSTEPS], doreg[KSTEPS];
+#pragma unroll
+    for (int kk = 0; kk < KSTEPS; kk++) {
+        uint4 u = make_uint4(0, 0, 0, 0), g = make_uint4(0, 0, 0, 0);
+        if (qvalid) {
+            u = ldg16(Q + (long long)(ob + qi) * a.ld_q + h * DH + 16 * kk + 8 * hh);
+            g = ldg16(DO + (long long)(ob + qi) * a.ld_o + h * DH + 16 * kk + 8 * hh);
+        }
+        qreg[kk] = as_bf16x8(u);
+        doreg[kk] = as_bf16x8(g);
+    }
+    if (RAB && tid < MTGR_RAB_LDS) {
+        sRab[tid] = tid < a.nbuckets ? a.rab[h * a.nbuckets + tid] : 0.f;
+        sHist[tid] = 0.f;
+    }
+    floatx16 dqacc[DBLK];
+#pragma unroll
+    for (int i = 0; i < DBLK; i++) zero(dqacc[i]);
+
+    auto klass = [&](int t) {
+        const bool overlap = (t * BN < q0 + BM) && (q0 < t * BN + BN);
+        return tile_class(sq, load_summary(summ, t), overlap);
+    };
+    auto next_visible = [&](int t) {
+        while (t < ntk && klass(t) == TILE_MASKED) ++t;
+        return t;
+    };
+
+    uint4 kreg[KCH], vreg[KCH], ktreg[RPT];
+    int kcode_reg = 0, kts_reg = 0;
+    const int tcc = tid % CPR, trg = tid / CPR;
+    auto gload = [&](int t) {
+        const int kb = t * BN;
+#pragma unroll
+        for (int i = 0; i < KCH; i++) {
+            const int c = tid + 256 * i, row = c / CPR, cc = c % CPR, key = kb + row;
+            const bool ok = key < nb;
+            kreg[i] = ok ? ldg16(K + (long long)(ob + key) * a.ld_k + h * DH + cc * 8) : make_uint4(0, 0, 0, 0);
+            vreg[i] = ok ? ldg16(V + (long long)(ob + key) * a.ld_v + h * DH + cc * 8) : make_uint4(0, 0, 0, 0);
+        }
+#pragma unroll
+        for (int r = 0; r < RPT; r++) {
+            const int key = kb + trg * RPT + r;
+            ktreg[r] = key < nb ? ldg16(K + (long long)(ob + key) * a.ld_k + h * DH + tcc * 8)
+                                : make_uint4(0, 0, 0, 0);
+        }
+        if (tid < BN) {
+            const int key = kb + tid;
+            kcode_reg = key < nb ? token_code(a.seg[ob + key]) : 0;
+            kts_reg = key < nb ? a.ts[ob + key] : 0;
+        }
+    };
+    auto sstore = [&]() {
+#pragma unroll
+        for (int i = 0; i < KCH; i++) {
+            const int c = tid + 256 * i, row = c / CPR, cc = c % CPR;
+            *(uint4*)&sK[row * KP + cc * 8] = kreg[i];
+            *(uint4*)&sV[row * KP + cc * 8] = vreg[i];
+        }
+        store_transposed<DH, RPT>(sKt, TP, ktreg, tcc, trg);
+        if (tid < BN) {
+            sKcode[tid] = kcode_reg;
+            sKts[tid] = kts_reg;
+        }
+    };
+
+    int t = next_visible(0);
+    if (t < ntk) gload(t);
+    while (t < ntk) {
+        const int cls = klass(t);
+        __syncthreads();
+        sstore();
+        __syncthreads();
+        const int tn = next_visible(t + 1);
+        if (tn < ntk) gload(tn);
+
+        floatx16 sacc[2], dpacc[2];
+        zero(sacc[0]); zero(sacc[1]); zero(dpacc[0]); zero(dpacc[1]);
+#pragma unroll
+        for (int kk = 0; kk < KSTEPS; kk++) {
+#pragma unroll
+            for (int blk = 0; blk < 2; blk++) {
+                const int off = (32 * blk + col) * KP + 16 * kk + 8 * hh;
+                const bf16x8 ka = *(const bf16x8*)&sK[off];
+                const bf16x8 va = *(const bf16x8*)&sV[off];
+                sacc[blk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qreg[kk], sacc[blk], 0, 0, 0);
+                dpacc[blk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, doreg[kk], dpacc[blk], 0, 0, 0);
+            }
+        }
+        uint32_t dsk[4][4];
+#pragma unroll
+        for (int blk = 0; blk < 2; blk++) {
+#pragma unroll
+            for (int r = 0; r < 16; r += 2) {
+                float dv[2];
+#pragma unroll
+                for (int e = 0; e < 2; e++) {
+                    const int rr = r + e;
+                    const int kl = 32 * blk + 8 * (rr >> 2) + 4 * hh + (rr & 3);
+                    float x = sacc[blk][rr] * alpha;
+                    int bk = 0;
+                    if (RAB) {
+                        bk = rab_bucket(qts, sKts[kl], a.nbuckets);
+                        x += sRab[bk];
+                    }
+                    float sg;
+                    silu_sig(x, sg);
+                    float ds = dpacc[blk][rr] * sg * (1.0f + x * (1.0f - sg)) * inv_n;
+                    if (cls == TILE_PARTIAL)
+                        ds = visible(qcode, qts, qi, sKcode[kl], sKts[kl], t * BN + kl) ? ds : 0.f;
+                    else if (!qvalid)
+                        ds = 0.f;
+                    if (want_drab && ds != 0.f) atomicAdd(&sHist[bk], ds);
+                    dv[e] = ds;
+                }
+                dsk[2 * blk + (r >> 3)][(r & 7) >> 1] = pack_bf16x2(dv[0], dv[1]);
+            }
+        }
+#pragma unroll
+        for (int ks = 0; ks < 4; ks++) {
+            const bf16x8 db = as_bf16x8(make_uint4(dsk[ks][0], dsk[ks][1], dsk[ks][2], dsk[ks][3]));
+#pragma unroll
+            for (int d = 0; d < DBLK; d++) {
+                const bf16x8 kt = ld_tr8(&sKt[(32 * d + col) * TP + 16 * ks + 4 * hh]);
+                dqacc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kt, db, dqacc[d], 0, 0, 0);
+            }
+        }
+        t = tn;
+    }
+
+    __syncthreads();
+    if (want_drab && tid < a.nbuckets && sHist[tid] != 0.f) atomicAdd(&a.drab[h * a.nbuckets + tid], sHist[tid]);
+    uint16_t* sO = (uint16_t*)smem;
+#pragma unroll
+    for (int d = 0; d < DBLK; d++) {
+#pragma unroll
+        for (int g = 0; g < 4; g++) {
+            const int dd = 32 * d + 8 * g + 4 * hh;
+            *(uint2*)&sO[(w * 32 + col) * OP + dd] =
+                make_uint2(pack_bf16x2(alpha * dqacc[d][4 * g + 0], alpha * dqacc[d][4 * g + 1]),
+                           pack_bf16x2(alpha * dqacc[d][4 * g + 2], alpha * dqacc[d][4 * g + 3]));
+        }
+    }
+    __syncthreads();
+    uint16_t* DQ = (uint16_t*)a.dq;
+#pragma unroll
+    for (int i = 0; i < 32 * CPR / 64; i++) {
+        const int c = lane + 64 * i, row = c / CPR, cc = c % CPR;
+        const int qr = q0 + w * 32 + row;
+        if (qr < nb)
+            *(uint4*)(DQ + (long long)(ob + qr) * a.ld_q + h * DH + cc * 8) =
+                *(const uint4*)&sO[(w * 32 + row) * OP + cc * 8];
+    }
+}
+
+// ------------------------------------------------------------------ dK, dV, bf16
+template <int DH, bool RAB>
+__global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) {
+    constexpr int QP = DH + 8, TP = BN + 4, OP = DH + 8;
+    constexpr int KSTEPS = DH / 16, DBLK = DH / 32, CPR = DH / 8;
+    constexpr int QCH = BN * CPR / 256, RPT = DH / 32;
+    constexpr int T_BYTES = 2 * BN * QP * 2 + 2 * DH * TP * 2;
+    constexpr int O_BYTES = BM * OP * 2;
+    constexpr int BYTES = T_BYTES > O_BYTES ? T_BYTES : O_BYTES;
+    __shared__ __align__(16) char smem[BYTES];
+    __shared__ int sQcode[BN];
+    __shared__ int sQts[BN];
+    __shared__ float sRab[MTGR_RAB_LDS];
+    uint16_t* sQ = (uint16_t*)smem;
+    uint16_t* sDO = sQ + BN * QP;
+    uint16_t* sQt = sDO + BN * QP;
+    uint16_t* sDOt = sQt + DH * TP;
+
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int2 item = a.items[blockIdx.x];
+    if (item.x < 0) return;
+    const int b = item.x, kt = item.y >> 8, h = item.y & 255;
+    const int ob = a.offsets[b], nb = a.offsets[b + 1] - ob;
+    const int k0 = kt * BM;
+    const int ntq = (nb + BN - 1) / BN;
+    const float inv_n = 1.0f / (float)nb;
+    const float alpha = a.alpha;
+    const int4* summ = a.summ + (long long)b * a.ntile;
+    TileSummary sk = load_summary(summ, 2 * kt);
+    if (2 * kt + 1 < ntq) sk = combine(sk, load_summary(summ, 2 * kt + 1));
+    else sk.flags &= ~TS_ALL_STATIC;   // a lone half tile is never fully visible
+
+    const int col = lane & 31, hh = lane >> 5;
+    const int kj = k0 + w * 32 + col;
+    const bool kvalid = kj < nb;
+    int kcode = 0, kts = 0;
+    if (kvalid) {
+        kcode = token_code(a.seg[ob + kj]);
+        kts = a.ts[ob + kj];
+    }
+    const uint16_t* Q = (const uint16_t*)a.q;
+    const uint16_t* K = (const uint16_t*)a.k;
+    const uint16_t* V = (const uint16_t*)a.v;
+    const uint16_t* DO = (const uint16_t*)a.dout;
+    bf16x8 kreg[KSTEPS], vreg[KSTEPS];
+#pragma unroll
+    for (int kk = 0; kk < KSTEPS; kk++) {
+        uint4 u = make_uint4(0, 0, 0, 0), g = make_uint4(0, 0, 0, 0);
+        if (kvalid) {
+            u = ldg16(K + (long long)(ob + kj) * a.ld_k + h * DH + 16 * kk + 8 * hh);
+            g = ldg16(V + (long long)(ob + kj) * a.ld_v + h * DH + 16 * kk + 8 * hh);
+        }
+        kreg[kk] = as_bf16x8(u);
+        vreg[kk] = as_bf16x8(g);
+    }
+    if (RAB && tid < MTGR_RAB_LDS) sRab[tid] = tid < a.nbuckets ? a.rab[h * a.nbuckets + tid] : 0.f;
+    floatx16 dkacc[DBLK], dvacc[DBLK];
+#pragma unroll
+    for (int i = 0; i < DBLK; i++) {
+        zero(dkacc[i]);
+        zero(dvacc[i]);
+    }
+
+    auto klass = [&](int t) {
+        const bool overlap = (t * BN < k0 + BM) && (k0 < t * BN + BN);
+        return tile_class(load_summary(summ, t), sk, overlap);
+    };
+    auto next_visible = [&](int t) {
+        while (t < ntq && klass(t) == TILE_MASKED) ++t;
+        return t;
+    };
+
+    uint4 qreg[QCH], goreg[QCH], qtreg[RPT], gotreg[RPT];
+    int qcode_reg = 0, qts_reg = 0;
+    const int tcc = tid % CPR, trg = tid / CPR;
+    auto gload = [&](int t) {
+        const int qb = t * BN;
+#pragma unroll
+        for (int i = 0; i < QCH; i++) {
+            const int c = tid + 256 * i, row = c / CPR, cc = c % CPR, qr = qb + row;
+            const bool ok = qr < nb;
+            qreg[i] = ok ? ldg16(Q + (long long)(ob + qr) * a.ld_q + h * DH + cc * 8) : make_uint4(0, 0, 0, 0);
+            goreg[i] = ok ? ldg16(DO + (long long)(ob + qr) * a.ld_o + h * DH + cc * 8) : make_uint4(0, 0, 0, 0);
+        }
+#pragma unroll
+        for (int r = 0; r < RPT; r++) {
+            const int qr = qb + trg * RPT + r;
+            const bool ok = qr < nb;
+            qtreg[r] = ok ? ldg16(Q + (long long)(ob + qr) * a.ld_q + h * DH + tcc * 8) : make_uint4(0, 0, 0, 0);
+            gotreg[r] = ok ? ldg16(DO + (long long)(ob + qr) * a.ld_o + h * DH + tcc * 8) : make_uint4(0, 0, 0, 0);
+        }
+        if (tid < BN) {
+            const int qr = qb + tid;
+            qcode_reg = qr < nb ? token_code(a.seg[ob + qr]) : 0;
+            qts_reg = qr < nb ? a.ts[ob + qr] : 0;
+        }
+    };
+    auto sstore = [&]() {
+#pragma unroll
+        for (int i = 0; i < QCH; i++) {
+            const int c = tid + 256 * i, row = c / CPR, cc = c % CPR;
+            *(uint4*)&sQ[row * QP + cc * 8] = qreg[i];
+            *(uint4*)&sDO[row * QP + cc * 8] = goreg[i];
+        }
+        store_transposed<DH, RPT>(sQt, TP, qtreg, tcc, trg);
+        store_transposed<DH, RPT>(sDOt, TP, gotreg, tcc, trg);
+        if (tid < BN) {
+            sQcode[tid] = qcode_reg;
+            sQts[tid] = qts_reg;
+        }
+    };
+
+    int t = next_visible(0);
+    if (t < ntq) gload(t);
+    while (t < ntq) {
+        const int cls = klass(t);
+        __syncthreads();
+        sstore();
+        __syncthreads();
+        const int tn = next_visible(t + 1);
+        if (tn < ntq) gload(tn);
+
+        // S (64 q x 32 keys) = Q K^T and dP = dO V^T: lane = key column, registers = queries.
+        floatx16 sacc[2], dpacc[2];
+        zero(sacc[0]); zero(sacc[1]); zero(dpacc[0]); zero(dpacc[1]);
+#pragma unroll
+        for (int kk = 0; kk < KSTEPS; kk++) {
+#pragma unroll
+            for (int qb = 0; qb < 2; qb++) {
+                const int off = (32 * qb + col) * QP + 16 * kk + 8 * hh;
+                const bf16x8 qa = *(const bf16x8*)&sQ[off];
+                const bf16x8 ga = *(const bf16x8*)&sDO[off];
+                sacc[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa, kreg[kk], sacc[qb], 0, 0, 0);
+                dpacc[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ga, vreg[kk], dpacc[qb], 0, 0, 0);
+            }
+        }
+        uint32_t pk[4][4], dsk[4][4];
+#pragma unroll
+        for (int qb = 0; qb < 2; qb++) {
+#pragma unroll
+            for (int r = 0; r < 16; r += 2) {
+                float pv[2], dv[2];
+#pragma unroll
+                for (int e = 0; e < 2; e++) {
+                    const int rr = r + e;
+                    const int ql = 32 * qb + 8 * (rr >> 2) + 4 * hh + (rr & 3);
+                    float x = sacc[qb][rr] * alpha;
+                    if (RAB) x += sRab[rab_bucket(sQts[ql], kts, a.nbuckets)];
+                    float sg;
+                    float p = silu_sig(x, sg) * inv_n;
+                    float ds = dpacc[qb][rr] * sg * (1.0f + x * (1.0f - sg)) * inv_n;
+                    if (cls == TILE_PARTIAL) {
+                        const bool vis = visible(sQcode[ql], sQts[ql], t * BN + ql, kcode, kts, kj);
+                        p = vis ? p : 0.f;
+                        ds = vis ? ds : 0.f;
+                    }
+                    pv[e] = p;
+                    dv[e] = ds;
+                }
+                pk[2 * qb + (r >> 3)][(r & 7) >> 1] = pack_bf16x2(pv[0], pv[1]);
+                dsk[2 * qb + (r >> 3)][(r & 7) >> 1] = pack_bf16x2(dv[0], dv[1]);
+            }
+        }
+        // dV (32 keys x dh) += P^T dO ; dK += dS^T Q.  A = P^T / dS^T straight from registers.
+#pragma unroll
+        for (int ks = 0; ks < 4; ks++) {
+            const bf16x8 pa = as_bf16x8(make_uint4(pk[ks][0], pk[ks][1], pk[ks][2], pk[ks][3]));
+            const bf16x8 da = as_bf16x8(make_uint4(dsk[ks][0], dsk[ks][1], dsk[ks][2], dsk[ks][3]));
+#pragma unroll
+            for (int d = 0; d < DBLK; d++) {
+                const bf16x8 gb = ld_tr8(&sDOt[(32 * d + col) * TP + 16 * ks + 4 * hh]);
+                const bf16x8 qbv = ld_tr8(&sQt[(32 * d + col) * TP + 16 * ks + 4 * hh]);
+                dvacc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pa, gb, dvacc[d], 0, 0, 0);
+                dkacc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(da, qbv, dkacc[d], 0, 0, 0);
+            }
+        }
+        t = tn;
+    }
+
+    // dK / dV accumulators: lane = feature column, registers = key rows.
+    uint16_t* sO = (uint16_t*)smem;
+    uint16_t* DK = (uint16_t*)a.dk;
+    uint16_t* DV = (uint16_t*)a.dv;
+#pragma unroll
+    for (int which = 0; which < 2; which++) {
+        __syncthreads();
+#pragma unroll
+        for (int d = 0; d < DBLK; d++) {
+#pragma unroll
+            for (int r = 0; r < 16; r++) {
+                const int krow = w * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
+                const float val = which == 0 ? alpha * dkacc[d][r] : dvacc[d][r];
+                sO[krow * OP + 32 * d + col] = (uint16_t)f32_to_bf16_bits(val);
+            }
+        }
+        __syncthreads();
+        uint16_t* dst = which == 0 ? DK : DV;
+        const long long ld = which == 0 ? a.ld_k : a.ld_v;
+#pragma unroll
+        for (int i = 0; i < 32 * CPR / 64; i++) {
+            const int c = lane + 64 * i, row = c / CPR, cc = c % CPR;
+            const int kr = k0 + w * 32 + row;
+            if (kr < nb)
+                *(uint4*)(dst + (long long)(ob + kr) * ld + h * DH + cc * 8) =
+                    *(const uint4*)&sO[(w * 32 + row) * OP + cc * 8];
+        }
+    }
+}
+
+// ------------------------------------------------------------------ fp32 parity kernels
+// dq kernel: 64 query rows, 4 threads per row (dh/4 features each); keys staged 32 at a time.
+template <int DH, bool RAB>
+__global__ __launch_bounds__(256) void attn_bwd_dq_f32_kernel(AttnArgs a) {
+    constexpr int BMF = 64, SUB = 32, Q4 = DH / 4, KP = DH + 1;
+    __shared__ float sK[SUB * KP];
+    __shared__ float sV[SUB * KP];
+    __shared__ int sKcode[SUB];
+    __shared__ int sKts[SUB];
+    __shared__ float sRab[MTGR_RAB_LDS];
+    __shared__ float sHist[MTGR_RAB_LDS];
+    const int tid = threadIdx.x;
+    const int2 item = a.items[blockIdx.x];
+    if (item.x < 0) return;
+    const int b = item.x, qt = item.y >> 8, h = item.y & 255;
+    const bool want_drab = RAB && a.drab != nullptr;
+    const int ob = a.offsets[b], nb = a.offsets[b + 1] - ob;
+    const int q0 = qt * BMF;
+    const int ntk = (nb + BN - 1) / BN;
+    const float inv_n = 1.0f / (float)nb;
+    const int4* summ = a.summ + (long long)b * a.ntile;
+    const TileSummary sq = load_summary(summ, qt);
+    const int qi = q0 + (tid >> 2), part = tid & 3;
+    const bool qvalid = qi < nb;
+    const float* Q = (const float*)a.q;
+    const float* K = (const float*)a.k;
+    const float* V = (const float*)a.v;
+    const float* DO = (const float*)a.dout;
+    float qv[Q4], gv[Q4], acc[Q4];
+#pragma unroll
+    for (int c = 0; c < Q4; c++) {
+        qv[c] = qvalid ? Q[(long long)(ob + qi) * a.ld_q + h * DH + part * Q4 + c] : 0.f;
+        gv[c] = qvalid ? DO[(long long)(ob + qi) * a.ld_o + h * DH + part * Q4 + c] : 0.f;
+        acc[c] = 0.f;
+    }
+    int qcode = 0, qts = 0;
+    if (qvalid) {
+        qcode = token_code(a.seg[ob + qi]);
+        qts = a.ts[ob + qi];
+    }
+    if (RAB && tid < MTGR_RAB_LDS) {
+        sRab[tid] = tid < a.nbuckets ? a.rab[h * a.nbuckets + tid] : 0.f;
+        sHist[tid] = 0.f;
+    }
+    for (int t = 0; t < ntk; t++) {
+        const bool overlap = (t * BN < q0 + BMF) && (q0 < t * BN + BN);
+        if (tile_class(sq, load_summary(summ, t), overlap) == TILE_MASKED) continue;
+        for (int sub = 0; sub < BN / SUB; sub++) {
+            const int kb = t * BN + sub * SUB;
+            __syncthreads();
+            for (int i = tid; i < SUB * DH; i += 256) {
+                const int row = i / DH, c = i % DH, key = kb + row;
+                sK[row * KP + c] = key < nb ? K[(long long)(ob + key) * a.ld_k + h * DH + c] : 0.f;
+                sV[row * KP + c] = key < nb ? V[(long long)(ob + key) * a.ld_v + h * DH + c] : 0.f;
+            }
+            if (tid < SUB) {
+                const int key = kb + tid;
+                sKcode[tid] = key < nb ? token_code(a.seg[ob + key]) : 0;
+                sKts[tid] = key < nb ? a.ts[ob + key] : 0;
+            }
+            __syncthreads();
+            for (int j = 0; j < SUB; j++) {
+                float s = 0.f, dp = 0.f;
+#pragma unroll
+                for (int c = 0; c < Q4; c++) {
+                    s = fmaf(qv[c], sK[j * KP + part * Q4 + c], s);
+                    dp = fmaf(gv[c], sV[j * KP + part * Q4 + c], dp);
+                }
+                s += __shfl_xor(s, 1, 64);
+                s += __shfl_xor(s, 2, 64);
+                dp += __shfl_xor(dp, 1, 64);
+                dp += __shfl_xor(dp, 2, 64);
+                float x = s * a.alpha;
+                int bk = 0;
+                if (RAB) {
+                    bk = rab_bucket(qts, sKts[j], a.nbuckets);
+                    x += sRab[bk];
+                }
+                const float sg = 1.0f / (1.0f + expf(-x));
+                const float ds = dp * sg * (1.0f + x * (1.0f - sg)) * inv_n;
+                if (visible(qcode, qts, qi, sKcode[j], sKts[j], kb + j)) {
+#pragma unroll
+                    for (int c = 0; c < Q4; c++) acc[c] = fmaf(ds, sK[j * KP + part * Q4 + c], acc[c]);
+                    if (want_drab && part == 0) atomicAdd(&sHist[bk], ds);
+                }
+            }
+        }
+    }
+    __syncthreads();
+    if (want_drab && tid < a.nbuckets && sHist[tid] != 0.f) atomicAdd(&a.drab[h * a.nbuckets + tid], sHist[tid]);
+    if (qvalid) {
+        float* DQ = (float*)a.dq;
+#pragma unroll
+        for (int c = 0; c < Q4; c++)
+            DQ[(long long)(ob + qi) * a.ld_q + h * DH + part * Q4 + c] = a.alpha * acc[c];
+    }
+}
+
+// dkdv kernel: 64 key rows, 4 threads per key; queries staged 32 at a time.
+template <int DH, bool RAB>
+__global__ __launch_bounds__(256) void attn_bwd_dkdv_f32_kernel(AttnArgs a) {
+    constexpr int BMF = 64, SUB = 32, Q4 = DH / 4, KP = DH + 1;
+    __shared__ float sQ[SUB * KP];
+    __shared__ float sG[SUB * KP];
+    __shared__ int sQcode[SUB];
+    __shared__ int sQts[SUB];
+    __shared__ float sRab[MTGR_RAB_LDS];
+    const int tid = threadIdx.x;
+    const int2 item = a.items[blockIdx.x];
+    if (item.x < 0) return;
+    const int b = item.x, kt = item.y >> 8, h = item.y & 255;
+    const int ob = a.offsets[b], nb = a.offsets[b + 1] - ob;
+    const int k0 = kt * BMF;
+    const int ntq = (nb + BN - 1) / BN;
+    const float inv_n = 1.0f / (float)nb;
+    const int4* summ = a.summ + (long long)b * a.ntile;
+    const TileSummary sk = load_summary(summ, kt);
+    const int kj = k0 + (tid >> 2), part = tid & 3;
+    const bool kvalid = kj < nb;
+    const float* Q = (const float*)a.q;
+    const float* K = (const float*)a.k;
+    const float* V = (const float*)a.v;
+    const float* DO = (const float*)a.dout;
+    float kv[Q4], vv[Q4], dk[Q4], dv[Q4];
+#pragma unroll
+    for (int c = 0; c < Q4; c++) {
+        kv[c] = kvalid ? K[(long long)(ob + kj) * a.ld_k + h * DH + part * Q4 + c] : 0.f;
+        vv[c] = kvalid ? V[(long long)(ob + kj) * a.ld_v + h * DH + part * Q4 + c] : 0.f;
+        dk[c] = 0.f;
+        dv[c] = 0.f;
+    }
+    int kcode = 0, kts = 0;
+    if (kvalid) {
+        kcode = token_code(a.seg[ob + kj]);
+        kts = a.ts[ob + kj];
+    }
+    if (RAB && tid < MTGR_RAB_LDS) sRab[tid] = tid < a.nbuckets ? a.rab[h * a.nbuckets + tid] : 0.f;
+    for (int t = 0; t < ntq; t++) {
+        const bool overlap = (t * BN < k0 + BMF) && (k0 < t * BN + BN);
+        if (tile_class(load_summary(summ, t), sk, overlap) == TILE_MASKED) continue;
+        for (int sub = 0; sub < BN / SUB; sub++) {
+            const int qb = t * BN + sub * SUB;
+            __syncthreads();
+            for (int i = tid; i < SUB * DH; i += 256) {
+                const int row = i / DH, c = i % DH, qr = qb + row;
+                sQ[row * KP + c] = qr < nb ? Q[(long long)(ob + qr) * a.ld_q + h * DH + c] : 0.f;
+                sG[row * KP + c] = qr < nb ? DO[(long long)(ob + qr) * a.ld_o + h * DH + c] : 0.f;
+            }
+            if (tid < SUB) {
+                const int qr = qb + tid;
+                sQcode[tid] = qr < nb ? token_code(a.seg[ob + qr]) : 0;
+                sQts[tid] = qr < nb ? a.ts[ob + qr] : 0;
+            }
+            __syncthreads();
+            for (int i = 0; i < SUB; i++) {
+                float s = 0.f, dp = 0.f;
+#pragma unroll
+                for (int c = 0; c < Q4; c++) {
+                    s = fmaf(sQ[i * KP + part * Q4 + c], kv[c], s);
+                    dp = fmaf(sG[i * KP + part * Q4 + c], vv[c], dp);
+                }
+                s += __shfl_xor(s, 1, 64);
+                s += __shfl_xor(s, 2, 64);
+                dp += __shfl_xor(dp, 1, 64);
+                dp += __shfl_xor(dp, 2, 64);
+                float x = s * a.alpha;
+                if (RAB) x += sRab[rab_bucket(sQts[i], kts, a.nbuckets)];
+                const float sg = 1.0f / (1.0f + expf(-x));
+                const float p = x * sg * inv_n;
+                const float ds = dp * sg * (1.0f + x * (1.0f - sg)) * inv_n;
+                if (visible(sQcode[i], sQts[i], qb + i, kcode, kts, kj)) {
+#pragma unroll
+                    for (int c = 0; c < Q4; c++) {
+                        dv[c] = fmaf(p, sG[i * KP + part * Q4 + c], dv[c]);
+                        dk[c] = fmaf(ds, sQ[i * KP + part * Q4 + c], dk[c]);
+                    }
+                }
+            }
+        }
+    }
+    if (kvalid) {
+        float* DK = (float*)a.dk;
+        float* DV = (float*)a.dv;
+#pragma unroll
+        for (int c = 0; c < Q4; c++) {
+            DK[(long long)(ob + kj) * a.ld_k + h * DH + part * Q4 + c] = a.alpha * dk[c];
+            DV[(long long)(ob + kj) * a.ld_v + h * DH + part * Q4 + c] = dv[c];
+        }
+    }
+}
+
+// The relative bias enters the scores of both kernels (RAB_IN); drab is formed by the dq
+// kernel only when the caller asked for it (a.drab != nullptr).
+template <int DH, bool RAB_IN>
+static hipError_t bwd_bf16_dh(const AttnArgs& a, int slots, bool dq, bool dkdv, hipStream_t s) {
+    if (dq) {
+        attn_bwd_dq_bf16_kernel<DH, RAB_IN><<<slots, 256, 0, s>>>(a);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    if (dkdv) {
+        attn_bwd_dkdv_bf16_kernel<DH, RAB_IN><<<slots, 256, 0, s>>>(a);
+        return hipGetLastError();
+    }
+    return hipSuccess;
+}
+
+template <int DH, bool RAB_IN>
+static hipError_t bwd_f32_dh(const AttnArgs& a, int slots, bool dq, bool dkdv, hipStream_t s) {
+    if (dq) {
+        attn_bwd_dq_f32_kernel<DH, RAB_IN><<<slots, 256, 0, s>>>(a);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    if (dkdv) {
+        attn_bwd_dkdv_f32_kernel<DH, RAB_IN><<<slots, 256, 0, s>>>(a);
+        return hipGetLastError();
+    }
+    return hipSuccess;
+}
+
+hipError_t launch_attn_bwd_bf16(const AttnArgs& a, int head_dim, int slots, bool dq, bool dkdv,
+                                hipStream_t s) {
+    const bool rab = a.rab != nullptr;
+    switch (head_dim) {
+        case 32: return rab ? bwd_bf16_dh<32, true>(a, slots, dq, dkdv, s) : bwd_bf16_dh<32, false>(a, slots, dq, dkdv, s);
+        case 64: return rab ? bwd_bf16_dh<64, true>(a, slots, dq, dkdv, s) : bwd_bf16_dh<64, false>(a, slots, dq, dkdv, s);
+        case 128: return rab ? bwd_bf16_dh<128, true>(a, slots, dq, dkdv, s) : bwd_bf16_dh<128, false>(a, slots, dq, dkdv, s);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+hipError_t launch_attn_bwd_f32(const AttnArgs& a, int head_dim, int slots, bool dq, bool dkdv,
+                               hipStream_t s) {
+    const bool rab = a.rab != nullptr;
+    switch (head_dim) {
+        case 16: return rab ? bwd_f32_dh<16, true>(a, slots, dq, dkdv, s) : bwd_f32_dh<16, false>(a, slots, dq, dkdv, s);
+        case 32: return rab ? bwd_f32_dh<32, true>(a, slots, dq, dkdv, s) : bwd_f32_dh<32, false>(a, slots, dq, dkdv, s);
+        case 64: return rab ? bwd_f32_dh<64, true>(a, slots, dq, dkdv, s) : bwd_f32_dh<64, false>(a, slots, dq, dkdv, s);
+        case 128: return rab ? bwd_f32_dh<128, true>(a, slots, dq, dkdv, s) : bwd_f32_dh<128, false>(a, slots, dq, dkdv, s);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace mtgr

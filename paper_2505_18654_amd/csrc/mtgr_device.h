@@ -1,0 +1,147 @@
+// Internal device-side helpers for the gfx950 kernels (not part of the ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#define MTGR_RAB_LDS 64   // relative-bias buckets held in LDS (the ABI maximum)
+
+namespace mtgr {
+
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
+typedef __attribute__((__vector_size__(4 * sizeof(__bf16)))) __bf16 bf16x4;
+typedef __attribute__((__vector_size__(16 * sizeof(float)))) float floatx16;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float floatx4;
+
+constexpr int SEG_USER = 0, SEG_HIST = 1, SEG_RT = 2, SEG_CAND = 3;
+
+// Per-64-token tile summary flags (relative to one user's tokens).
+constexpr int TS_ANY_STATIC = 1;   // some valid token is USER/HIST
+constexpr int TS_ALL_STATIC = 2;   // all 64 slots are valid USER/HIST tokens
+constexpr int TS_ANY_RT = 4;       // some valid token is RT
+constexpr int TS_ANY_DYN = 8;      // some valid token is RT or CAND
+constexpr int SUMMARY_TILE = 64;
+
+// Tile classes of a (query range, key range) pair.
+constexpr int TILE_MASKED = 0, TILE_PARTIAL = 1, TILE_FULL = 2;
+
+struct TileSummary {
+    int flags;
+    int min_rt_ts;    // min ts over RT tokens (INT_MAX if none)
+    int max_dyn_ts;   // max ts over RT/CAND tokens (INT_MIN if none)
+    int pad;
+};
+
+__device__ __forceinline__ TileSummary combine(TileSummary a, TileSummary b) {
+    TileSummary r;
+    r.flags = ((a.flags | b.flags) & ~TS_ALL_STATIC) | (a.flags & b.flags & TS_ALL_STATIC);
+    r.min_rt_ts = min(a.min_rt_ts, b.min_rt_ts);
+    r.max_dyn_ts = max(a.max_dyn_ts, b.max_dyn_ts);
+    r.pad = 0;
+    return r;
+}
+
+__device__ __forceinline__ TileSummary empty_summary() {
+    TileSummary r;
+    r.flags = TS_ALL_STATIC;  // neutral for combine()
+    r.min_rt_ts = 0x7fffffff;
+    r.max_dyn_ts = (int)0x80000000;
+    r.pad = 0;
+    return r;
+}
+
+__device__ __forceinline__ TileSummary load_summary(const int4* s, int idx) {
+    int4 v = s[idx];
+    TileSummary r;
+    r.flags = v.x;
+    r.min_rt_ts = v.y;
+    r.max_dyn_ts = v.z;
+    r.pad = 0;
+    return r;
+}
+
+// Class of the pair (queries summarised by sq, keys summarised by sk).  `overlap`
+// says whether the two token ranges intersect (the diagonal i == j is always seen).
+__device__ __forceinline__ int tile_class(TileSummary sq, TileSummary sk, bool overlap) {
+    if (sk.flags & TS_ALL_STATIC) return TILE_FULL;
+    if (sk.flags & TS_ANY_STATIC) return TILE_PARTIAL;
+    if ((sk.flags & TS_ANY_RT) && (sq.flags & TS_ANY_DYN) && sk.min_rt_ts < sq.max_dyn_ts)
+        return TILE_PARTIAL;
+    return overlap ? TILE_PARTIAL : TILE_MASKED;
+}
+
+// Per-token mask code: bit0 static, bit1 real-time, bit2 dynamic (RT or CAND), bit3 valid.
+constexpr int KC_STATIC = 1, KC_RT = 2, KC_DYN = 4, KC_VALID = 8;
+
+__device__ __forceinline__ int token_code(int seg) {
+    int c = KC_VALID;
+    if (seg <= SEG_HIST) c |= KC_STATIC;
+    if (seg == SEG_RT) c |= KC_RT;
+    if (seg >= SEG_RT) c |= KC_DYN;
+    return c;
+}
+
+// Dynamic mask of Sec. 4.2 from token codes: i == j, static key (rule 1), or an RT key
+// strictly earlier than a dynamic query (rule 2); candidates only see themselves (rule 3).
+__device__ __forceinline__ bool visible(int qcode, int qts, int qidx, int kcode, int kts,
+                                        int kidx) {
+    bool v = (kcode & KC_STATIC) || (qidx == kidx) ||
+             ((kcode & KC_RT) && (qcode & KC_DYN) && kts < qts);
+    return v && (kcode & KC_VALID) && (qcode & KC_VALID);
+}
+
+// Half-octave log-time bucket of |a - b| (gap as uint32), clamped to nb - 1.
+__device__ __forceinline__ int rab_bucket(int a, int b, int nb) {
+    uint32_t g = a >= b ? (uint32_t)a - (uint32_t)b : (uint32_t)b - (uint32_t)a;
+    int bk;
+    if (g < 2u) {
+        bk = (int)g;
+    } else {
+        int e = 31 - __clz(g);
+        bk = 2 * e + (int)((g >> (e - 1)) & 1u);
+    }
+    return min(bk, nb - 1);
+}
+
+__device__ __forceinline__ float silu_sig(float x, float& sg) {
+    sg = __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-1.4426950408889634f * x));
+    return x * sg;
+}
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) {
+    return __uint_as_float(((uint32_t)h) << 16);
+}
+
+// fp32 -> bf16 bits, round to nearest even (inputs here are finite or inf).
+__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;  // quiet NaN
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return u >> 16;
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    return f32_to_bf16_bits(lo) | (f32_to_bf16_bits(hi) << 16);
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
+    return v;
+}
+
+__device__ __forceinline__ int wave_min(int v) {
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) v = min(v, __shfl_xor(v, off, 64));
+    return v;
+}
+
+__device__ __forceinline__ int wave_max(int v) {
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) v = max(v, __shfl_xor(v, off, 64));
+    return v;
+}
+
+__device__ __forceinline__ bf16x8 as_bf16x8(uint4 u) { return __builtin_bit_cast(bf16x8, u); }
+
+}  // namespace mtgr

@@ -1,0 +1,80 @@
+// Host-side internal declarations shared by the C-ABI layer and the kernel files.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace mtgr {
+
+// Arguments of every attention kernel (one struct, passed by value).
+struct AttnArgs {
+    const int* offsets;
+    const int8_t* seg;
+    const int* ts;
+    const void* q;
+    const void* k;
+    const void* v;
+    const float* rab;
+    const void* dout;
+    void* out;
+    void* dq;
+    void* dk;
+    void* dv;
+    float* drab;
+    long long ld_q, ld_k, ld_v, ld_o;
+    const int4* summ;     // [B][ntile] per-64-token tile summaries
+    const int2* items;    // work list: {user, (tile << 8) | head}, user < 0 = empty slot
+    int ntile;
+    int heads;
+    float alpha;
+    int nbuckets;
+};
+
+// Number of physical work-list slots for tiles of `bm` rows (see build_schedule).
+long long schedule_slots(long long total_tokens, int num_users, int max_seqlen, int heads, int bm);
+
+// Launchers; each returns the hipError_t of its launch.
+hipError_t launch_tile_summaries(const int* offsets, const int8_t* seg, const int* ts, int num_users,
+                                 int ntile, int4* summ, hipStream_t s);
+hipError_t launch_build_schedule(const int* offsets, int num_users, int heads, int bm, int2* items,
+                                 int slots, int* sorted_users, hipStream_t s);
+hipError_t launch_fill_f32(float* p, long long n, float value, hipStream_t s);
+
+hipError_t launch_attn_fwd_bf16(const AttnArgs& a, int head_dim, int slots, hipStream_t s);
+hipError_t launch_attn_fwd_f32(const AttnArgs& a, int head_dim, int slots, hipStream_t s);
+hipError_t launch_attn_bwd_bf16(const AttnArgs& a, int head_dim, int slots, bool dq, bool dkdv,
+                                hipStream_t s);
+hipError_t launch_attn_bwd_f32(const AttnArgs& a, int head_dim, int slots, bool dq, bool dkdv,
+                               hipStream_t s);
+
+struct GlnArgs {
+    long long T;
+    int d;
+    int G;
+    float eps;
+    long long ld_x, ld_u, ld_y;
+    const void* x;
+    const void* u;
+    const int8_t* gid;
+    const float* gamma;
+    const float* beta;
+    void* y;
+    float* mean;
+    float* rstd;
+    const void* dy;
+    void* dx;
+    void* du;
+    float* dgamma;
+    float* dbeta;
+};
+
+hipError_t launch_gln_fwd(const GlnArgs& a, bool bf16, hipStream_t s);
+hipError_t launch_gln_bwd(const GlnArgs& a, bool bf16, hipStream_t s);
+
+constexpr int ATTN_TILE_BF16 = 128;   // query / key rows per work item, bf16 kernels
+constexpr int ATTN_TILE_F32 = 64;     // rows per work item, fp32 kernels
+constexpr int SCHED_BUCKETS = 4096;   // length buckets of the heavy-first sort
+constexpr int XCDS = 8;               // accelerator complex dies of an MI355X
+
+}  // namespace mtgr

@@ -1,0 +1,202 @@
+"""ctypes binding of libmtgr_hstu.so: the C entry points under the same names.
+
+Argument marshalling only.  Every computation runs in the HIP kernels of the
+library; torch is used for device buffers and the current stream.  Importing
+this module does not need a GPU, but loading fails loudly (MtgrLibraryMissing)
+when the library has not been built: there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libmtgr_hstu.so")
+
+MTGR_SUCCESS = 0
+MTGR_ERROR_NULL_POINTER = 1
+MTGR_ERROR_INVALID_ARGUMENT = 2
+MTGR_ERROR_UNSUPPORTED = 3
+MTGR_ERROR_WORKSPACE_TOO_SMALL = 4
+MTGR_ERROR_DEVICE = 5
+MTGR_DTYPE_BF16 = 0
+MTGR_DTYPE_FP32 = 1
+MTGR_SEG_USER, MTGR_SEG_HIST, MTGR_SEG_RT, MTGR_SEG_CAND = 0, 1, 2, 3
+MTGR_MAX_RAB_BUCKETS = 64
+MTGR_ATTN_PLANNED = 1
+MTGR_BWD_SKIP_DQ = 2
+MTGR_BWD_SKIP_DKDV = 4
+
+EXPORTED = (
+    "mtgr_hstu_attn_workspace_size", "mtgr_hstu_attn_plan", "mtgr_hstu_attn_fwd", "mtgr_hstu_attn_bwd",
+    "mtgr_group_layernorm_workspace_size", "mtgr_group_layernorm_fwd", "mtgr_group_layernorm_bwd",
+    "mtgr_status_string", "mtgr_last_error_message", "mtgr_version",
+)
+
+
+class MtgrLibraryMissing(RuntimeError):
+    pass
+
+
+class MtgrError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{message} (status {status})")
+        self.status = status
+
+
+class HstuProblem(ctypes.Structure):
+    _fields_ = [
+        ("num_users", ctypes.c_int32), ("max_seqlen", ctypes.c_int32),
+        ("total_tokens", ctypes.c_int64), ("num_heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32), ("dtype", ctypes.c_int32), ("alpha", ctypes.c_float),
+        ("num_rab_buckets", ctypes.c_int32), ("flags", ctypes.c_uint32),
+        ("ld_q", ctypes.c_int64), ("ld_k", ctypes.c_int64), ("ld_v", ctypes.c_int64),
+        ("ld_o", ctypes.c_int64),
+    ]
+
+
+class GlnProblem(ctypes.Structure):
+    _fields_ = [
+        ("num_tokens", ctypes.c_int64), ("dim", ctypes.c_int32), ("num_groups", ctypes.c_int32),
+        ("dtype", ctypes.c_int32), ("eps", ctypes.c_float),
+        ("ld_x", ctypes.c_int64), ("ld_u", ctypes.c_int64), ("ld_y", ctypes.c_int64),
+    ]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise MtgrLibraryMissing(
+                f"{LIB_PATH} is not built; run `python -m paper_2505_18654_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, sz, i32 = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int32
+        P = ctypes.POINTER(HstuProblem)
+        G = ctypes.POINTER(GlnProblem)
+        L.mtgr_hstu_attn_workspace_size.argtypes = [P, ctypes.c_int, ctypes.POINTER(sz)]
+        L.mtgr_hstu_attn_plan.argtypes = [P, vp, vp, vp, vp, sz, vp]
+        L.mtgr_hstu_attn_fwd.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.mtgr_hstu_attn_bwd.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.mtgr_group_layernorm_workspace_size.argtypes = [G, ctypes.c_int, ctypes.POINTER(sz)]
+        L.mtgr_group_layernorm_fwd.argtypes = [G, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+        L.mtgr_group_layernorm_bwd.argtypes = [G, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        for name in ("mtgr_hstu_attn_workspace_size", "mtgr_hstu_attn_plan", "mtgr_hstu_attn_fwd",
+                     "mtgr_hstu_attn_bwd",
+                     "mtgr_group_layernorm_workspace_size", "mtgr_group_layernorm_fwd",
+                     "mtgr_group_layernorm_bwd"):
+            getattr(L, name).restype = ctypes.c_int
+        L.mtgr_status_string.argtypes = [ctypes.c_int]
+        L.mtgr_status_string.restype = ctypes.c_char_p
+        L.mtgr_last_error_message.argtypes = []
+        L.mtgr_last_error_message.restype = ctypes.c_char_p
+        L.mtgr_version.argtypes = []
+        L.mtgr_version.restype = i32
+        _lib = L
+    return _lib
+
+
+def _check(status: int) -> None:
+    if status != MTGR_SUCCESS:
+        msg = lib().mtgr_last_error_message().decode()
+        kind = lib().mtgr_status_string(status).decode()
+        raise MtgrError(status, f"{kind}: {msg}")
+
+
+def _ptr(x) -> Optional[int]:
+    """Device (or host) address of a tensor, an int address, or None."""
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return x.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+# ------------------------------------------------------------------ raw entry points
+
+def mtgr_version() -> int:
+    return int(lib().mtgr_version())
+
+
+def mtgr_status_string(status: int) -> str:
+    return lib().mtgr_status_string(status).decode()
+
+
+def mtgr_last_error_message() -> str:
+    return lib().mtgr_last_error_message().decode()
+
+
+def mtgr_hstu_attn_workspace_size(problem: HstuProblem, backward: bool = False) -> int:
+    out = ctypes.c_size_t(0)
+    _check(lib().mtgr_hstu_attn_workspace_size(ctypes.byref(problem), int(backward), ctypes.byref(out)))
+    return int(out.value)
+
+
+def mtgr_hstu_attn_plan(problem, offsets, seg, ts, workspace, workspace_bytes, stream=None) -> None:
+    _check(lib().mtgr_hstu_attn_plan(ctypes.byref(problem), _ptr(offsets), _ptr(seg), _ptr(ts),
+                                     _ptr(workspace), int(workspace_bytes), _stream(stream)))
+
+
+def mtgr_hstu_attn_fwd(problem, offsets, seg, ts, q, k, v, rab, out, workspace, workspace_bytes,
+                       stream=None) -> None:
+    _check(lib().mtgr_hstu_attn_fwd(ctypes.byref(problem), _ptr(offsets), _ptr(seg), _ptr(ts),
+                                    _ptr(q), _ptr(k), _ptr(v), _ptr(rab), _ptr(out), _ptr(workspace),
+                                    int(workspace_bytes), _stream(stream)))
+
+
+def mtgr_hstu_attn_bwd(problem, offsets, seg, ts, q, k, v, rab, dout, dq, dk, dv, drab, workspace,
+                       workspace_bytes, stream=None) -> None:
+    _check(lib().mtgr_hstu_attn_bwd(ctypes.byref(problem), _ptr(offsets), _ptr(seg), _ptr(ts),
+                                    _ptr(q), _ptr(k), _ptr(v), _ptr(rab), _ptr(dout), _ptr(dq),
+                                    _ptr(dk), _ptr(dv), _ptr(drab), _ptr(workspace),
+                                    int(workspace_bytes), _stream(stream)))
+
+
+def mtgr_group_layernorm_workspace_size(problem: GlnProblem, backward: bool = False) -> int:
+    out = ctypes.c_size_t(0)
+    _check(lib().mtgr_group_layernorm_workspace_size(ctypes.byref(problem), int(backward),
+                                                     ctypes.byref(out)))
+    return int(out.value)
+
+
+def mtgr_group_layernorm_fwd(problem, x, u, group_ids, gamma, beta, y, mean, rstd, stream=None) -> None:
+    _check(lib().mtgr_group_layernorm_fwd(ctypes.byref(problem), _ptr(x), _ptr(u), _ptr(group_ids),
+                                          _ptr(gamma), _ptr(beta), _ptr(y), _ptr(mean), _ptr(rstd),
+                                          _stream(stream)))
+
+
+def mtgr_group_layernorm_bwd(problem, dy, x, u, group_ids, gamma, mean, rstd, dx, du, dgamma, dbeta,
+                             workspace=None, workspace_bytes=0, stream=None) -> None:
+    _check(lib().mtgr_group_layernorm_bwd(ctypes.byref(problem), _ptr(dy), _ptr(x), _ptr(u),
+                                          _ptr(group_ids), _ptr(gamma), _ptr(mean), _ptr(rstd),
+                                          _ptr(dx), _ptr(du), _ptr(dgamma), _ptr(dbeta),
+                                          _ptr(workspace), int(workspace_bytes), _stream(stream)))
+
+
+# ------------------------------------------------------------------ problem builders
+
+def attn_problem(num_users: int, total_tokens: int, max_seqlen: int, heads: int, head_dim: int,
+                 dtype: int = MTGR_DTYPE_BF16, alpha: float = 1.0, rab_buckets: int = 0,
+                 ld_q: Optional[int] = None, ld_k: Optional[int] = None, ld_v: Optional[int] = None,
+                 ld_o: Optional[int] = None, flags: int = 0) -> HstuProblem:
+    row = heads * head_dim
+    return HstuProblem(num_users, max_seqlen, total_tokens, heads, head_dim, dtype, alpha, rab_buckets,
+                       flags, ld_q or row, ld_k or row, ld_v or row, ld_o or row)
+
+
+def gln_problem(num_tokens: int, dim: int, groups: int, dtype: int = MTGR_DTYPE_BF16,
+                eps: float = 1e-5, ld_x: Optional[int] = None, ld_u: Optional[int] = None,
+                ld_y: Optional[int] = None) -> GlnProblem:
+    return GlnProblem(num_tokens, dim, groups, dtype, eps, ld_x or dim, ld_u or dim, ld_y or dim)

@@ -113,10 +113,12 @@ class Layout:
             lens.append(sl.stop - sl.start)
         off = np.zeros(len(users) + 1, np.int64)
         off[1:] = np.cumsum(lens)
+        base = self.extra.get("users")           # compose with an earlier subset
+        orig = [base[u] for u in users] if base is not None else users
         return Layout(self.spec, off,
                       np.concatenate(segs) if segs else np.zeros(0, np.int8),
                       np.concatenate(tss) if tss else np.zeros(0, np.int32),
-                      self.counts[users], dict(self.extra, users=users))
+                      self.counts[users], dict(self.extra, users=orig))
 
 
 def make_layout(config: str, seed: Optional[int] = None) -> Layout:

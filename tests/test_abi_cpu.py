@@ -1,0 +1,194 @@
+"""The C ABI on the CPU: the library loads, exports every declared symbol, and rejects
+bad arguments with a status before touching the device (CPU only, no GPU calls)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2505_18654_amd import hstu
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "mtgr_hstu.h")
+
+BF16, FP32 = hstu.MTGR_DTYPE_BF16, hstu.MTGR_DTYPE_FP32
+FAKE = 0x7f0000000000           # 256-byte aligned non-NULL address, never dereferenced
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(mtgr_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function():
+    names = declared_functions()
+    assert "mtgr_hstu_attn_fwd" in names and "mtgr_group_layernorm_bwd" in names
+    L = hstu.lib()
+    for n in names:
+        assert hasattr(L, n), n
+    assert set(names) == set(hstu.EXPORTED)
+
+
+def test_version_and_status_strings():
+    assert hstu.mtgr_version() == 100
+    for s in range(6):
+        assert hstu.mtgr_status_string(s)
+    assert hstu.mtgr_status_string(99) == "unknown status"
+
+
+def test_struct_layout_matches_header():
+    assert ctypes.sizeof(hstu.HstuProblem) == 72
+    assert ctypes.sizeof(hstu.GlnProblem) == 48
+    assert hstu.HstuProblem.ld_q.offset == 40
+
+
+def prob(**kw):
+    base = dict(num_users=4, total_tokens=100, max_seqlen=40, heads=2, head_dim=64, dtype=BF16)
+    base.update(kw)
+    return hstu.attn_problem(**base)
+
+
+@pytest.mark.parametrize("mutate,status", [
+    (dict(head_dim=48), hstu.MTGR_ERROR_UNSUPPORTED),
+    (dict(head_dim=16), hstu.MTGR_ERROR_UNSUPPORTED),          # bf16 supports 32/64/128
+    (dict(dtype=7), hstu.MTGR_ERROR_UNSUPPORTED),
+    (dict(heads=0), hstu.MTGR_ERROR_INVALID_ARGUMENT),
+    (dict(heads=256), hstu.MTGR_ERROR_INVALID_ARGUMENT),
+    (dict(num_users=-1), hstu.MTGR_ERROR_INVALID_ARGUMENT),
+    (dict(total_tokens=-5), hstu.MTGR_ERROR_INVALID_ARGUMENT),
+    (dict(total_tokens=2**31), hstu.MTGR_ERROR_INVALID_ARGUMENT),
+    (dict(max_seqlen=0), hstu.MTGR_ERROR_INVALID_ARGUMENT),
+    (dict(max_seqlen=300000), hstu.MTGR_ERROR_UNSUPPORTED),
+    (dict(rab_buckets=65), hstu.MTGR_ERROR_INVALID_ARGUMENT),
+    (dict(ld_q=100), hstu.MTGR_ERROR_INVALID_ARGUMENT),        # below H*dh = 128
+    (dict(ld_k=132), hstu.MTGR_ERROR_INVALID_ARGUMENT),        # 264 bytes: not 16-byte multiple
+    (dict(alpha=float("nan")), hstu.MTGR_ERROR_INVALID_ARGUMENT),
+])
+def test_problem_validation(mutate, status):
+    p = prob(**mutate)
+    with pytest.raises(hstu.MtgrError) as e:
+        hstu.mtgr_hstu_attn_workspace_size(p)
+    assert e.value.status == status
+    assert hstu.mtgr_last_error_message()
+
+
+def test_unknown_flags_rejected():
+    p = prob()
+    p.flags = 8
+    with pytest.raises(hstu.MtgrError) as e:
+        hstu.mtgr_hstu_attn_workspace_size(p)
+    assert e.value.status == hstu.MTGR_ERROR_INVALID_ARGUMENT
+
+
+def test_fp32_supports_head_dim_16():
+    assert hstu.mtgr_hstu_attn_workspace_size(prob(dtype=FP32, head_dim=16)) > 0
+
+
+def test_workspace_grows_with_problem():
+    a = hstu.mtgr_hstu_attn_workspace_size(prob())
+    b = hstu.mtgr_hstu_attn_workspace_size(prob(num_users=40, total_tokens=1000))
+    assert 0 < a < b
+    assert a % 256 == 0
+    assert hstu.mtgr_hstu_attn_workspace_size(prob(num_users=0, total_tokens=0)) == 0
+
+
+def fwd(p, **over):
+    args = dict(offsets=FAKE, seg=FAKE, ts=FAKE, q=FAKE, k=FAKE, v=FAKE, rab=None, out=FAKE,
+                workspace=FAKE, workspace_bytes=1 << 30)
+    args.update(over)
+    hstu.mtgr_hstu_attn_fwd(p, args["offsets"], args["seg"], args["ts"], args["q"], args["k"],
+                            args["v"], args["rab"], args["out"], args["workspace"],
+                            args["workspace_bytes"], 0)
+
+
+@pytest.mark.parametrize("name", ["offsets", "seg", "ts", "q", "k", "v", "out", "workspace"])
+def test_fwd_null_pointers(name):
+    with pytest.raises(hstu.MtgrError) as e:
+        fwd(prob(), **{name: None})
+    assert e.value.status == hstu.MTGR_ERROR_NULL_POINTER
+    assert name in hstu.mtgr_last_error_message()
+
+
+@pytest.mark.parametrize("name", ["q", "k", "v", "out"])
+def test_fwd_misaligned_tensors(name):
+    with pytest.raises(hstu.MtgrError) as e:
+        fwd(prob(), **{name: FAKE + 2})
+    assert e.value.status == hstu.MTGR_ERROR_INVALID_ARGUMENT
+
+
+def test_fwd_workspace_checks():
+    p = prob()
+    need = hstu.mtgr_hstu_attn_workspace_size(p)
+    with pytest.raises(hstu.MtgrError) as e:
+        fwd(p, workspace_bytes=need - 1)
+    assert e.value.status == hstu.MTGR_ERROR_WORKSPACE_TOO_SMALL
+    with pytest.raises(hstu.MtgrError) as e:
+        fwd(p, workspace=FAKE + 16)
+    assert e.value.status == hstu.MTGR_ERROR_INVALID_ARGUMENT
+
+
+def test_fwd_rab_without_buckets():
+    with pytest.raises(hstu.MtgrError) as e:
+        fwd(prob(), rab=FAKE)
+    assert e.value.status == hstu.MTGR_ERROR_INVALID_ARGUMENT
+
+
+def test_empty_batches_are_noops():
+    for p in (prob(num_users=0, total_tokens=0), prob(num_users=3, total_tokens=0)):
+        fwd(p, offsets=FAKE, seg=None, ts=None, q=None, k=None, v=None, out=None, workspace=None,
+            workspace_bytes=0)
+        hstu.mtgr_hstu_attn_bwd(p, FAKE, None, None, None, None, None, None, None, None, None, None,
+                                None, None, 0, 0)
+
+
+def test_bwd_argument_checks():
+    p = prob(rab_buckets=64)
+    args = [FAKE] * 12
+    with pytest.raises(hstu.MtgrError) as e:       # drab without rab
+        hstu.mtgr_hstu_attn_bwd(p, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE, FAKE,
+                                FAKE, FAKE, 1 << 30, 0)
+    assert e.value.status == hstu.MTGR_ERROR_INVALID_ARGUMENT
+    with pytest.raises(hstu.MtgrError) as e:       # missing dout
+        hstu.mtgr_hstu_attn_bwd(p, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE,
+                                FAKE, FAKE, 1 << 30, 0)
+    assert e.value.status == hstu.MTGR_ERROR_NULL_POINTER
+    assert len(args) == 12
+
+
+@pytest.mark.parametrize("mutate,status", [
+    (dict(dim=12), hstu.MTGR_ERROR_INVALID_ARGUMENT),          # bf16 needs multiples of 8
+    (dict(dim=8192), hstu.MTGR_ERROR_UNSUPPORTED),
+    (dict(groups=0), hstu.MTGR_ERROR_INVALID_ARGUMENT),
+    (dict(groups=128), hstu.MTGR_ERROR_INVALID_ARGUMENT),
+    (dict(eps=0.0), hstu.MTGR_ERROR_INVALID_ARGUMENT),
+    (dict(ld_x=8), hstu.MTGR_ERROR_INVALID_ARGUMENT),
+    (dict(dtype=3), hstu.MTGR_ERROR_UNSUPPORTED),
+    (dict(num_tokens=-1), hstu.MTGR_ERROR_INVALID_ARGUMENT),
+])
+def test_gln_validation(mutate, status):
+    base = dict(num_tokens=10, dim=64, groups=4, dtype=BF16)
+    base.update(mutate)
+    p = hstu.gln_problem(**base)
+    with pytest.raises(hstu.MtgrError) as e:
+        hstu.mtgr_group_layernorm_workspace_size(p)
+    assert e.value.status == status
+
+
+def test_gln_pointer_checks():
+    p = hstu.gln_problem(10, 64, 4, BF16)
+    with pytest.raises(hstu.MtgrError) as e:
+        hstu.mtgr_group_layernorm_fwd(p, FAKE, None, FAKE, FAKE, FAKE, None, None, None, 0)
+    assert e.value.status == hstu.MTGR_ERROR_NULL_POINTER
+    with pytest.raises(hstu.MtgrError) as e:       # du given without u
+        hstu.mtgr_group_layernorm_bwd(p, FAKE, FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                      FAKE, None, 0, 0)
+    assert e.value.status == hstu.MTGR_ERROR_INVALID_ARGUMENT
+    assert hstu.mtgr_group_layernorm_workspace_size(p) == 0
+
+
+def test_missing_library_fails_loudly(monkeypatch, tmp_path):
+    monkeypatch.setattr(hstu, "_lib", None)
+    monkeypatch.setattr(hstu, "LIB_PATH", str(tmp_path / "absent.so"))
+    with pytest.raises(hstu.MtgrLibraryMissing):
+        hstu.lib()

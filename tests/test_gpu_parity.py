@@ -1,0 +1,179 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Bar, per output tensor, each stage fed with the device's stored inputs (so every
+kernel is checked on its own inputs):
+  bf16: max over users of  max_i (|gpu_i - ref_i| - 2^-8 |ref_i|)_+ / rms_user(ref) <= 2e-2
+  fp32: the same with no allowance, <= 1e-4
+Users are independent problems whose output scales differ by 1/sqrt(n_b), so the
+RMS is taken per user; the 2^-8 |ref| allowance is the rounding of a bf16 result
+(half an ulp for the stored output, half for the bf16 MFMA operand P or dS).
+Batch-summed gradients (dgamma, dbeta, drab) use max |gpu - ref| / rms(ref).
+The mask itself is checked exactly in test_gpu_mask.py (one-hot extraction of
+every p_ij and dS_ij).
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_2505_18654_amd import ops
+from synth import SEG_CAND, SEG_HIST, SEG_RT, SEG_USER, make_layout
+from tests.gpu_util import (TOL, compare, custom_layout, gpu_step, jagged, make_inputs, oracle_stages,
+                            rows_of, say, to_np)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def check(layout, users, inp, whole_batch, fwd_only=False, label=""):
+    tol = TOL[layout.spec.dtype]
+    say(f"[parity] {label} users={len(users)} T={layout.total_tokens} dtype={layout.spec.dtype}")
+    gpu = gpu_step(inp, fwd_only=fwd_only)
+    torch.cuda.synchronize()
+    ref = oracle_stages(layout, users, inp, gpu, fwd_only=fwd_only)
+    errs, raw, bad = compare(layout, users, gpu, ref, tol, whole_batch)
+    say(f"[parity] {label} " + " ".join(f"{k}={v:.2e}" for k, v in errs.items()))
+    say(f"[parity] {label} raw max/rms " + " ".join(f"{k}={v:.2e}" for k, v in raw.items()))
+    assert not bad, f"{label}: above {tol}: {bad}"
+    return gpu, ref, errs
+
+
+@pytest.mark.parametrize("config", ["tiny", "small"])
+def test_whole_batch(config):
+    L = make_layout(config)
+    inp = make_inputs(L, all_exact=True)
+    check(L, list(range(L.num_users)), inp, whole_batch=True, label=config)
+
+
+@pytest.mark.parametrize("config,nusers", [("mtgr_small", 10), ("mtgr_large", 6), ("serving", 5)])
+def test_subset_batch_all_outputs(config, nusers):
+    """A few users of the big configs (longest and shortest included) as a batch of their own."""
+    L = make_layout(config)
+    lens = np.diff(L.offsets)
+    rng = np.random.default_rng(0)
+    users = sorted(set([int(np.argmax(lens)), int(np.argmin(lens))] +
+                       rng.choice(L.num_users, nusers - 2, replace=False).tolist()))
+    sub = L.subset(users)
+    inp = make_inputs(sub, all_exact=True)
+    check(sub, list(range(sub.num_users)), inp, whole_batch=True,
+          fwd_only=L.spec.fwd_only, label=f"{config}-subset")
+
+
+@pytest.mark.parametrize("config", ["mtgr_small", "mtgr_large", "serving"])
+def test_full_size_sampled_users(config):
+    """Full-size batch in the benchmark's launch configuration; sampled users compared."""
+    L = make_layout(config)
+    lens = np.diff(L.offsets)
+    users = sorted({int(np.argmax(lens)), int(np.argmin(lens)), L.num_users // 2, L.num_users - 1})
+    tensors = ("q", "k", "v", "u") if L.spec.fwd_only else ("q", "k", "v", "u", "dy")
+    from synth.torch_inputs import device_inputs
+    inp = device_inputs(L, "cuda", exact_users=users, tensors=tensors)
+    check(L, users, inp, whole_batch=False, fwd_only=L.spec.fwd_only, label=f"{config}-full")
+
+
+# ------------------------------------------------------------------ edge cases
+
+def edge_layouts():
+    U, S, R, C = SEG_USER, SEG_HIST, SEG_RT, SEG_CAND
+    cases = {}
+    cases["empty_users"] = ([[], [U, S, S, R, C], [], [C], []], [[], [0, -5, -3, 10, 20], [], [7], []])
+    cases["only_candidates"] = ([[C] * 70], [list(range(70))])
+    cases["causal_rt"] = ([[R] * 150], [list(range(150))])
+    cases["ties"] = ([[U, S, R, R, R, C, C, C] * 9], [[0, -1, 5, 5, 5, 5, 5, 6] * 9])
+    cases["ragged"] = ([[U] * 3 + [S] * 60 + [R] * 7 + [C] * 1, [U] * 1 + [S] * 129 + [R] * 2 + [C] * 3,
+                        [S] * 64, [S] * 128, [S] * 127 + [C]],
+                       [[0] * 3 + list(range(-60, 0)) + [1, 2, 3, 9, 10, 11, 12] + [5],
+                        [0] + list(range(-129, 0)) + [50, 10] + [60, 11, 1],
+                        list(range(-64, 0)), list(range(-128, 0)), list(range(-127, 0)) + [3]])
+    rng = np.random.default_rng(3)
+    n_rt, n_c = 300, 200
+    cases["long_user"] = ([[U] * 16 + [S] * 3500 + [R] * n_rt + [C] * n_c],
+                          [[0] * 16 + sorted(rng.integers(-10**7, 0, 3500).tolist()) +
+                           sorted(rng.choice(86400, n_rt, replace=False).tolist()) +
+                           rng.integers(0, 86400, n_c).tolist()])
+    return cases
+
+
+@pytest.mark.parametrize("name", list(edge_layouts()))
+@pytest.mark.parametrize("dtype,dh", [("bf16", 128), ("bf16", 64), ("bf16", 32), ("fp32", 16), ("fp32", 64)])
+def test_edge_cases(name, dtype, dh):
+    if name == "long_user" and dtype == "fp32":
+        pytest.skip("fp32 parity kernel is for small shapes")
+    segs, tss = edge_layouts()[name]
+    L = custom_layout(segs, tss, heads=2, head_dim=dh, dtype=dtype, rab_buckets=64 if dh == 64 else 0)
+    inp = make_inputs(L, all_exact=True)
+    check(L, list(range(L.num_users)), inp, whole_batch=True, label=f"{name}-{dtype}-{dh}")
+
+
+def test_strided_views_of_fused_projection():
+    """q, k, v, u as column slices of one [T, 4d] buffer (token stride 4d)."""
+    L = make_layout("small")
+    inp = make_inputs(L, all_exact=True)
+    T, H, dh = inp["q"].shape
+    d = H * dh
+    fused = torch.empty((T, 4 * d), dtype=inp["q"].dtype, device="cuda")
+    for i, name in enumerate(("q", "k", "v", "u")):
+        fused[:, i * d:(i + 1) * d] = inp[name].reshape(T, d)
+    views = dict(inp)
+    for i, name in enumerate(("q", "k", "v")):
+        views[name] = fused[:, i * d:(i + 1) * d].view(T, H, dh)
+    views["u"] = fused[:, 3 * d:]
+    say("[parity] strided views")
+    a = gpu_step(inp)
+    b = gpu_step(views)
+    torch.cuda.synchronize()
+    for key in ("o", "y", "dq", "dk", "dv", "du"):
+        assert torch.equal(a[key].reshape(T, -1), b[key].reshape(T, -1)), key
+
+
+def test_forward_and_backward_are_deterministic():
+    L = make_layout("mtgr_small")
+    inp = make_inputs(L, users=[0])
+    jag = jagged(inp)
+    say("[determinism] mtgr_small")
+    o1 = ops.attn_fwd(inp["q"], inp["k"], inp["v"], jag, inp["rab"])
+    o2 = ops.attn_fwd(inp["q"], inp["k"], inp["v"], jag, inp["rab"])
+    g1 = ops.attn_bwd(inp["q"], inp["k"], inp["v"], inp["do"], jag, inp["rab"])
+    g2 = ops.attn_bwd(inp["q"], inp["k"], inp["v"], inp["do"], jag, inp["rab"])
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2)
+    for a, b in zip(g1[:3], g2[:3]):
+        assert torch.equal(a, b)
+
+
+def test_candidate_isolation_bitwise():
+    """Perturbing one candidate leaves every other token's forward output bit-identical."""
+    L = make_layout("small")
+    inp = make_inputs(L, all_exact=True)
+    jag = jagged(inp)
+    c = int(np.nonzero(L.seg == SEG_CAND)[0][3])
+    say("[isolation] candidate", c)
+    o1 = ops.attn_fwd(inp["q"], inp["k"], inp["v"], jag)
+    q2, k2, v2 = inp["q"].clone(), inp["k"].clone(), inp["v"].clone()
+    q2[c] += 1.0
+    k2[c] -= 0.5
+    v2[c] *= 3.0
+    o2 = ops.attn_fwd(q2, k2, v2, jag)
+    torch.cuda.synchronize()
+    keep = torch.ones(L.total_tokens, dtype=torch.bool, device="cuda")
+    keep[c] = False
+    assert torch.equal(o1[keep], o2[keep])
+    assert not torch.equal(o1[c], o2[c])
+
+
+def test_user_permutation_bitwise():
+    L = make_layout("small")
+    perm = list(np.random.default_rng(1).permutation(L.num_users))
+    P = L.subset(perm)
+    a = make_inputs(L, all_exact=True)
+    b = make_inputs(P, all_exact=True)
+    say("[permutation] small")
+    oa = ops.attn_fwd(a["q"], a["k"], a["v"], jagged(a))
+    ob = ops.attn_fwd(b["q"], b["k"], b["v"], jagged(b))
+    torch.cuda.synchronize()
+    idx = torch.from_numpy(rows_of(L, perm)).cuda()
+    assert torch.equal(oa[idx], ob)

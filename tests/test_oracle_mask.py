@@ -125,3 +125,11 @@ def test_bucket_bit_length_identity():
     got = [oracle.rab_bucket(d) for d in range(0, 70000)]
     assert all(a <= b for a, b in zip(got, got[1:]))          # monotone in the gap
     assert max(oracle.rab_bucket(int(d)) for d in deltas.tolist()) <= 63
+
+
+def test_bench_pair_count_matches_oracle():
+    import bench
+    for config in ("tiny", "small"):
+        L = make_layout(config)
+        sub = L.subset(range(min(L.num_users, 8)))
+        assert int(bench.visible_pairs(sub).sum()) == oracle.count_visible(sub.offsets, sub.seg, sub.ts)

@@ -63,3 +63,10 @@ def test_bf16_rounding():
     assert abs(r[3] - x[3]) <= 2**-7 * 4
     vals = make_values(make_layout("small"), users=[0], tensors=("q",))
     assert np.array_equal(vals["q"], bf16_bits_to_f32(f32_to_bf16_bits(vals["q"])))
+
+
+def test_subset_of_subset_keeps_original_users():
+    L = make_layout("small")
+    a = L.subset([7, 3, 20])
+    b = a.subset([2, 0])
+    np.testing.assert_array_equal(make_values(b)["q"], make_values(L.subset([20, 7]))["q"])

@@ -185,6 +185,7 @@ def main():
     dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
     drab = torch.empty_like(rab) if rab is not None else None
     ws = ops.workspace_for(ops.attn_problem(jag, q, k, v, o, rab), "cuda")
+    gws = ops.gln_workspace(y, gamma.shape[0])
 
     stages = ["plan", "attn_fwd", "gln_fwd"] + ([] if fwd_only else ["gln_bwd", "attn_bwd_dq", "attn_bwd_dkdv"])
 
@@ -196,7 +197,8 @@ def main():
         elif name == "gln_fwd":
             ops.gln_fwd(o.view(T, d), u, seg, gamma, beta, y=y, stats=(mean, rstd))
         elif name == "gln_bwd":
-            ops.gln_bwd(inp["dy"], o.view(T, d), u, seg, gamma, mean, rstd, grads=(dx, du, dg, db))
+            ops.gln_bwd(inp["dy"], o.view(T, d), u, seg, gamma, mean, rstd, grads=(dx, du, dg, db),
+                        workspace=gws)
         elif name == "attn_bwd_dq":
             ops.attn_bwd(q, k, v, dx.view(T, H, dh), jag, rab, grads=(dq, dk, dv, drab), workspace=ws,
                          planned=True, parts="dq")

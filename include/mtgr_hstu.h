@@ -158,7 +158,8 @@ mtgr_status_t mtgr_hstu_attn_bwd(const mtgr_hstu_problem_t* p, const int32_t* of
                                  const void* dout, void* dq, void* dk, void* dv, float* drab,
                                  void* workspace, size_t workspace_bytes, mtgr_stream_t stream);
 
-/* Bytes of device workspace for the Group-LN calls (currently always 0). */
+/* Bytes of device workspace for the Group-LN calls: 0 for the forward; the backward
+ * keeps per-workgroup dgamma/dbeta partials (about 512 x 2 G d floats at most). */
 mtgr_status_t mtgr_group_layernorm_workspace_size(const mtgr_gln_problem_t* p, int backward,
                                                   size_t* bytes);
 
@@ -178,7 +179,9 @@ mtgr_status_t mtgr_group_layernorm_fwd(const mtgr_gln_problem_t* p, const void* 
  *   dz = rstd (g - mean(g) - zhat mean(g (*) zhat)),  dx = dz (*) u,  du = dz (*) x,
  *   dgamma[g] = sum over tokens of group g of dy (*) zhat,  dbeta[g] = sum of dy.
  *   du must be non-NULL iff u is non-NULL.  dgamma, dbeta [G][d] fp32 are
- *   overwritten; their summation order is not fixed (fp32 atomics). */
+ *   overwritten: summed per workgroup (LDS atomics among its waves, order not fixed),
+ *   then over workgroups in a fixed order.  workspace: at least
+ *   mtgr_group_layernorm_workspace_size(p, 1) bytes, 16-byte aligned. */
 mtgr_status_t mtgr_group_layernorm_bwd(const mtgr_gln_problem_t* p, const void* dy, const void* x,
                                        const void* u, const int8_t* group_ids, const float* gamma,
                                        const float* mean, const float* rstd, void* dx, void* du,

@@ -336,11 +336,12 @@ extern "C" {
 
 mtgr_status_t mtgr_group_layernorm_workspace_size(const mtgr_gln_problem_t* p, int backward,
                                                   size_t* bytes) {
-    (void)backward;
     if (!bytes) return fail(MTGR_ERROR_NULL_POINTER, "bytes is NULL");
     mtgr_status_t st = check_gln(p);
     if (st != MTGR_SUCCESS) return st;
-    *bytes = 0;
+    *bytes = (backward && p->num_tokens > 0)
+                 ? align256(mtgr::gln_bwd_workspace_bytes(p->num_tokens, p->dim, p->num_groups))
+                 : 0;
     return ok();
 }
 
@@ -377,8 +378,6 @@ mtgr_status_t mtgr_group_layernorm_bwd(const mtgr_gln_problem_t* p, const void* 
                                        const float* mean, const float* rstd, void* dx, void* du,
                                        float* dgamma, float* dbeta, void* workspace,
                                        size_t workspace_bytes, mtgr_stream_t stream) {
-    (void)workspace;
-    (void)workspace_bytes;
     mtgr_status_t st = check_gln(p);
     if (st != MTGR_SUCCESS) return st;
     REQUIRE_PTR(gamma, "gamma");
@@ -386,6 +385,12 @@ mtgr_status_t mtgr_group_layernorm_bwd(const mtgr_gln_problem_t* p, const void* 
     REQUIRE_PTR(dbeta, "dbeta");
     if ((u == nullptr) != (du == nullptr))
         return fail(MTGR_ERROR_INVALID_ARGUMENT, "du must be given exactly when u is given");
+    if (p->num_tokens > 0) {
+        const size_t need = align256(mtgr::gln_bwd_workspace_bytes(p->num_tokens, p->dim, p->num_groups));
+        if (workspace_bytes < need)
+            return fail(MTGR_ERROR_WORKSPACE_TOO_SMALL, "workspace %zu bytes, need %zu", workspace_bytes, need);
+        REQUIRE_PTR(workspace, "workspace");
+    }
     if (p->num_tokens > 0) {
         REQUIRE_PTR(dy, "dy");
         REQUIRE_PTR(x, "x");
@@ -410,6 +415,7 @@ mtgr_status_t mtgr_group_layernorm_bwd(const mtgr_gln_problem_t* p, const void* 
     a.du = du;
     a.dgamma = dgamma;
     a.dbeta = dbeta;
+    a.workspace = (float*)workspace;
     hipError_t e = mtgr::launch_gln_bwd(a, p->dtype == MTGR_DTYPE_BF16, (hipStream_t)stream);
     if (e != hipSuccess) return device_fail(e, "group layernorm backward");
     return ok();

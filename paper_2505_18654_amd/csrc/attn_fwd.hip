@@ -35,7 +35,7 @@ __device__ __forceinline__ uint4 ldg16(const uint16_t* p) { return *(const uint4
 }  // namespace
 
 template <int DH, bool RAB>
-__global__ __launch_bounds__(256) void attn_fwd_bf16_kernel(AttnArgs a) {
+__global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
     using SM = FwdSmem<DH>;
     constexpr int KP = SM::KP, VP = SM::VP, OP = SM::OP;
     constexpr int KSTEPS = DH / 16;   // k-steps of S^T = K Q^T

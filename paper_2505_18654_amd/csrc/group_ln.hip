@@ -4,16 +4,16 @@
 // cross-lane shuffles, two-pass variance on values held in registers.  Each wave walks a
 // run of consecutive tokens; since a user's tokens come segment by segment ([U|S|R|I]) and
 // the groups are the segments, gamma/beta rows stay in registers across a run and are only
-// re-read when the group changes.  The backward keeps dgamma/dbeta partials for the current
-// group in registers and flushes them with fp32 atomics when the group changes.
+// re-read when the group changes.
 #include "mtgr_device.h"
 #include "mtgr_internal.h"
 
 namespace mtgr {
 
 namespace {
-constexpr int WAVES = 4;
-constexpr int TOKENS_PER_WAVE = 16;
+constexpr int WAVES = 4;            // forward: waves per workgroup
+constexpr int TOKENS_PER_WAVE = 16;  // forward: consecutive tokens per wave
+constexpr int BWD_WAVES = 8;         // backward: waves per workgroup
 
 template <bool BF16>
 struct Vec;   // 16-byte chunk of the storage type
@@ -134,15 +134,29 @@ __global__ __launch_bounds__(WAVES * 64) void gln_fwd_kernel(GlnArgs a) {
     }
 }
 
-template <bool BF16, int NCH, bool GATE>
-__global__ __launch_bounds__(WAVES * 64) void gln_bwd_kernel(GlnArgs a) {
+// Backward.  Workgroup = BWD_WAVES waves over a contiguous chunk of tokens, each wave a
+// contiguous run of `tpw` tokens (the next token's rows are loaded while the current one is
+// processed).  dgamma/dbeta: each wave keeps the partial sums of its current group in
+// registers and adds them into a per-workgroup accumulator [2][G][d] when the group changes
+// (LDS atomics among the workgroup's waves, or the workgroup's own workspace slot when
+// 2 G d floats do not fit in LDS); the accumulator is then stored to the workgroup's slot
+// and gln_param_reduce_kernel sums the slots in a fixed order.  No device-wide atomics.
+template <bool BF16, int NCH, bool GATE, bool LDS_ACC>
+__global__ __launch_bounds__(BWD_WAVES * 64) void gln_bwd_kernel(GlnArgs a, float* __restrict__ part,
+                                                                 int tpw) {
     using V = Vec<BF16>;
     constexpr int N = V::N;
-    const int lane = threadIdx.x & 63;
-    const long long wave = (long long)blockIdx.x * WAVES + (threadIdx.x >> 6);
-    const long long t0 = wave * TOKENS_PER_WAVE;
+    extern __shared__ float sAcc[];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int d = a.d;
     const int nch = d / N;
+    const int accn = 2 * a.G * d;
+    float* slot = part + (long long)blockIdx.x * accn;
+    float* acc = LDS_ACC ? sAcc : slot;
+    for (int i = threadIdx.x; i < accn; i += BWD_WAVES * 64) acc[i] = 0.f;
+    __syncthreads();
+    const long long t0 = ((long long)blockIdx.x * BWD_WAVES + w) * tpw;
+    const long long t1 = min(t0 + tpw, a.T);
     const float inv_d = 1.0f / (float)d;
     float gam[NCH][N], pg[NCH][N], pb[NCH][N];
     int gcur = -1;
@@ -154,14 +168,39 @@ __global__ __launch_bounds__(WAVES * 64) void gln_bwd_kernel(GlnArgs a) {
             if (ch < nch) {
 #pragma unroll
                 for (int i = 0; i < N; i++) {
-                    atomicAdd(&a.dgamma[gcur * d + ch * N + i], pg[c][i]);
-                    atomicAdd(&a.dbeta[gcur * d + ch * N + i], pb[c][i]);
+                    atomicAdd(&acc[gcur * d + ch * N + i], pg[c][i]);
+                    atomicAdd(&acc[(a.G + gcur) * d + ch * N + i], pb[c][i]);
                 }
             }
         }
     };
-    for (long long t = t0; t < t0 + TOKENS_PER_WAVE && t < a.T; t++) {
+    // raw rows of the token being processed and of the next one
+    float xr[NCH][N], ur[NCH][N], yr[NCH][N];
+    auto load_rows = [&](long long t) {
+#pragma unroll
+        for (int c = 0; c < NCH; c++) {
+            const int ch = lane + 64 * c;
+            if (ch < nch) {
+                V::load(a.x, t * a.ld_x + ch * N, xr[c]);
+                V::load(a.dy, t * a.ld_y + ch * N, yr[c]);
+                if (GATE) V::load(a.u, t * a.ld_u + ch * N, ur[c]);
+            }
+        }
+    };
+    if (t0 < t1) load_rows(t0);
+    for (long long t = t0; t < t1; t++) {
+        float xx[NCH][N], uu[NCH][N], dy[NCH][N];
+#pragma unroll
+        for (int c = 0; c < NCH; c++)
+#pragma unroll
+            for (int i = 0; i < N; i++) {
+                xx[c][i] = xr[c][i];
+                dy[c][i] = yr[c][i];
+                uu[c][i] = GATE ? ur[c][i] : 1.f;
+            }
         const int g = a.gid[t];
+        const float mean = a.mean[t], rstd = a.rstd[t];
+        if (t + 1 < t1) load_rows(t + 1);
         if (g != gcur) {
             flush();
             gcur = g;
@@ -176,31 +215,19 @@ __global__ __launch_bounds__(WAVES * 64) void gln_bwd_kernel(GlnArgs a) {
                 }
             }
         }
-        const float mean = a.mean[t], rstd = a.rstd[t];
-        float xh[NCH][N], gy[NCH][N];
+        float xh[NCH][N];
         float s1 = 0.f, s2 = 0.f;
 #pragma unroll
         for (int c = 0; c < NCH; c++) {
-            const int ch = lane + 64 * c;
-            if (ch < nch) {
-                float xx[N], dy[N];
-                V::load(a.x, t * a.ld_x + ch * N, xx);
-                V::load(a.dy, t * a.ld_y + ch * N, dy);
-                if (GATE) {
-                    float uu[N];
-                    V::load(a.u, t * a.ld_u + ch * N, uu);
-#pragma unroll
-                    for (int i = 0; i < N; i++) xx[i] *= uu[i];
-                }
+            if (lane + 64 * c < nch) {
 #pragma unroll
                 for (int i = 0; i < N; i++) {
-                    xh[c][i] = (xx[i] - mean) * rstd;
-                    gy[c][i] = dy[i];
-                    const float gg = dy[i] * gam[c][i];
+                    xh[c][i] = (xx[c][i] * uu[c][i] - mean) * rstd;
+                    const float gg = dy[c][i] * gam[c][i];
                     s1 += gg;
                     s2 += gg * xh[c][i];
-                    pg[c][i] += dy[i] * xh[c][i];
-                    pb[c][i] += dy[i];
+                    pg[c][i] += dy[c][i] * xh[c][i];
+                    pb[c][i] += dy[c][i];
                 }
             }
         }
@@ -212,15 +239,13 @@ __global__ __launch_bounds__(WAVES * 64) void gln_bwd_kernel(GlnArgs a) {
             if (ch < nch) {
                 float dz[N];
 #pragma unroll
-                for (int i = 0; i < N; i++) dz[i] = rstd * (gy[c][i] * gam[c][i] - m1 - xh[c][i] * m2);
+                for (int i = 0; i < N; i++) dz[i] = rstd * (dy[c][i] * gam[c][i] - m1 - xh[c][i] * m2);
                 if (GATE) {
-                    float xx[N], uu[N], dx[N], du[N];
-                    V::load(a.x, t * a.ld_x + ch * N, xx);
-                    V::load(a.u, t * a.ld_u + ch * N, uu);
+                    float dx[N], du[N];
 #pragma unroll
                     for (int i = 0; i < N; i++) {
-                        dx[i] = dz[i] * uu[i];
-                        du[i] = dz[i] * xx[i];
+                        dx[i] = dz[i] * uu[c][i];
+                        du[i] = dz[i] * xx[c][i];
                     }
                     V::store(a.dx, t * a.ld_x + ch * N, dx);
                     V::store(a.du, t * a.ld_u + ch * N, du);
@@ -231,20 +256,58 @@ __global__ __launch_bounds__(WAVES * 64) void gln_bwd_kernel(GlnArgs a) {
         }
     }
     flush();
+    __syncthreads();
+    if (LDS_ACC)
+        for (int i = threadIdx.x; i < accn; i += BWD_WAVES * 64) slot[i] = sAcc[i];
+}
+
+// dgamma/dbeta = sum over workgroup slots (fixed order).  Block = 64 columns x 4 row sets.
+__global__ __launch_bounds__(256) void gln_param_reduce_kernel(const float* __restrict__ part,
+                                                               int nslots, int accn, int gd,
+                                                               float* __restrict__ dgamma,
+                                                               float* __restrict__ dbeta) {
+    __shared__ float sRed[4][64];
+    const int c = threadIdx.x & 63, r = threadIdx.x >> 6;
+    const int e = blockIdx.x * 64 + c;
+    float sum = 0.f;
+    if (e < accn)
+        for (int s = r; s < nslots; s += 4) sum += part[(long long)s * accn + e];
+    sRed[r][c] = sum;
+    __syncthreads();
+    if (r == 0 && e < accn) {
+        const float tot = ((sRed[0][c] + sRed[1][c]) + sRed[2][c]) + sRed[3][c];
+        if (e < gd) dgamma[e] = tot;
+        else dbeta[e - gd] = tot;
+    }
 }
 
 template <bool BF16, int NCH>
 static hipError_t gln_launch(const GlnArgs& a, bool bwd, hipStream_t s) {
-    const long long waves = (a.T + TOKENS_PER_WAVE - 1) / TOKENS_PER_WAVE;
-    const int blocks = (int)((waves + WAVES - 1) / WAVES);
     const bool gate = a.u != nullptr;
     if (!bwd) {
+        const long long waves = (a.T + TOKENS_PER_WAVE - 1) / TOKENS_PER_WAVE;
+        const int blocks = (int)((waves + WAVES - 1) / WAVES);
         if (gate) gln_fwd_kernel<BF16, NCH, true><<<blocks, WAVES * 64, 0, s>>>(a);
         else gln_fwd_kernel<BF16, NCH, false><<<blocks, WAVES * 64, 0, s>>>(a);
-    } else {
-        if (gate) gln_bwd_kernel<BF16, NCH, true><<<blocks, WAVES * 64, 0, s>>>(a);
-        else gln_bwd_kernel<BF16, NCH, false><<<blocks, WAVES * 64, 0, s>>>(a);
+        return hipGetLastError();
     }
+    int nslots, tpw;
+    gln_bwd_partition(a.T, &nslots, &tpw);
+    const int accn = 2 * a.G * a.d;
+    const bool lds = accn * (int)sizeof(float) <= GLN_LDS_ACC_BYTES;
+    const size_t shm = lds ? accn * sizeof(float) : 0;
+    float* part = a.workspace;
+    if (lds) {
+        if (gate) gln_bwd_kernel<BF16, NCH, true, true><<<nslots, BWD_WAVES * 64, shm, s>>>(a, part, tpw);
+        else gln_bwd_kernel<BF16, NCH, false, true><<<nslots, BWD_WAVES * 64, shm, s>>>(a, part, tpw);
+    } else {
+        if (gate) gln_bwd_kernel<BF16, NCH, true, false><<<nslots, BWD_WAVES * 64, 0, s>>>(a, part, tpw);
+        else gln_bwd_kernel<BF16, NCH, false, false><<<nslots, BWD_WAVES * 64, 0, s>>>(a, part, tpw);
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    gln_param_reduce_kernel<<<(accn + 63) / 64, 256, 0, s>>>(part, nslots, accn, a.G * a.d, a.dgamma,
+                                                            a.dbeta);
     return hipGetLastError();
 }
 
@@ -259,16 +322,30 @@ static hipError_t gln_dispatch(const GlnArgs& a, bool bwd, hipStream_t s) {
     return hipErrorInvalidValue;
 }
 
+void gln_bwd_partition(long long T, int* nslots, int* tpw) {
+    const long long per_wave = (T + (long long)GLN_BWD_SLOTS * BWD_WAVES - 1) / ((long long)GLN_BWD_SLOTS * BWD_WAVES);
+    *tpw = (int)(per_wave < 1 ? 1 : per_wave);
+    *nslots = (int)((T + (long long)*tpw * BWD_WAVES - 1) / ((long long)*tpw * BWD_WAVES));
+    if (*nslots < 1) *nslots = 1;
+}
+
+size_t gln_bwd_workspace_bytes(long long T, int d, int G) {
+    int nslots, tpw;
+    gln_bwd_partition(T, &nslots, &tpw);
+    return (size_t)nslots * 2 * G * d * sizeof(float);
+}
+
 hipError_t launch_gln_fwd(const GlnArgs& a, bool bf16, hipStream_t s) {
     if (a.T == 0) return hipSuccess;
     return bf16 ? gln_dispatch<true>(a, false, s) : gln_dispatch<false>(a, false, s);
 }
 
 hipError_t launch_gln_bwd(const GlnArgs& a, bool bf16, hipStream_t s) {
-    hipError_t e = launch_fill_f32(a.dgamma, (long long)a.G * a.d, 0.f, s);
-    if (e != hipSuccess) return e;
-    e = launch_fill_f32(a.dbeta, (long long)a.G * a.d, 0.f, s);
-    if (e != hipSuccess || a.T == 0) return e;
+    if (a.T == 0) {
+        hipError_t e = launch_fill_f32(a.dgamma, (long long)a.G * a.d, 0.f, s);
+        if (e != hipSuccess) return e;
+        return launch_fill_f32(a.dbeta, (long long)a.G * a.d, 0.f, s);
+    }
     return bf16 ? gln_dispatch<true>(a, true, s) : gln_dispatch<false>(a, true, s);
 }
 

@@ -83,11 +83,13 @@ __device__ __forceinline__ int token_code(int seg) {
 
 // Dynamic mask of Sec. 4.2 from token codes: i == j, static key (rule 1), or an RT key
 // strictly earlier than a dynamic query (rule 2); candidates only see themselves (rule 3).
+// Evaluated with bitwise logic so that it compiles to compares and selects, not branches.
 __device__ __forceinline__ bool visible(int qcode, int qts, int qidx, int kcode, int kts,
                                         int kidx) {
-    bool v = (kcode & KC_STATIC) || (qidx == kidx) ||
-             ((kcode & KC_RT) && (qcode & KC_DYN) && kts < qts);
-    return v && (kcode & KC_VALID) && (qcode & KC_VALID);
+    const int both_valid = kcode & qcode & KC_VALID;
+    const int rule2 = (kcode & KC_RT) & ((qcode & KC_DYN) >> 1) & (kts < qts ? KC_RT : 0);
+    const int seen = (kcode & KC_STATIC) | (qidx == kidx ? 1 : 0) | (rule2 >> 1);
+    return (seen != 0) & (both_valid != 0);
 }
 
 // Half-octave log-time bucket of |a - b| (gap as uint32), clamped to nb - 1.
@@ -112,17 +114,16 @@ __device__ __forceinline__ float bf16_to_f32(uint16_t h) {
     return __uint_as_float(((uint32_t)h) << 16);
 }
 
-// fp32 -> bf16 bits, round to nearest even (inputs here are finite or inf).
-__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;  // quiet NaN
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return u >> 16;
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float float2_t __attribute__((ext_vector_type(2)));
+
+// fp32 pair -> packed bf16 pair, round to nearest even (one v_cvt_pk_bf16_f32).
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    const float2_t f = {lo, hi};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2_t));
 }
 
-__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-    return f32_to_bf16_bits(lo) | (f32_to_bf16_bits(hi) << 16);
-}
+__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) { return pack_bf16x2(f, 0.f) & 0xffffu; }
 
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll

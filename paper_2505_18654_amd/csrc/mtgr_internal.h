@@ -67,7 +67,13 @@ struct GlnArgs {
     void* du;
     float* dgamma;
     float* dbeta;
+    float* workspace;   // backward: per-workgroup dgamma/dbeta partials
 };
+
+constexpr int GLN_BWD_SLOTS = 512;            // target workgroups of the backward
+constexpr int GLN_LDS_ACC_BYTES = 64 * 1024;  // largest per-workgroup accumulator kept in LDS
+void gln_bwd_partition(long long T, int* nslots, int* tokens_per_wave);
+size_t gln_bwd_workspace_bytes(long long T, int d, int G);
 
 hipError_t launch_gln_fwd(const GlnArgs& a, bool bf16, hipStream_t s);
 hipError_t launch_gln_bwd(const GlnArgs& a, bool bf16, hipStream_t s);

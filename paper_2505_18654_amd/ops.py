@@ -142,7 +142,7 @@ def gln_fwd(x, u, group_ids, gamma, beta, eps: float = 1e-5, y=None, stats=None)
     return y, mean, rstd
 
 
-def gln_bwd(dy, x, u, group_ids, gamma, mean, rstd, eps: float = 1e-5, grads=None):
+def gln_bwd(dy, x, u, group_ids, gamma, mean, rstd, eps: float = 1e-5, grads=None, workspace=None):
     """Gate + Group-LN backward: returns (dx, du-or-None, dgamma, dbeta)."""
     T, d = x.shape
     if grads is None:
@@ -156,5 +156,16 @@ def gln_bwd(dy, x, u, group_ids, gamma, mean, rstd, eps: float = 1e-5, grads=Non
                          _token_stride(u, d) if u is not None else d, _token_stride(dy, d))
     if _token_stride(dx, d) != p.ld_x or (du is not None and _token_stride(du, d) != p.ld_u):
         raise ValueError("gradients must share the layout of x, u")
-    hstu.mtgr_group_layernorm_bwd(p, dy, x, u, group_ids, gamma, mean, rstd, dx, du, dgamma, dbeta)
+    if workspace is None:
+        n = hstu.mtgr_group_layernorm_workspace_size(p, True)
+        workspace = torch.empty(max(n, 256), dtype=torch.uint8, device=x.device)
+    hstu.mtgr_group_layernorm_bwd(p, dy, x, u, group_ids, gamma, mean, rstd, dx, du, dgamma, dbeta,
+                                  workspace, workspace.numel())
     return dx, du, dgamma, dbeta
+
+
+def gln_workspace(x, groups: int) -> torch.Tensor:
+    T, d = x.shape
+    p = hstu.gln_problem(T, d, groups, _dtype_code(x))
+    n = hstu.mtgr_group_layernorm_workspace_size(p, True)
+    return torch.empty(max(n, 256), dtype=torch.uint8, device=x.device)

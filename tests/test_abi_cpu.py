@@ -185,6 +185,12 @@ def test_gln_pointer_checks():
                                       FAKE, None, 0, 0)
     assert e.value.status == hstu.MTGR_ERROR_INVALID_ARGUMENT
     assert hstu.mtgr_group_layernorm_workspace_size(p) == 0
+    need = hstu.mtgr_group_layernorm_workspace_size(p, True)
+    assert need >= 2 * 4 * 64 * 4
+    with pytest.raises(hstu.MtgrError) as e:       # backward workspace too small
+        hstu.mtgr_group_layernorm_bwd(p, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                      FAKE, FAKE, need - 1, 0)
+    assert e.value.status == hstu.MTGR_ERROR_WORKSPACE_TOO_SMALL
 
 
 def test_missing_library_fails_loudly(monkeypatch, tmp_path):

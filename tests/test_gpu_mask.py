@@ -103,9 +103,12 @@ def test_pair_extraction(name, which):
     zero_g, zero_w = g == 0.0, w == 0.0
     assert np.array_equal(zero_g, zero_w), f"mask pattern differs at {np.argwhere(zero_g != zero_w)[:5]}"
     vis = ~zero_w
-    rel = np.abs(g[vis] - w[vis]) / np.abs(w[vis])
-    say(f"[mask] {name} {which} visible={int(vis.sum())} max rel={rel.max():.2e}")
-    assert rel.max() < 2.0 ** -6
+    # bf16 rounding of p (or dS) is <= 2^-8 relative; scores q.k that nearly cancel carry
+    # an fp32 accumulation error that is absolute, hence the small floor.
+    floor = 1e-4 * np.abs(w).max()
+    excess = np.abs(g[vis] - w[vis]) - 2.0 ** -7 * np.abs(w[vis])
+    say(f"[mask] {name} {which} visible={int(vis.sum())} max excess/floor={excess.max() / floor:.2e}")
+    assert excess.max() <= floor
 
 
 def test_schedule_covers_every_tile_once():

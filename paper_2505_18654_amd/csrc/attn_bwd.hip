@@ -8,10 +8,13 @@
 //
 // Two kernels, no atomics on dQ/dK/dV (results are deterministic):
 //   dq kernel (row-parallel, like the forward): per wave 32 queries, Q and dO in VGPRs;
-//     per 64-key tile: S^T = K Q^T, dP^T = V dO^T, dS^T in registers, dQ^T += K^T dS^T.
+//     per 32-key half of a 64-key tile: S^T = K Q^T, dP^T = V dO^T, dS^T in registers,
+//     dQ^T += K^T dS^T with K^T read by ds_read_b64_tr_b16 from the row-major K tile.
 //     It also forms drab (LDS histogram, one global atomic per bucket per workgroup).
-//   dkdv kernel (column-parallel): per wave 32 keys, K and V in VGPRs; per 64-query tile:
-//     S = Q K^T, dP = dO V^T (lane = key column), then dV += P^T dO and dK += dS^T Q.
+//   dkdv kernel (column-parallel): per wave 32 keys, K and V in VGPRs; per 32-query half of
+//     a 64-query tile: S = Q K^T, dP = dO V^T (lane = key column), then dV += P^T dO and
+//     dK += dS^T Q with dO and Q read transposed from their row-major tiles.
+// Only row-major tiles live in LDS; every transposed operand comes from the transposing read.
 #include "mtgr_device.h"
 #include "mtgr_internal.h"
 
@@ -26,49 +29,15 @@ __device__ __forceinline__ void zero(floatx16& x) {
 #pragma unroll
     for (int r = 0; r < 16; r++) x[r] = 0.f;
 }
-
-// 8 bf16 of a transposed LDS row in the k-slot order of the accumulator layout:
-// slots 0..3 = columns c0 + 4hh + 0..3, slots 4..7 = columns c0 + 8 + 4hh + 0..3.
-__device__ __forceinline__ bf16x8 ld_tr8(const uint16_t* row) {
-    const uint2 lo = *(const uint2*)row;
-    const uint2 hi = *(const uint2*)(row + 8);
-    return as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y));
-}
-
-// Stage `rows` x DH bf16 from registers (uint4 chunks) into a row-major LDS tile and its
-// transpose.  reg[i] holds chunk (tid + 256 i) of the row-major tile for the row-major
-// copy; treg[r] holds row (rg * RPT + r), chunk cc for the transposed copy.
-template <int DH, int RPT>
-__device__ __forceinline__ void store_transposed(uint16_t* sT, int TP, const uint4* treg, int cc,
-                                                 int rg) {
-#pragma unroll
-    for (int e = 0; e < 8; e++) {
-        uint16_t vals[RPT];
-#pragma unroll
-        for (int r = 0; r < RPT; r++) {
-            const uint32_t word = ((const uint32_t*)&treg[r])[e >> 1];
-            vals[r] = (uint16_t)(word >> (16 * (e & 1)));
-        }
-        uint16_t* dst = &sT[(cc * 8 + e) * TP + rg * RPT];
-        if constexpr (RPT == 4) {
-            *(uint2*)dst = make_uint2(vals[0] | ((uint32_t)vals[1] << 16),
-                                      vals[2] | ((uint32_t)vals[3] << 16));
-        } else if constexpr (RPT == 2) {
-            *(uint32_t*)dst = vals[0] | ((uint32_t)vals[1] << 16);
-        } else {
-            dst[0] = vals[0];
-        }
-    }
-}
 }  // namespace
 
 // ------------------------------------------------------------------ dQ (+ drab), bf16
 template <int DH, bool RAB>
-__global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
-    constexpr int KP = DH + 8, TP = BN + 4, OP = DH + 8;
+__global__ __launch_bounds__(256, 2) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
+    constexpr int KP = DH + 8, OP = DH + 8;
     constexpr int KSTEPS = DH / 16, DBLK = DH / 32, CPR = DH / 8;
-    constexpr int KCH = BN * CPR / 256, RPT = DH / 32;
-    constexpr int KV_BYTES = 2 * BN * KP * 2 + DH * TP * 2;
+    constexpr int KCH = BN * CPR / 256;
+    constexpr int KV_BYTES = 2 * BN * KP * 2;
     constexpr int O_BYTES = BM * OP * 2;
     constexpr int BYTES = KV_BYTES > O_BYTES ? KV_BYTES : O_BYTES;
     __shared__ __align__(16) char smem[BYTES];
@@ -78,7 +47,6 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
     __shared__ float sHist[MTGR_RAB_LDS];
     uint16_t* sK = (uint16_t*)smem;
     uint16_t* sV = sK + BN * KP;
-    uint16_t* sKt = sV + BN * KP;
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int2 item = a.items[blockIdx.x];
@@ -134,9 +102,8 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
         return t;
     };
 
-    uint4 kreg[KCH], vreg[KCH], ktreg[RPT];
+    uint4 kreg[KCH], vreg[KCH];
     int kcode_reg = 0, kts_reg = 0;
-    const int tcc = tid % CPR, trg = tid / CPR;
     auto gload = [&](int t) {
         const int kb = t * BN;
 #pragma unroll
@@ -145,12 +112,6 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
             const bool ok = key < nb;
             kreg[i] = ok ? ldg16(K + (long long)(ob + key) * a.ld_k + h * DH + cc * 8) : make_uint4(0, 0, 0, 0);
             vreg[i] = ok ? ldg16(V + (long long)(ob + key) * a.ld_v + h * DH + cc * 8) : make_uint4(0, 0, 0, 0);
-        }
-#pragma unroll
-        for (int r = 0; r < RPT; r++) {
-            const int key = kb + trg * RPT + r;
-            ktreg[r] = key < nb ? ldg16(K + (long long)(ob + key) * a.ld_k + h * DH + tcc * 8)
-                                : make_uint4(0, 0, 0, 0);
         }
         if (tid < BN) {
             const int key = kb + tid;
@@ -165,7 +126,6 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
             *(uint4*)&sK[row * KP + cc * 8] = kreg[i];
             *(uint4*)&sV[row * KP + cc * 8] = vreg[i];
         }
-        store_transposed<DH, RPT>(sKt, TP, ktreg, tcc, trg);
         if (tid < BN) {
             sKcode[tid] = kcode_reg;
             sKts[tid] = kts_reg;
@@ -182,22 +142,20 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
         const int tn = next_visible(t + 1);
         if (tn < ntk) gload(tn);
 
-        floatx16 sacc[2], dpacc[2];
-        zero(sacc[0]); zero(sacc[1]); zero(dpacc[0]); zero(dpacc[1]);
 #pragma unroll
-        for (int kk = 0; kk < KSTEPS; kk++) {
+        for (int blk = 0; blk < 2; blk++) {
+            floatx16 sacc, dpacc;
+            zero(sacc);
+            zero(dpacc);
 #pragma unroll
-            for (int blk = 0; blk < 2; blk++) {
+            for (int kk = 0; kk < KSTEPS; kk++) {
                 const int off = (32 * blk + col) * KP + 16 * kk + 8 * hh;
                 const bf16x8 ka = *(const bf16x8*)&sK[off];
                 const bf16x8 va = *(const bf16x8*)&sV[off];
-                sacc[blk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qreg[kk], sacc[blk], 0, 0, 0);
-                dpacc[blk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, doreg[kk], dpacc[blk], 0, 0, 0);
+                sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qreg[kk], sacc, 0, 0, 0);
+                dpacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, doreg[kk], dpacc, 0, 0, 0);
             }
-        }
-        uint32_t dsk[4][4];
-#pragma unroll
-        for (int blk = 0; blk < 2; blk++) {
+            uint32_t dsk[2][4];
 #pragma unroll
             for (int r = 0; r < 16; r += 2) {
                 float dv[2];
@@ -205,7 +163,7 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
                 for (int e = 0; e < 2; e++) {
                     const int rr = r + e;
                     const int kl = 32 * blk + 8 * (rr >> 2) + 4 * hh + (rr & 3);
-                    float x = sacc[blk][rr] * alpha;
+                    float x = sacc[rr] * alpha;
                     int bk = 0;
                     if (RAB) {
                         bk = rab_bucket(qts, sKts[kl], a.nbuckets);
@@ -213,7 +171,7 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
                     }
                     float sg;
                     silu_sig(x, sg);
-                    float ds = dpacc[blk][rr] * sg * (1.0f + x * (1.0f - sg)) * inv_n;
+                    float ds = dpacc[rr] * sg * (1.0f + x * (1.0f - sg)) * inv_n;
                     if (cls == TILE_PARTIAL)
                         ds = visible(qcode, qts, qi, sKcode[kl], sKts[kl], t * BN + kl) ? ds : 0.f;
                     else if (!qvalid)
@@ -221,16 +179,16 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
                     if (want_drab && ds != 0.f) atomicAdd(&sHist[bk], ds);
                     dv[e] = ds;
                 }
-                dsk[2 * blk + (r >> 3)][(r & 7) >> 1] = pack_bf16x2(dv[0], dv[1]);
+                dsk[r >> 3][(r & 7) >> 1] = pack_bf16x2(dv[0], dv[1]);
             }
-        }
 #pragma unroll
-        for (int ks = 0; ks < 4; ks++) {
-            const bf16x8 db = as_bf16x8(make_uint4(dsk[ks][0], dsk[ks][1], dsk[ks][2], dsk[ks][3]));
+            for (int kq = 0; kq < 2; kq++) {
+                const bf16x8 db = as_bf16x8(make_uint4(dsk[kq][0], dsk[kq][1], dsk[kq][2], dsk[kq][3]));
 #pragma unroll
-            for (int d = 0; d < DBLK; d++) {
-                const bf16x8 kt = ld_tr8(&sKt[(32 * d + col) * TP + 16 * ks + 4 * hh]);
-                dqacc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kt, db, dqacc[d], 0, 0, 0);
+                for (int d = 0; d < DBLK; d++) {
+                    const bf16x8 kt = lds_read_tr(sK, KP, 32 * blk + 16 * kq, 32 * d, lane);
+                    dqacc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kt, db, dqacc[d], 0, 0, 0);
+                }
             }
         }
         t = tn;
@@ -263,11 +221,11 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
 
 // ------------------------------------------------------------------ dK, dV, bf16
 template <int DH, bool RAB>
-__global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) {
-    constexpr int QP = DH + 8, TP = BN + 4, OP = DH + 8;
+__global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) {
+    constexpr int QP = DH + 8, OP = DH + 8;
     constexpr int KSTEPS = DH / 16, DBLK = DH / 32, CPR = DH / 8;
-    constexpr int QCH = BN * CPR / 256, RPT = DH / 32;
-    constexpr int T_BYTES = 2 * BN * QP * 2 + 2 * DH * TP * 2;
+    constexpr int QCH = BN * CPR / 256;
+    constexpr int T_BYTES = 2 * BN * QP * 2;
     constexpr int O_BYTES = BM * OP * 2;
     constexpr int BYTES = T_BYTES > O_BYTES ? T_BYTES : O_BYTES;
     __shared__ __align__(16) char smem[BYTES];
@@ -276,8 +234,6 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) {
     __shared__ float sRab[MTGR_RAB_LDS];
     uint16_t* sQ = (uint16_t*)smem;
     uint16_t* sDO = sQ + BN * QP;
-    uint16_t* sQt = sDO + BN * QP;
-    uint16_t* sDOt = sQt + DH * TP;
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int2 item = a.items[blockIdx.x];
@@ -328,116 +284,83 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) {
         const bool overlap = (t * BN < k0 + BM) && (k0 < t * BN + BN);
         return tile_class(load_summary(summ, t), sk, overlap);
     };
-    auto next_visible = [&](int t) {
-        while (t < ntq && klass(t) == TILE_MASKED) ++t;
-        return t;
-    };
 
-    uint4 qreg[QCH], goreg[QCH], qtreg[RPT], gotreg[RPT];
-    int qcode_reg = 0, qts_reg = 0;
-    const int tcc = tid % CPR, trg = tid / CPR;
-    auto gload = [&](int t) {
+    // No register prefetch here (the K/V operands and both accumulators fill the budget of
+    // two waves per SIMD); the second workgroup on the CU covers the load latency.
+    for (int t = 0; t < ntq; t++) {
+        const int cls = klass(t);
+        if (cls == TILE_MASKED) continue;
         const int qb = t * BN;
+        __syncthreads();
 #pragma unroll
         for (int i = 0; i < QCH; i++) {
             const int c = tid + 256 * i, row = c / CPR, cc = c % CPR, qr = qb + row;
             const bool ok = qr < nb;
-            qreg[i] = ok ? ldg16(Q + (long long)(ob + qr) * a.ld_q + h * DH + cc * 8) : make_uint4(0, 0, 0, 0);
-            goreg[i] = ok ? ldg16(DO + (long long)(ob + qr) * a.ld_o + h * DH + cc * 8) : make_uint4(0, 0, 0, 0);
-        }
-#pragma unroll
-        for (int r = 0; r < RPT; r++) {
-            const int qr = qb + trg * RPT + r;
-            const bool ok = qr < nb;
-            qtreg[r] = ok ? ldg16(Q + (long long)(ob + qr) * a.ld_q + h * DH + tcc * 8) : make_uint4(0, 0, 0, 0);
-            gotreg[r] = ok ? ldg16(DO + (long long)(ob + qr) * a.ld_o + h * DH + tcc * 8) : make_uint4(0, 0, 0, 0);
+            *(uint4*)&sQ[row * QP + cc * 8] =
+                ok ? ldg16(Q + (long long)(ob + qr) * a.ld_q + h * DH + cc * 8) : make_uint4(0, 0, 0, 0);
+            *(uint4*)&sDO[row * QP + cc * 8] =
+                ok ? ldg16(DO + (long long)(ob + qr) * a.ld_o + h * DH + cc * 8) : make_uint4(0, 0, 0, 0);
         }
         if (tid < BN) {
             const int qr = qb + tid;
-            qcode_reg = qr < nb ? token_code(a.seg[ob + qr]) : 0;
-            qts_reg = qr < nb ? a.ts[ob + qr] : 0;
+            sQcode[tid] = qr < nb ? token_code(a.seg[ob + qr]) : 0;
+            sQts[tid] = qr < nb ? a.ts[ob + qr] : 0;
         }
-    };
-    auto sstore = [&]() {
-#pragma unroll
-        for (int i = 0; i < QCH; i++) {
-            const int c = tid + 256 * i, row = c / CPR, cc = c % CPR;
-            *(uint4*)&sQ[row * QP + cc * 8] = qreg[i];
-            *(uint4*)&sDO[row * QP + cc * 8] = goreg[i];
-        }
-        store_transposed<DH, RPT>(sQt, TP, qtreg, tcc, trg);
-        store_transposed<DH, RPT>(sDOt, TP, gotreg, tcc, trg);
-        if (tid < BN) {
-            sQcode[tid] = qcode_reg;
-            sQts[tid] = qts_reg;
-        }
-    };
-
-    int t = next_visible(0);
-    if (t < ntq) gload(t);
-    while (t < ntq) {
-        const int cls = klass(t);
         __syncthreads();
-        sstore();
-        __syncthreads();
-        const int tn = next_visible(t + 1);
-        if (tn < ntq) gload(tn);
 
-        // S (64 q x 32 keys) = Q K^T and dP = dO V^T: lane = key column, registers = queries.
-        floatx16 sacc[2], dpacc[2];
-        zero(sacc[0]); zero(sacc[1]); zero(dpacc[0]); zero(dpacc[1]);
 #pragma unroll
-        for (int kk = 0; kk < KSTEPS; kk++) {
+        for (int half = 0; half < 2; half++) {
+            // S (32 q x 32 keys) = Q K^T and dP = dO V^T: lane = key column, registers = queries.
+            floatx16 sacc, dpacc;
+            zero(sacc);
+            zero(dpacc);
 #pragma unroll
-            for (int qb = 0; qb < 2; qb++) {
-                const int off = (32 * qb + col) * QP + 16 * kk + 8 * hh;
+            for (int kk = 0; kk < KSTEPS; kk++) {
+                const int off = (32 * half + col) * QP + 16 * kk + 8 * hh;
                 const bf16x8 qa = *(const bf16x8*)&sQ[off];
                 const bf16x8 ga = *(const bf16x8*)&sDO[off];
-                sacc[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa, kreg[kk], sacc[qb], 0, 0, 0);
-                dpacc[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ga, vreg[kk], dpacc[qb], 0, 0, 0);
+                sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa, kreg[kk], sacc, 0, 0, 0);
+                dpacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ga, vreg[kk], dpacc, 0, 0, 0);
             }
-        }
-        uint32_t pk[4][4], dsk[4][4];
-#pragma unroll
-        for (int qb = 0; qb < 2; qb++) {
+            uint32_t pk[2][4], dsk[2][4];
 #pragma unroll
             for (int r = 0; r < 16; r += 2) {
                 float pv[2], dv[2];
 #pragma unroll
                 for (int e = 0; e < 2; e++) {
                     const int rr = r + e;
-                    const int ql = 32 * qb + 8 * (rr >> 2) + 4 * hh + (rr & 3);
-                    float x = sacc[qb][rr] * alpha;
+                    const int ql = 32 * half + 8 * (rr >> 2) + 4 * hh + (rr & 3);
+                    float x = sacc[rr] * alpha;
                     if (RAB) x += sRab[rab_bucket(sQts[ql], kts, a.nbuckets)];
                     float sg;
                     float p = silu_sig(x, sg) * inv_n;
-                    float ds = dpacc[qb][rr] * sg * (1.0f + x * (1.0f - sg)) * inv_n;
+                    float ds = dpacc[rr] * sg * (1.0f + x * (1.0f - sg)) * inv_n;
                     if (cls == TILE_PARTIAL) {
-                        const bool vis = visible(sQcode[ql], sQts[ql], t * BN + ql, kcode, kts, kj);
+                        const bool vis = visible(sQcode[ql], sQts[ql], qb + ql, kcode, kts, kj);
                         p = vis ? p : 0.f;
                         ds = vis ? ds : 0.f;
                     }
                     pv[e] = p;
                     dv[e] = ds;
                 }
-                pk[2 * qb + (r >> 3)][(r & 7) >> 1] = pack_bf16x2(pv[0], pv[1]);
-                dsk[2 * qb + (r >> 3)][(r & 7) >> 1] = pack_bf16x2(dv[0], dv[1]);
+                pk[r >> 3][(r & 7) >> 1] = pack_bf16x2(pv[0], pv[1]);
+                dsk[r >> 3][(r & 7) >> 1] = pack_bf16x2(dv[0], dv[1]);
+            }
+            // dV (32 keys x dh) += P^T dO ; dK += dS^T Q.  A = P^T / dS^T from registers,
+            // B = dO / Q read transposed (lane = feature column, slots = queries).
+#pragma unroll
+            for (int kq = 0; kq < 2; kq++) {
+                const bf16x8 pa = as_bf16x8(make_uint4(pk[kq][0], pk[kq][1], pk[kq][2], pk[kq][3]));
+                const bf16x8 da = as_bf16x8(make_uint4(dsk[kq][0], dsk[kq][1], dsk[kq][2], dsk[kq][3]));
+#pragma unroll
+                for (int d = 0; d < DBLK; d++) {
+                    const bf16x8 gb = lds_read_tr(sDO, QP, 32 * half + 16 * kq, 32 * d, lane);
+                    const bf16x8 qbv = lds_read_tr(sQ, QP, 32 * half + 16 * kq, 32 * d, lane);
+                    dvacc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pa, gb, dvacc[d], 0, 0, 0);
+                    dkacc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(da, qbv, dkacc[d], 0, 0, 0);
+                }
             }
         }
-        // dV (32 keys x dh) += P^T dO ; dK += dS^T Q.  A = P^T / dS^T straight from registers.
-#pragma unroll
-        for (int ks = 0; ks < 4; ks++) {
-            const bf16x8 pa = as_bf16x8(make_uint4(pk[ks][0], pk[ks][1], pk[ks][2], pk[ks][3]));
-            const bf16x8 da = as_bf16x8(make_uint4(dsk[ks][0], dsk[ks][1], dsk[ks][2], dsk[ks][3]));
-#pragma unroll
-            for (int d = 0; d < DBLK; d++) {
-                const bf16x8 gb = ld_tr8(&sDOt[(32 * d + col) * TP + 16 * ks + 4 * hh]);
-                const bf16x8 qbv = ld_tr8(&sQt[(32 * d + col) * TP + 16 * ks + 4 * hh]);
-                dvacc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pa, gb, dvacc[d], 0, 0, 0);
-                dkacc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(da, qbv, dkacc[d], 0, 0, 0);
-            }
-        }
-        t = tn;
     }
 
     // dK / dV accumulators: lane = feature column, registers = key rows.

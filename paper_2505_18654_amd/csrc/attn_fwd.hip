@@ -2,14 +2,15 @@
 //
 // bf16 kernel: one workgroup = 4 waves = 128 query rows of one (user, head); each wave owns
 // 32 query rows.  For every 64-key tile of the user that is not fully masked, K and V are
-// staged through LDS (V transposed) and the wave computes
-//     S^T (64 keys x 32 queries) = K Q^T          v_mfma_f32_32x32x16_bf16, Q held in VGPRs
+// staged row-major through LDS (the next tile's rows are fetched into registers while the
+// current one is computed) and the wave computes, per 32-key half of the tile,
+//     S^T (32 keys x 32 queries) = K Q^T          v_mfma_f32_32x32x16_bf16, Q held in VGPRs
 //     P = silu(alpha S + rab) / n_b, masked        in registers, straight from the accumulators
-//     O^T (dh x 32 queries)     += V^T P^T         P^T re-enters the MFMA as the B operand
+//     O^T (dh x 32 queries)     += V^T P^T         V^T read with ds_read_b64_tr_b16
 // Computing the transposed products lets the accumulator layout of S^T (lane = query column,
 // registers = keys) serve directly as the B operand of the second product, so P never goes
-// through LDS.  The mask is evaluated only on PARTIAL tiles, from segment codes and
-// timestamps staged with the keys; fully visible tiles take the unmasked path.
+// through LDS, and the transposing LDS read gives V^T without a transposed copy.  The mask
+// is evaluated only on PARTIAL tiles, from segment codes and timestamps staged with the keys.
 #include "mtgr_device.h"
 #include "mtgr_internal.h"
 
@@ -20,37 +21,28 @@ namespace {
 constexpr int BM = 128;   // query rows per workgroup
 constexpr int BN = 64;    // keys per tile
 
-template <int DH>
-struct FwdSmem {
-    static constexpr int KP = DH + 8;        // padded K row (elements)
-    static constexpr int VP = BN + 4;        // padded V^T row
-    static constexpr int OP = DH + 8;        // padded output staging row
-    static constexpr int KV_BYTES = BN * KP * 2 + DH * VP * 2;
-    static constexpr int O_BYTES = BM * OP * 2;
-    static constexpr int BYTES = KV_BYTES > O_BYTES ? KV_BYTES : O_BYTES;
-};
-
 __device__ __forceinline__ uint4 ldg16(const uint16_t* p) { return *(const uint4*)p; }
 
 }  // namespace
 
 template <int DH, bool RAB>
 __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
-    using SM = FwdSmem<DH>;
-    constexpr int KP = SM::KP, VP = SM::VP, OP = SM::OP;
+    constexpr int KP = DH + 8;        // padded LDS row (elements)
+    constexpr int OP = DH + 8;        // padded output staging row
     constexpr int KSTEPS = DH / 16;   // k-steps of S^T = K Q^T
     constexpr int DBLK = DH / 32;     // 32-row blocks of O^T
     constexpr int CPR = DH / 8;       // 16-byte chunks per row
     constexpr int KCH = BN * CPR / 256;
-    constexpr int RPT = DH / 32;      // V rows per thread in the transposed staging
-    static_assert(KCH == RPT, "staging layout");
+    constexpr int KV_BYTES = 2 * BN * KP * 2;
+    constexpr int O_BYTES = BM * OP * 2;
+    constexpr int BYTES = KV_BYTES > O_BYTES ? KV_BYTES : O_BYTES;
 
-    __shared__ __align__(16) char smem[SM::BYTES];
+    __shared__ __align__(16) char smem[BYTES];
     __shared__ int sKcode[BN];
     __shared__ int sKts[BN];
     __shared__ float sRab[MTGR_RAB_LDS];
     uint16_t* sK = (uint16_t*)smem;
-    uint16_t* sVt = (uint16_t*)(smem + BN * KP * 2);
+    uint16_t* sV = sK + BN * KP;
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int2 item = a.items[blockIdx.x];
@@ -101,23 +93,17 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
         return t;
     };
 
-    uint4 kreg[KCH], vreg[RPT];
+    uint4 kreg[KCH], vreg[KCH];
     int kcode_reg = 0, kts_reg = 0;
-    const int vcc = tid % CPR, vrg = tid / CPR;
     auto gload = [&](int t) {
         const int kb = t * BN;
 #pragma unroll
         for (int i = 0; i < KCH; i++) {
             const int c = tid + 256 * i, row = c / CPR, cc = c % CPR;
             const int key = kb + row;
-            kreg[i] = key < nb ? ldg16(K + (long long)(ob + key) * a.ld_k + h * DH + cc * 8)
-                               : make_uint4(0, 0, 0, 0);
-        }
-#pragma unroll
-        for (int r = 0; r < RPT; r++) {
-            const int key = kb + vrg * RPT + r;
-            vreg[r] = key < nb ? ldg16(V + (long long)(ob + key) * a.ld_v + h * DH + vcc * 8)
-                               : make_uint4(0, 0, 0, 0);
+            const bool ok = key < nb;
+            kreg[i] = ok ? ldg16(K + (long long)(ob + key) * a.ld_k + h * DH + cc * 8) : make_uint4(0, 0, 0, 0);
+            vreg[i] = ok ? ldg16(V + (long long)(ob + key) * a.ld_v + h * DH + cc * 8) : make_uint4(0, 0, 0, 0);
         }
         if (tid < BN) {
             const int key = kb + tid;
@@ -130,24 +116,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
         for (int i = 0; i < KCH; i++) {
             const int c = tid + 256 * i, row = c / CPR, cc = c % CPR;
             *(uint4*)&sK[row * KP + cc * 8] = kreg[i];
-        }
-#pragma unroll
-        for (int e = 0; e < 8; e++) {
-            uint16_t vals[RPT];
-#pragma unroll
-            for (int r = 0; r < RPT; r++) {
-                const uint32_t word = ((const uint32_t*)&vreg[r])[e >> 1];
-                vals[r] = (uint16_t)(word >> (16 * (e & 1)));
-            }
-            uint16_t* dst = &sVt[(vcc * 8 + e) * VP + vrg * RPT];
-            if constexpr (RPT == 4) {
-                *(uint2*)dst = make_uint2(vals[0] | ((uint32_t)vals[1] << 16),
-                                          vals[2] | ((uint32_t)vals[3] << 16));
-            } else if constexpr (RPT == 2) {
-                *(uint32_t*)dst = vals[0] | ((uint32_t)vals[1] << 16);
-            } else {
-                dst[0] = vals[0];
-            }
+            *(uint4*)&sV[row * KP + cc * 8] = vreg[i];
         }
         if (tid < BN) {
             sKcode[tid] = kcode_reg;
@@ -165,24 +134,18 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
         const int tn = next_visible(t + 1);
         if (tn < ntk) gload(tn);
 
-        floatx16 sacc[2];
-#pragma unroll
-        for (int blk = 0; blk < 2; blk++)
-#pragma unroll
-            for (int r = 0; r < 16; r++) sacc[blk][r] = 0.f;
-#pragma unroll
-        for (int kk = 0; kk < KSTEPS; kk++) {
-#pragma unroll
-            for (int blk = 0; blk < 2; blk++) {
-                const bf16x8 ka = *(const bf16x8*)&sK[(32 * blk + col) * KP + 16 * kk + 8 * hh];
-                sacc[blk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qreg[kk], sacc[blk], 0, 0, 0);
-            }
-        }
-
-        // P in bf16, already in B-operand order: pk[ks] holds keys 16ks + 8(s/4) + 4hh + s%4.
-        uint32_t pk[4][4];
 #pragma unroll
         for (int blk = 0; blk < 2; blk++) {
+            floatx16 sacc;
+#pragma unroll
+            for (int r = 0; r < 16; r++) sacc[r] = 0.f;
+#pragma unroll
+            for (int kk = 0; kk < KSTEPS; kk++) {
+                const bf16x8 ka = *(const bf16x8*)&sK[(32 * blk + col) * KP + 16 * kk + 8 * hh];
+                sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qreg[kk], sacc, 0, 0, 0);
+            }
+            // P in bf16 in B-operand order: pk[kq] holds keys 32 blk + 16 kq + 8(s/4) + 4hh + s%4.
+            uint32_t pk[2][4];
 #pragma unroll
             for (int r = 0; r < 16; r += 2) {
                 float pv[2];
@@ -190,7 +153,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
                 for (int e = 0; e < 2; e++) {
                     const int rr = r + e;
                     const int kl = 32 * blk + 8 * (rr >> 2) + 4 * hh + (rr & 3);
-                    float x = sacc[blk][rr] * alpha;
+                    float x = sacc[rr] * alpha;
                     if (RAB) x += sRab[rab_bucket(qts, sKts[kl], a.nbuckets)];
                     float sg;
                     float p = silu_sig(x, sg) * inv_n;
@@ -198,19 +161,16 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
                         p = visible(qcode, qts, qi, sKcode[kl], sKts[kl], t * BN + kl) ? p : 0.f;
                     pv[e] = p;
                 }
-                pk[2 * blk + (r >> 3)][(r & 7) >> 1] = pack_bf16x2(pv[0], pv[1]);
+                pk[r >> 3][(r & 7) >> 1] = pack_bf16x2(pv[0], pv[1]);
             }
-        }
 #pragma unroll
-        for (int ks = 0; ks < 4; ks++) {
-            const bf16x8 pb = as_bf16x8(make_uint4(pk[ks][0], pk[ks][1], pk[ks][2], pk[ks][3]));
+            for (int kq = 0; kq < 2; kq++) {
+                const bf16x8 pb = as_bf16x8(make_uint4(pk[kq][0], pk[kq][1], pk[kq][2], pk[kq][3]));
 #pragma unroll
-            for (int db = 0; db < DBLK; db++) {
-                const uint16_t* vrow = &sVt[(32 * db + col) * VP + 16 * ks + 4 * hh];
-                const uint2 lo = *(const uint2*)vrow;
-                const uint2 hi = *(const uint2*)(vrow + 8);
-                const bf16x8 va = as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y));
-                oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb, oacc[db], 0, 0, 0);
+                for (int db = 0; db < DBLK; db++) {
+                    const bf16x8 va = lds_read_tr(sV, KP, 32 * blk + 16 * kq, 32 * db, lane);
+                    oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb, oacc[db], 0, 0, 0);
+                }
             }
         }
         t = tn;

@@ -145,4 +145,26 @@ __device__ __forceinline__ int wave_max(int v) {
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 u) { return __builtin_bit_cast(bf16x8, u); }
 
+typedef short short4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) short4_t lds_short4;
+
+// MFMA 32x32x16 operand read "down the columns" of a row-major bf16 LDS tile with the
+// transposing load ds_read_b64_tr_b16.  Lane l receives column c0 + (l % 32) and, in its 8
+// k-slots, rows r0 + 4 (l / 32) + {0,1,2,3} (slots 0..3) and r0 + 8 + 4 (l / 32) + {0,1,2,3}
+// (slots 4..7): the row order of the 32x32 accumulator layout, so P^T / dS^T taken from an
+// accumulator pair with it slot for slot.  Within each 16-lane group, lane j = 4 s + q
+// supplies row (.. + s), columns (.. + 4 q .. 4 q + 3); the hardware hands lane i of the group
+// element i % 4 of supplier 4 s + i / 4 in slot s.  `ld` is the tile's row stride (elements,
+// a multiple of 4), r0 a multiple of 16 and c0 a multiple of 32.
+__device__ __forceinline__ bf16x8 lds_read_tr(const uint16_t* tile, int ld, int r0, int c0, int lane) {
+    const int j = lane & 15;
+    const int row = r0 + 4 * (lane >> 5) + (j >> 2);
+    const int colx = c0 + 16 * ((lane >> 4) & 1) + 4 * (j & 3);
+    const uint16_t* p = tile + row * ld + colx;
+    const short4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4*)p);
+    const short4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4*)(p + 8 * ld));
+    const short __attribute__((ext_vector_type(8))) v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    return __builtin_bit_cast(bf16x8, v);
+}
+
 }  // namespace mtgr

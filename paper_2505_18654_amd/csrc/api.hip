@@ -42,7 +42,7 @@ struct AttnLayout {
     int tile;            // rows per work item
     int ntile;           // 64-token summary tiles per user
     long long slots;     // physical work-list entries (= grid size)
-    size_t off_summ, off_items, off_sorted, total;
+    size_t off_summ, off_items, off_sorted, off_code, total;
 };
 
 AttnLayout attn_layout(const mtgr_hstu_problem_t* p) {
@@ -53,7 +53,8 @@ AttnLayout attn_layout(const mtgr_hstu_problem_t* p) {
     L.off_summ = 0;
     L.off_items = align256((size_t)p->num_users * L.ntile * sizeof(int4));
     L.off_sorted = L.off_items + align256((size_t)L.slots * sizeof(int2));
-    L.total = L.off_sorted + align256((size_t)p->num_users * sizeof(int));
+    L.off_code = L.off_sorted + align256((size_t)p->num_users * sizeof(int));
+    L.total = L.off_code + align256((size_t)p->total_tokens * sizeof(int));
     return L;
 }
 
@@ -155,6 +156,7 @@ mtgr::AttnArgs make_args(const mtgr_hstu_problem_t* p, const AttnLayout& L, cons
     a.ld_o = p->ld_o;
     char* ws = (char*)workspace;
     a.summ = (const int4*)(ws + L.off_summ);
+    a.tok_code = (const int*)(ws + L.off_code);
     a.items = (const int2*)(ws + L.off_items);
     a.ntile = L.ntile;
     a.heads = p->num_heads;
@@ -168,7 +170,7 @@ mtgr_status_t schedule(const mtgr_hstu_problem_t* p, const AttnLayout& L, const 
                        const int8_t* seg, const int32_t* ts, void* workspace, hipStream_t s) {
     char* ws = (char*)workspace;
     hipError_t e = mtgr::launch_tile_summaries(offsets, seg, ts, p->num_users, L.ntile,
-                                               (int4*)(ws + L.off_summ), s);
+                                               (int4*)(ws + L.off_summ), (int*)(ws + L.off_code), s);
     if (e != hipSuccess) return device_fail(e, "tile summaries");
     e = mtgr::launch_build_schedule(offsets, p->num_users, p->num_heads, L.tile,
                                     (int2*)(ws + L.off_items), (int)L.slots, (int*)(ws + L.off_sorted), s);

@@ -7,14 +7,15 @@
 // There is no softmax, so nothing is saved by the forward and no row statistic is needed.
 //
 // Two kernels, no atomics on dQ/dK/dV (results are deterministic):
-//   dq kernel (row-parallel, like the forward): per wave 32 queries, Q and dO in VGPRs;
-//     per 32-key half of a 64-key tile: S^T = K Q^T, dP^T = V dO^T, dS^T in registers,
-//     dQ^T += K^T dS^T with K^T read by ds_read_b64_tr_b16 from the row-major K tile.
-//     It also forms drab (LDS histogram, one global atomic per bucket per workgroup).
-//   dkdv kernel (column-parallel): per wave 32 keys, K and V in VGPRs; per 32-query half of
-//     a 64-query tile: S = Q K^T, dP = dO V^T (lane = key column), then dV += P^T dO and
-//     dK += dS^T Q with dO and Q read transposed from their row-major tiles.
-// Only row-major tiles live in LDS; every transposed operand comes from the transposing read.
+//   dq kernel (row-parallel, like the forward): per wave 32 queries, Q and dO in VGPRs; the
+//     user's visible 64-key tiles stream through two LDS buffers (global_load_lds); per
+//     32-key half: S^T = K Q^T, dP^T = V dO^T, dS^T in registers, dQ^T += K^T dS^T with K^T
+//     read by ds_read_b64_tr_b16.  It also forms drab (LDS histogram, one global atomic per
+//     bucket per workgroup).
+//   dkdv kernel (column-parallel): per wave 32 keys, K and V in VGPRs; the visible 64-query
+//     tiles of Q and dO stream through two LDS buffers; per 32-query half: S = Q K^T,
+//     dP = dO V^T (lane = key column), then dV += P^T dO and dK += dS^T Q with dO and Q read
+//     transposed from their row-major tiles.
 #include "mtgr_device.h"
 #include "mtgr_internal.h"
 
@@ -34,19 +35,15 @@ __device__ __forceinline__ void zero(floatx16& x) {
 // ------------------------------------------------------------------ dQ (+ drab), bf16
 template <int DH, bool RAB>
 __global__ __launch_bounds__(256, 2) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
-    constexpr int KP = DH + 8, OP = DH + 8;
-    constexpr int KSTEPS = DH / 16, DBLK = DH / 32, CPR = DH / 8;
-    constexpr int KCH = BN * CPR / 256;
-    constexpr int KV_BYTES = 2 * BN * KP * 2;
-    constexpr int O_BYTES = BM * OP * 2;
-    constexpr int BYTES = KV_BYTES > O_BYTES ? KV_BYTES : O_BYTES;
-    __shared__ __align__(16) char smem[BYTES];
-    __shared__ int sKcode[BN];
-    __shared__ int sKts[BN];
+    constexpr int CPR = DH / 8, KSTEPS = DH / 16, DBLK = DH / 32, TILE = BN * DH;
+    __shared__ __align__(16) uint16_t sK0[TILE];
+    __shared__ __align__(16) uint16_t sK1[TILE];
+    __shared__ __align__(16) uint16_t sV0[TILE];
+    __shared__ __align__(16) uint16_t sV1[TILE];
+    __shared__ int sKts[2][BN];
+    __shared__ int sKcode[2][BN];
     __shared__ float sRab[MTGR_RAB_LDS];
     __shared__ float sHist[MTGR_RAB_LDS];
-    uint16_t* sK = (uint16_t*)smem;
-    uint16_t* sV = sK + BN * KP;
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int2 item = a.items[blockIdx.x];
@@ -71,9 +68,9 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
         qts = a.ts[ob + qi];
     }
     const uint16_t* Q = (const uint16_t*)a.q;
-    const uint16_t* K = (const uint16_t*)a.k;
-    const uint16_t* V = (const uint16_t*)a.v;
     const uint16_t* DO = (const uint16_t*)a.dout;
+    const uint16_t* Kb = (const uint16_t*)a.k + (long long)ob * a.ld_k;
+    const uint16_t* Vb = (const uint16_t*)a.v + (long long)ob * a.ld_v;
     bf16x8 qreg[KSTEPS], doreg[KSTEPS];
 #pragma unroll
     for (int kk = 0; kk < KSTEPS; kk++) {
@@ -95,52 +92,32 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
 
     auto klass = [&](int t) {
         const bool overlap = (t * BN < q0 + BM) && (q0 < t * BN + BN);
-        return tile_class(sq, load_summary(summ, t), overlap);
+        return __builtin_amdgcn_readfirstlane(tile_class(sq, load_summary(summ, t), overlap));
     };
     auto next_visible = [&](int t) {
         while (t < ntk && klass(t) == TILE_MASKED) ++t;
         return t;
     };
-
-    uint4 kreg[KCH], vreg[KCH];
-    int kcode_reg = 0, kts_reg = 0;
-    auto gload = [&](int t) {
-        const int kb = t * BN;
-#pragma unroll
-        for (int i = 0; i < KCH; i++) {
-            const int c = tid + 256 * i, row = c / CPR, cc = c % CPR, key = kb + row;
-            const bool ok = key < nb;
-            kreg[i] = ok ? ldg16(K + (long long)(ob + key) * a.ld_k + h * DH + cc * 8) : make_uint4(0, 0, 0, 0);
-            vreg[i] = ok ? ldg16(V + (long long)(ob + key) * a.ld_v + h * DH + cc * 8) : make_uint4(0, 0, 0, 0);
-        }
-        if (tid < BN) {
-            const int key = kb + tid;
-            kcode_reg = key < nb ? token_code(a.seg[ob + key]) : 0;
-            kts_reg = key < nb ? a.ts[ob + key] : 0;
-        }
-    };
-    auto sstore = [&]() {
-#pragma unroll
-        for (int i = 0; i < KCH; i++) {
-            const int c = tid + 256 * i, row = c / CPR, cc = c % CPR;
-            *(uint4*)&sK[row * KP + cc * 8] = kreg[i];
-            *(uint4*)&sV[row * KP + cc * 8] = vreg[i];
-        }
-        if (tid < BN) {
-            sKcode[tid] = kcode_reg;
-            sKts[tid] = kts_reg;
-        }
+    auto issue = [&](int t, int buf) {
+        tile_dma<DH>(buf ? sK1 : sK0, Kb, a.ld_k, t * BN, nb, h * DH, tid);
+        tile_dma<DH>(buf ? sV1 : sV0, Vb, a.ld_v, t * BN, nb, h * DH, tid);
+        codes_dma(sKts[buf], sKcode[buf], a.ts + ob, a.tok_code + ob, t * BN, nb, tid);
     };
 
     int t = next_visible(0);
-    if (t < ntk) gload(t);
+    int cur = 0;
+    if (t < ntk) issue(t, 0);
     while (t < ntk) {
         const int cls = klass(t);
-        __syncthreads();
-        sstore();
+        wait_vmem();
+        if (tid < BN && t * BN + tid >= nb) sKcode[cur][tid] = 0;
         __syncthreads();
         const int tn = next_visible(t + 1);
-        if (tn < ntk) gload(tn);
+        if (tn < ntk) issue(tn, cur ^ 1);
+        const uint16_t* sK = cur ? sK1 : sK0;
+        const uint16_t* sV = cur ? sV1 : sV0;
+        const int* kts = sKts[cur];
+        const int* kcode = sKcode[cur];
 
 #pragma unroll
         for (int blk = 0; blk < 2; blk++) {
@@ -149,9 +126,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
             zero(dpacc);
 #pragma unroll
             for (int kk = 0; kk < KSTEPS; kk++) {
-                const int off = (32 * blk + col) * KP + 16 * kk + 8 * hh;
-                const bf16x8 ka = *(const bf16x8*)&sK[off];
-                const bf16x8 va = *(const bf16x8*)&sV[off];
+                const bf16x8 ka = tile_read8<CPR>(sK, 32 * blk + col, 2 * kk + hh);
+                const bf16x8 va = tile_read8<CPR>(sV, 32 * blk + col, 2 * kk + hh);
                 sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qreg[kk], sacc, 0, 0, 0);
                 dpacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, doreg[kk], dpacc, 0, 0, 0);
             }
@@ -166,14 +142,14 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
                     float x = sacc[rr] * alpha;
                     int bk = 0;
                     if (RAB) {
-                        bk = rab_bucket(qts, sKts[kl], a.nbuckets);
+                        bk = rab_bucket(qts, kts[kl], a.nbuckets);
                         x += sRab[bk];
                     }
                     float sg;
                     silu_sig(x, sg);
                     float ds = dpacc[rr] * sg * (1.0f + x * (1.0f - sg)) * inv_n;
                     if (cls == TILE_PARTIAL)
-                        ds = visible(qcode, qts, qi, sKcode[kl], sKts[kl], t * BN + kl) ? ds : 0.f;
+                        ds = visible(qcode, qts, qi, kcode[kl], kts[kl], t * BN + kl) ? ds : 0.f;
                     else if (!qvalid)
                         ds = 0.f;
                     if (want_drab && ds != 0.f) atomicAdd(&sHist[bk], ds);
@@ -186,23 +162,24 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
                 const bf16x8 db = as_bf16x8(make_uint4(dsk[kq][0], dsk[kq][1], dsk[kq][2], dsk[kq][3]));
 #pragma unroll
                 for (int d = 0; d < DBLK; d++) {
-                    const bf16x8 kt = lds_read_tr(sK, KP, 32 * blk + 16 * kq, 32 * d, lane);
+                    const bf16x8 kt = tile_read_tr<CPR>(sK, 32 * blk + 16 * kq, 32 * d, lane);
                     dqacc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kt, db, dqacc[d], 0, 0, 0);
                 }
             }
         }
+        __syncthreads();
         t = tn;
+        cur ^= 1;
     }
 
-    __syncthreads();
     if (want_drab && tid < a.nbuckets && sHist[tid] != 0.f) atomicAdd(&a.drab[h * a.nbuckets + tid], sHist[tid]);
-    uint16_t* sO = (uint16_t*)smem;
+    uint16_t* sO = (w < 2 ? sK0 : sK1) + (w & 1) * 32 * DH;
 #pragma unroll
     for (int d = 0; d < DBLK; d++) {
 #pragma unroll
         for (int g = 0; g < 4; g++) {
             const int dd = 32 * d + 8 * g + 4 * hh;
-            *(uint2*)&sO[(w * 32 + col) * OP + dd] =
+            *(uint2*)&sO[8 * tile_chunk<CPR>(col, dd >> 3) + (dd & 7)] =
                 make_uint2(pack_bf16x2(alpha * dqacc[d][4 * g + 0], alpha * dqacc[d][4 * g + 1]),
                            pack_bf16x2(alpha * dqacc[d][4 * g + 2], alpha * dqacc[d][4 * g + 3]));
         }
@@ -215,25 +192,21 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
         const int qr = q0 + w * 32 + row;
         if (qr < nb)
             *(uint4*)(DQ + (long long)(ob + qr) * a.ld_q + h * DH + cc * 8) =
-                *(const uint4*)&sO[(w * 32 + row) * OP + cc * 8];
+                *(const uint4*)&sO[8 * tile_chunk<CPR>(row, cc)];
     }
 }
 
 // ------------------------------------------------------------------ dK, dV, bf16
 template <int DH, bool RAB>
 __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) {
-    constexpr int QP = DH + 8, OP = DH + 8;
-    constexpr int KSTEPS = DH / 16, DBLK = DH / 32, CPR = DH / 8;
-    constexpr int QCH = BN * CPR / 256;
-    constexpr int T_BYTES = 2 * BN * QP * 2;
-    constexpr int O_BYTES = BM * OP * 2;
-    constexpr int BYTES = T_BYTES > O_BYTES ? T_BYTES : O_BYTES;
-    __shared__ __align__(16) char smem[BYTES];
-    __shared__ int sQcode[BN];
-    __shared__ int sQts[BN];
+    constexpr int CPR = DH / 8, KSTEPS = DH / 16, DBLK = DH / 32, TILE = BN * DH;
+    __shared__ __align__(16) uint16_t sQ0[TILE];
+    __shared__ __align__(16) uint16_t sQ1[TILE];
+    __shared__ __align__(16) uint16_t sG0[TILE];
+    __shared__ __align__(16) uint16_t sG1[TILE];
+    __shared__ int sQts[2][BN];
+    __shared__ int sQcode[2][BN];
     __shared__ float sRab[MTGR_RAB_LDS];
-    uint16_t* sQ = (uint16_t*)smem;
-    uint16_t* sDO = sQ + BN * QP;
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int2 item = a.items[blockIdx.x];
@@ -257,10 +230,10 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
         kcode = token_code(a.seg[ob + kj]);
         kts = a.ts[ob + kj];
     }
-    const uint16_t* Q = (const uint16_t*)a.q;
     const uint16_t* K = (const uint16_t*)a.k;
     const uint16_t* V = (const uint16_t*)a.v;
-    const uint16_t* DO = (const uint16_t*)a.dout;
+    const uint16_t* Qb = (const uint16_t*)a.q + (long long)ob * a.ld_q;
+    const uint16_t* Gb = (const uint16_t*)a.dout + (long long)ob * a.ld_o;
     bf16x8 kreg[KSTEPS], vreg[KSTEPS];
 #pragma unroll
     for (int kk = 0; kk < KSTEPS; kk++) {
@@ -280,33 +253,39 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
         zero(dvacc[i]);
     }
 
+    // A query tile that runs past the user's end holds copies of its last row; it must take
+    // the masked path so that those rows contribute nothing.
     auto klass = [&](int t) {
         const bool overlap = (t * BN < k0 + BM) && (k0 < t * BN + BN);
-        return tile_class(load_summary(summ, t), sk, overlap);
+        int c = tile_class(load_summary(summ, t), sk, overlap);
+        if (c == TILE_FULL && t * BN + BN > nb) c = TILE_PARTIAL;
+        return __builtin_amdgcn_readfirstlane(c);
+    };
+    auto next_visible = [&](int t) {
+        while (t < ntq && klass(t) == TILE_MASKED) ++t;
+        return t;
+    };
+    auto issue = [&](int t, int buf) {
+        tile_dma<DH>(buf ? sQ1 : sQ0, Qb, a.ld_q, t * BN, nb, h * DH, tid);
+        tile_dma<DH>(buf ? sG1 : sG0, Gb, a.ld_o, t * BN, nb, h * DH, tid);
+        codes_dma(sQts[buf], sQcode[buf], a.ts + ob, a.tok_code + ob, t * BN, nb, tid);
     };
 
-    // No register prefetch here (the K/V operands and both accumulators fill the budget of
-    // two waves per SIMD); the second workgroup on the CU covers the load latency.
-    for (int t = 0; t < ntq; t++) {
+    int t = next_visible(0);
+    int cur = 0;
+    if (t < ntq) issue(t, 0);
+    while (t < ntq) {
         const int cls = klass(t);
-        if (cls == TILE_MASKED) continue;
+        wait_vmem();
+        if (tid < BN && t * BN + tid >= nb) sQcode[cur][tid] = 0;
+        __syncthreads();
+        const int tn = next_visible(t + 1);
+        if (tn < ntq) issue(tn, cur ^ 1);
+        const uint16_t* sQ = cur ? sQ1 : sQ0;
+        const uint16_t* sG = cur ? sG1 : sG0;
+        const int* qts = sQts[cur];
+        const int* qcode = sQcode[cur];
         const int qb = t * BN;
-        __syncthreads();
-#pragma unroll
-        for (int i = 0; i < QCH; i++) {
-            const int c = tid + 256 * i, row = c / CPR, cc = c % CPR, qr = qb + row;
-            const bool ok = qr < nb;
-            *(uint4*)&sQ[row * QP + cc * 8] =
-                ok ? ldg16(Q + (long long)(ob + qr) * a.ld_q + h * DH + cc * 8) : make_uint4(0, 0, 0, 0);
-            *(uint4*)&sDO[row * QP + cc * 8] =
-                ok ? ldg16(DO + (long long)(ob + qr) * a.ld_o + h * DH + cc * 8) : make_uint4(0, 0, 0, 0);
-        }
-        if (tid < BN) {
-            const int qr = qb + tid;
-            sQcode[tid] = qr < nb ? token_code(a.seg[ob + qr]) : 0;
-            sQts[tid] = qr < nb ? a.ts[ob + qr] : 0;
-        }
-        __syncthreads();
 
 #pragma unroll
         for (int half = 0; half < 2; half++) {
@@ -316,9 +295,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
             zero(dpacc);
 #pragma unroll
             for (int kk = 0; kk < KSTEPS; kk++) {
-                const int off = (32 * half + col) * QP + 16 * kk + 8 * hh;
-                const bf16x8 qa = *(const bf16x8*)&sQ[off];
-                const bf16x8 ga = *(const bf16x8*)&sDO[off];
+                const bf16x8 qa = tile_read8<CPR>(sQ, 32 * half + col, 2 * kk + hh);
+                const bf16x8 ga = tile_read8<CPR>(sG, 32 * half + col, 2 * kk + hh);
                 sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa, kreg[kk], sacc, 0, 0, 0);
                 dpacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ga, vreg[kk], dpacc, 0, 0, 0);
             }
@@ -331,12 +309,12 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
                     const int rr = r + e;
                     const int ql = 32 * half + 8 * (rr >> 2) + 4 * hh + (rr & 3);
                     float x = sacc[rr] * alpha;
-                    if (RAB) x += sRab[rab_bucket(sQts[ql], kts, a.nbuckets)];
+                    if (RAB) x += sRab[rab_bucket(qts[ql], kts, a.nbuckets)];
                     float sg;
                     float p = silu_sig(x, sg) * inv_n;
                     float ds = dpacc[rr] * sg * (1.0f + x * (1.0f - sg)) * inv_n;
                     if (cls == TILE_PARTIAL) {
-                        const bool vis = visible(sQcode[ql], sQts[ql], qb + ql, kcode, kts, kj);
+                        const bool vis = visible(qcode[ql], qts[ql], qb + ql, kcode, kts, kj);
                         p = vis ? p : 0.f;
                         ds = vis ? ds : 0.f;
                     }
@@ -354,17 +332,21 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
                 const bf16x8 da = as_bf16x8(make_uint4(dsk[kq][0], dsk[kq][1], dsk[kq][2], dsk[kq][3]));
 #pragma unroll
                 for (int d = 0; d < DBLK; d++) {
-                    const bf16x8 gb = lds_read_tr(sDO, QP, 32 * half + 16 * kq, 32 * d, lane);
-                    const bf16x8 qbv = lds_read_tr(sQ, QP, 32 * half + 16 * kq, 32 * d, lane);
+                    const bf16x8 gb = tile_read_tr<CPR>(sG, 32 * half + 16 * kq, 32 * d, lane);
+                    const bf16x8 qbv = tile_read_tr<CPR>(sQ, 32 * half + 16 * kq, 32 * d, lane);
                     dvacc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pa, gb, dvacc[d], 0, 0, 0);
                     dkacc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(da, qbv, dkacc[d], 0, 0, 0);
                 }
             }
         }
+        __syncthreads();
+        t = tn;
+        cur ^= 1;
     }
 
-    // dK / dV accumulators: lane = feature column, registers = key rows.
-    uint16_t* sO = (uint16_t*)smem;
+    // dK / dV accumulators: lane = feature column, registers = key rows.  Each wave stages
+    // its 32 rows in a swizzled 32-row tile inside the Q buffers.
+    uint16_t* sO = (w < 2 ? sQ0 : sQ1) + (w & 1) * 32 * DH;
     uint16_t* DK = (uint16_t*)a.dk;
     uint16_t* DV = (uint16_t*)a.dv;
 #pragma unroll
@@ -374,9 +356,10 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
         for (int d = 0; d < DBLK; d++) {
 #pragma unroll
             for (int r = 0; r < 16; r++) {
-                const int krow = w * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
+                const int krow = 8 * (r >> 2) + 4 * hh + (r & 3);
+                const int dd = 32 * d + col;
                 const float val = which == 0 ? alpha * dkacc[d][r] : dvacc[d][r];
-                sO[krow * OP + 32 * d + col] = (uint16_t)f32_to_bf16_bits(val);
+                sO[8 * tile_chunk<CPR>(krow, dd >> 3) + (dd & 7)] = (uint16_t)f32_to_bf16_bits(val);
             }
         }
         __syncthreads();
@@ -388,7 +371,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
             const int kr = k0 + w * 32 + row;
             if (kr < nb)
                 *(uint4*)(dst + (long long)(ob + kr) * ld + h * DH + cc * 8) =
-                    *(const uint4*)&sO[(w * 32 + row) * OP + cc * 8];
+                    *(const uint4*)&sO[8 * tile_chunk<CPR>(row, cc)];
         }
     }
 }

@@ -1,16 +1,19 @@
 // Forward of the jagged dynamic-mask SiLU attention (Eq. 5, Sec. 4.2).
 //
 // bf16 kernel: one workgroup = 4 waves = 128 query rows of one (user, head); each wave owns
-// 32 query rows.  For every 64-key tile of the user that is not fully masked, K and V are
-// staged row-major through LDS (the next tile's rows are fetched into registers while the
-// current one is computed) and the wave computes, per 32-key half of the tile,
+// 32 query rows.  The user's 64-key tiles that are not fully masked stream through two LDS
+// buffers: while the waves compute on one tile, the next tile's K and V rows (and its
+// timestamps and mask codes) are copied straight from global memory into the other buffer
+// (global_load_lds, no staging registers).  Per 32-key half of a tile each wave computes
 //     S^T (32 keys x 32 queries) = K Q^T          v_mfma_f32_32x32x16_bf16, Q held in VGPRs
 //     P = silu(alpha S + rab) / n_b, masked        in registers, straight from the accumulators
 //     O^T (dh x 32 queries)     += V^T P^T         V^T read with ds_read_b64_tr_b16
 // Computing the transposed products lets the accumulator layout of S^T (lane = query column,
 // registers = keys) serve directly as the B operand of the second product, so P never goes
 // through LDS, and the transposing LDS read gives V^T without a transposed copy.  The mask
-// is evaluated only on PARTIAL tiles, from segment codes and timestamps staged with the keys.
+// is evaluated only on PARTIAL tiles.
+#include <type_traits>
+
 #include "mtgr_device.h"
 #include "mtgr_internal.h"
 
@@ -27,22 +30,18 @@ __device__ __forceinline__ uint4 ldg16(const uint16_t* p) { return *(const uint4
 
 template <int DH, bool RAB>
 __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
-    constexpr int KP = DH + 8;        // padded LDS row (elements)
-    constexpr int OP = DH + 8;        // padded output staging row
+    constexpr int CPR = DH / 8;       // 16-byte chunks per row
     constexpr int KSTEPS = DH / 16;   // k-steps of S^T = K Q^T
     constexpr int DBLK = DH / 32;     // 32-row blocks of O^T
-    constexpr int CPR = DH / 8;       // 16-byte chunks per row
-    constexpr int KCH = BN * CPR / 256;
-    constexpr int KV_BYTES = 2 * BN * KP * 2;
-    constexpr int O_BYTES = BM * OP * 2;
-    constexpr int BYTES = KV_BYTES > O_BYTES ? KV_BYTES : O_BYTES;
+    constexpr int TILE = BN * DH;     // elements of one 64-row tile
 
-    __shared__ __align__(16) char smem[BYTES];
-    __shared__ int sKcode[BN];
-    __shared__ int sKts[BN];
+    __shared__ __align__(16) uint16_t sK0[TILE];
+    __shared__ __align__(16) uint16_t sK1[TILE];
+    __shared__ __align__(16) uint16_t sV0[TILE];
+    __shared__ __align__(16) uint16_t sV1[TILE];
+    __shared__ int sKts[2][BN];
+    __shared__ int sKcode[2][BN];
     __shared__ float sRab[MTGR_RAB_LDS];
-    uint16_t* sK = (uint16_t*)smem;
-    uint16_t* sV = sK + BN * KP;
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int2 item = a.items[blockIdx.x];
@@ -66,9 +65,9 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
         qcode = token_code(a.seg[ob + qi]);
         qts = a.ts[ob + qi];
     }
+    const uint16_t* Kb = (const uint16_t*)a.k + (long long)ob * a.ld_k;
+    const uint16_t* Vb = (const uint16_t*)a.v + (long long)ob * a.ld_v;
     const uint16_t* Q = (const uint16_t*)a.q;
-    const uint16_t* K = (const uint16_t*)a.k;
-    const uint16_t* V = (const uint16_t*)a.v;
     bf16x8 qreg[KSTEPS];
 #pragma unroll
     for (int kk = 0; kk < KSTEPS; kk++) {
@@ -84,107 +83,124 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
 #pragma unroll
         for (int r = 0; r < 16; r++) oacc[i][r] = 0.f;
 
+    // Tile classes are wave-uniform: readfirstlane keeps them in scalar registers so the
+    // per-element mask test compiles to a scalar branch per tile.
     auto klass = [&](int t) {
         const bool overlap = (t * BN < q0 + BM) && (q0 < t * BN + BN);
-        return tile_class(sq, load_summary(summ, t), overlap);
+        return __builtin_amdgcn_readfirstlane(tile_class(sq, load_summary(summ, t), overlap));
     };
     auto next_visible = [&](int t) {
         while (t < ntk && klass(t) == TILE_MASKED) ++t;
         return t;
     };
-
-    uint4 kreg[KCH], vreg[KCH];
-    int kcode_reg = 0, kts_reg = 0;
-    auto gload = [&](int t) {
-        const int kb = t * BN;
-#pragma unroll
-        for (int i = 0; i < KCH; i++) {
-            const int c = tid + 256 * i, row = c / CPR, cc = c % CPR;
-            const int key = kb + row;
-            const bool ok = key < nb;
-            kreg[i] = ok ? ldg16(K + (long long)(ob + key) * a.ld_k + h * DH + cc * 8) : make_uint4(0, 0, 0, 0);
-            vreg[i] = ok ? ldg16(V + (long long)(ob + key) * a.ld_v + h * DH + cc * 8) : make_uint4(0, 0, 0, 0);
-        }
-        if (tid < BN) {
-            const int key = kb + tid;
-            kcode_reg = key < nb ? token_code(a.seg[ob + key]) : 0;
-            kts_reg = key < nb ? a.ts[ob + key] : 0;
-        }
-    };
-    auto sstore = [&]() {
-#pragma unroll
-        for (int i = 0; i < KCH; i++) {
-            const int c = tid + 256 * i, row = c / CPR, cc = c % CPR;
-            *(uint4*)&sK[row * KP + cc * 8] = kreg[i];
-            *(uint4*)&sV[row * KP + cc * 8] = vreg[i];
-        }
-        if (tid < BN) {
-            sKcode[tid] = kcode_reg;
-            sKts[tid] = kts_reg;
-        }
+    auto issue = [&](int t, int buf) {
+        tile_dma<DH>(buf ? sK1 : sK0, Kb, a.ld_k, t * BN, nb, h * DH, tid);
+        tile_dma<DH>(buf ? sV1 : sV0, Vb, a.ld_v, t * BN, nb, h * DH, tid);
+        codes_dma(sKts[buf], sKcode[buf], a.ts + ob, a.tok_code + ob, t * BN, nb, tid);
     };
 
     int t = next_visible(0);
-    if (t < ntk) gload(t);
+    int cur = 0;
+    if (t < ntk) issue(t, 0);
     while (t < ntk) {
         const int cls = klass(t);
-        __syncthreads();
-        sstore();
-        __syncthreads();
+        wait_vmem();                                   // this wave's copies of tile t landed
+        if (tid < BN && t * BN + tid >= nb) sKcode[cur][tid] = 0;
+        __syncthreads();                               // ... and every other wave's
         const int tn = next_visible(t + 1);
-        if (tn < ntk) gload(tn);
+        if (tn < ntk) issue(tn, cur ^ 1);              // overlaps the compute below
+        const uint16_t* sK = cur ? sK1 : sK0;
+        const uint16_t* sV = cur ? sV1 : sV0;
+        const int* kts = sKts[cur];
+        const int* kcode = sKcode[cur];
 
+        // One straight-line body per tile class (the branch is per tile, not per element), so
+        // the scheduler can overlap one half's SiLU epilogue with the other half's MFMAs.
+        auto body = [&](auto masked_tag) {
+            constexpr bool MASKED = decltype(masked_tag)::value;
+            // --- scores of both 32-key halves, operands read one k-step ahead
+            floatx16 sacc[2];
 #pragma unroll
-        for (int blk = 0; blk < 2; blk++) {
-            floatx16 sacc;
+            for (int blk = 0; blk < 2; blk++)
 #pragma unroll
-            for (int r = 0; r < 16; r++) sacc[r] = 0.f;
+                for (int r = 0; r < 16; r++) sacc[blk][r] = 0.f;
+            bf16x8 ka0 = tile_read8<CPR>(sK, col, hh);
+            bf16x8 ka1 = tile_read8<CPR>(sK, 32 + col, hh);
 #pragma unroll
             for (int kk = 0; kk < KSTEPS; kk++) {
-                const bf16x8 ka = *(const bf16x8*)&sK[(32 * blk + col) * KP + 16 * kk + 8 * hh];
-                sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qreg[kk], sacc, 0, 0, 0);
-            }
-            // P in bf16 in B-operand order: pk[kq] holds keys 32 blk + 16 kq + 8(s/4) + 4hh + s%4.
-            uint32_t pk[2][4];
-#pragma unroll
-            for (int r = 0; r < 16; r += 2) {
-                float pv[2];
-#pragma unroll
-                for (int e = 0; e < 2; e++) {
-                    const int rr = r + e;
-                    const int kl = 32 * blk + 8 * (rr >> 2) + 4 * hh + (rr & 3);
-                    float x = sacc[rr] * alpha;
-                    if (RAB) x += sRab[rab_bucket(qts, sKts[kl], a.nbuckets)];
-                    float sg;
-                    float p = silu_sig(x, sg) * inv_n;
-                    if (cls == TILE_PARTIAL)
-                        p = visible(qcode, qts, qi, sKcode[kl], sKts[kl], t * BN + kl) ? p : 0.f;
-                    pv[e] = p;
+                bf16x8 nx0 = ka0, nx1 = ka1;
+                if (kk + 1 < KSTEPS) {
+                    nx0 = tile_read8<CPR>(sK, col, 2 * kk + 2 + hh);
+                    nx1 = tile_read8<CPR>(sK, 32 + col, 2 * kk + 2 + hh);
                 }
-                pk[r >> 3][(r & 7) >> 1] = pack_bf16x2(pv[0], pv[1]);
+                sacc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka0, qreg[kk], sacc[0], 0, 0, 0);
+                sacc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka1, qreg[kk], sacc[1], 0, 0, 0);
+                ka0 = nx0;
+                ka1 = nx1;
+                __builtin_amdgcn_sched_barrier(0);
             }
+            // --- SiLU epilogue in quarters (8 keys each), p = (alpha s / n_b) / (1 + 2^(-alpha s log2 e))
+            const float c_exp = -1.4426950408889634f * alpha;
+            const float c_out = alpha * inv_n;
+            auto epilogue = [&](int blk, int q4, uint32_t* dst) {
 #pragma unroll
-            for (int kq = 0; kq < 2; kq++) {
-                const bf16x8 pb = as_bf16x8(make_uint4(pk[kq][0], pk[kq][1], pk[kq][2], pk[kq][3]));
+                for (int r = 8 * q4; r < 8 * q4 + 8; r += 2) {
+                    float pv[2];
+#pragma unroll
+                    for (int e = 0; e < 2; e++) {
+                        const int rr = r + e;
+                        const int kl = 32 * blk + 8 * (rr >> 2) + 4 * hh + (rr & 3);
+                        const float sv = sacc[blk][rr];
+                        float p;
+                        if (RAB) {
+                            const float x = sv * alpha + sRab[rab_bucket(qts, kts[kl], a.nbuckets)];
+                            float sg;
+                            p = silu_sig(x, sg) * inv_n;
+                        } else {
+                            p = (sv * c_out) * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(sv * c_exp));
+                        }
+                        if (MASKED) p = visible(qcode, qts, qi, kcode[kl], kts[kl], t * BN + kl) ? p : 0.f;
+                        pv[e] = p;
+                    }
+                    dst[(r & 7) >> 1] = pack_bf16x2(pv[0], pv[1]);
+                }
+            };
+            // --- O^T += V^T P^T, 16 keys (one k-step) at a time; each group of 4 MFMAs is
+            // followed by the epilogue of the next 16 keys, which the MFMAs do not depend on.
+            uint32_t pk[4][4];
+            epilogue(0, 0, pk[0]);
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int ks = 0; ks < 4; ks++) {
+                const int blk = ks >> 1, kq = ks & 1;
+                const bf16x8 pb = as_bf16x8(make_uint4(pk[ks][0], pk[ks][1], pk[ks][2], pk[ks][3]));
 #pragma unroll
                 for (int db = 0; db < DBLK; db++) {
-                    const bf16x8 va = lds_read_tr(sV, KP, 32 * blk + 16 * kq, 32 * db, lane);
+                    const bf16x8 va = tile_read_tr<CPR>(sV, 32 * blk + 16 * kq, 32 * db, lane);
                     oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb, oacc[db], 0, 0, 0);
                 }
+                if (ks + 1 < 4) epilogue((ks + 1) >> 1, (ks + 1) & 1, pk[ks + 1]);
+                __builtin_amdgcn_sched_barrier(0);
             }
-        }
+        };
+        if (cls == TILE_PARTIAL)
+            body(std::true_type{});
+        else
+            body(std::false_type{});
+        __syncthreads();                               // buffer `cur` is refilled next round
         t = tn;
+        cur ^= 1;
     }
 
-    // Output: O^T accumulators -> bf16 rows staged in LDS -> 16-byte coalesced stores.
-    __syncthreads();
-    uint16_t* sO = (uint16_t*)smem;
+    // Output: O^T accumulators -> bf16 rows of this wave staged in LDS (swizzled 32-row
+    // tile inside the K buffers) -> 16-byte coalesced stores.
+    uint16_t* sO = (w < 2 ? sK0 : sK1) + (w & 1) * 32 * DH;
 #pragma unroll
     for (int db = 0; db < DBLK; db++) {
 #pragma unroll
         for (int g = 0; g < 4; g++) {
             const int d = 32 * db + 8 * g + 4 * hh;
-            *(uint2*)&sO[(w * 32 + col) * OP + d] =
+            *(uint2*)&sO[8 * tile_chunk<CPR>(col, d >> 3) + (d & 7)] =
                 make_uint2(pack_bf16x2(oacc[db][4 * g + 0], oacc[db][4 * g + 1]),
                            pack_bf16x2(oacc[db][4 * g + 2], oacc[db][4 * g + 3]));
         }
@@ -197,7 +213,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
         const int qr = q0 + w * 32 + row;
         if (qr < nb)
             *(uint4*)(O + (long long)(ob + qr) * a.ld_o + h * DH + cc * 8) =
-                *(const uint4*)&sO[(w * 32 + row) * OP + cc * 8];
+                *(const uint4*)&sO[8 * tile_chunk<CPR>(row, cc)];
     }
 }
 

@@ -147,24 +147,84 @@ __device__ __forceinline__ bf16x8 as_bf16x8(uint4 u) { return __builtin_bit_cast
 
 typedef short short4_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) short4_t lds_short4;
+typedef __attribute__((address_space(3))) void lds_void;
 
-// MFMA 32x32x16 operand read "down the columns" of a row-major bf16 LDS tile with the
+// ---------------------------------------------------------------- swizzled LDS tiles
+// A tile holds 64 rows of DH bf16 without padding; row r's 16-byte chunk c is stored at chunk
+// position  r * CPR + (c ^ swz(r)),  CPR = DH / 8.  The XOR spreads a column of 16 rows over
+// all 16 four-bank groups (conflict-free 16-byte row reads) and 4 consecutive rows x 2 adjacent
+// chunks over 8 distinct groups (conflict-free transposing reads).
+template <int CPR>
+__device__ __forceinline__ int swz(int row) {
+    return (((row & 7) << 1) | ((row >> 3) & 1)) & (CPR - 1);
+}
+
+template <int CPR>
+__device__ __forceinline__ int tile_chunk(int row, int chunk) {
+    return row * CPR + (chunk ^ swz<CPR>(row));
+}
+
+// 8 bf16 (16 bytes) of row `row`, logical chunk `chunk`.
+template <int CPR>
+__device__ __forceinline__ bf16x8 tile_read8(const uint16_t* tile, int row, int chunk) {
+    return *(const bf16x8*)(tile + 8 * tile_chunk<CPR>(row, chunk));
+}
+
+// MFMA 32x32x16 operand read "down the columns" of a swizzled row-major bf16 tile with the
 // transposing load ds_read_b64_tr_b16.  Lane l receives column c0 + (l % 32) and, in its 8
 // k-slots, rows r0 + 4 (l / 32) + {0,1,2,3} (slots 0..3) and r0 + 8 + 4 (l / 32) + {0,1,2,3}
 // (slots 4..7): the row order of the 32x32 accumulator layout, so P^T / dS^T taken from an
 // accumulator pair with it slot for slot.  Within each 16-lane group, lane j = 4 s + q
 // supplies row (.. + s), columns (.. + 4 q .. 4 q + 3); the hardware hands lane i of the group
-// element i % 4 of supplier 4 s + i / 4 in slot s.  `ld` is the tile's row stride (elements,
-// a multiple of 4), r0 a multiple of 16 and c0 a multiple of 32.
-__device__ __forceinline__ bf16x8 lds_read_tr(const uint16_t* tile, int ld, int r0, int c0, int lane) {
+// element i % 4 of supplier 4 s + i / 4 in slot s.  r0 is a multiple of 16, c0 of 32.
+template <int CPR>
+__device__ __forceinline__ bf16x8 tile_read_tr(const uint16_t* tile, int r0, int c0, int lane) {
     const int j = lane & 15;
     const int row = r0 + 4 * (lane >> 5) + (j >> 2);
     const int colx = c0 + 16 * ((lane >> 4) & 1) + 4 * (j & 3);
-    const uint16_t* p = tile + row * ld + colx;
-    const short4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4*)p);
-    const short4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4*)(p + 8 * ld));
+    const uint16_t* p0 = tile + 8 * tile_chunk<CPR>(row, colx >> 3) + (colx & 7);
+    const uint16_t* p1 = tile + 8 * tile_chunk<CPR>(row + 8, colx >> 3) + (colx & 7);
+    const short4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4*)p0);
+    const short4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4*)p1);
     const short __attribute__((ext_vector_type(8))) v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
     return __builtin_bit_cast(bf16x8, v);
 }
+
+// Asynchronous copy of rows [row0, row0 + 64) of a [.., ld] bf16 matrix (columns col0 ..
+// col0 + DH) into a swizzled tile, straight from global memory to LDS (global_load_lds_dwordx4:
+// lane l of an instruction lands at the instruction's LDS base + 16 l).  Rows at or past
+// `nrows` are replaced by row nrows - 1, a valid row whose values the mask or a zero
+// multiplier neutralises.  Every wave of the 256-thread workgroup issues DH / 32 instructions.
+template <int DH>
+__device__ __forceinline__ void tile_dma(uint16_t* tile, const uint16_t* base, long long ld, int row0,
+                                         int nrows, int col0, int tid) {
+    constexpr int CPR = DH / 8;
+    const int lane = tid & 63, w = tid >> 6;
+#pragma unroll
+    for (int i = 0; i < DH / 32; i++) {
+        const int blk = __builtin_amdgcn_readfirstlane(i * 4 + w);   // 64-chunk block of the tile
+        const int pos = blk * 64 + lane;                              // chunk position in LDS
+        const int row = pos / CPR;
+        const int chunk = (pos % CPR) ^ swz<CPR>(row);
+        const int grow = min(row0 + row, nrows - 1);
+        const uint16_t* src = base + (long long)grow * ld + col0 + chunk * 8;
+        __builtin_amdgcn_global_load_lds((const void*)src, (lds_void*)(tile + blk * 512), 16, 0, 0);
+    }
+}
+
+// Timestamps and mask codes of 64 consecutive tokens into LDS (two 4-byte-per-lane DMA
+// instructions issued by wave 0).  Tokens at or past `ntok` are copied from token ntok - 1;
+// the caller zeroes their codes once the copy has landed.
+__device__ __forceinline__ void codes_dma(int* dst_ts, int* dst_code, const int* ts, const int* code,
+                                          int tok0, int ntok, int tid) {
+    if (tid < 64) {
+        const int t = min(tok0 + tid, ntok - 1);
+        __builtin_amdgcn_global_load_lds((const void*)(ts + t), (lds_void*)dst_ts, 4, 0, 0);
+        __builtin_amdgcn_global_load_lds((const void*)(code + t), (lds_void*)dst_code, 4, 0, 0);
+    }
+}
+
+// Wait for every outstanding vector-memory operation of this wave (including LDS DMA).
+__device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
 }  // namespace mtgr

@@ -24,6 +24,7 @@ struct AttnArgs {
     float* drab;
     long long ld_q, ld_k, ld_v, ld_o;
     const int4* summ;     // [B][ntile] per-64-token tile summaries
+    const int* tok_code;  // [T] per-token mask code (token_code of seg)
     const int2* items;    // work list: {user, (tile << 8) | head}, user < 0 = empty slot
     int ntile;
     int heads;
@@ -36,7 +37,7 @@ long long schedule_slots(long long total_tokens, int num_users, int max_seqlen, 
 
 // Launchers; each returns the hipError_t of its launch.
 hipError_t launch_tile_summaries(const int* offsets, const int8_t* seg, const int* ts, int num_users,
-                                 int ntile, int4* summ, hipStream_t s);
+                                 int ntile, int4* summ, int* tok_code, hipStream_t s);
 hipError_t launch_build_schedule(const int* offsets, int num_users, int heads, int bm, int2* items,
                                  int slots, int* sorted_users, hipStream_t s);
 hipError_t launch_fill_f32(float* p, long long n, float value, hipStream_t s);

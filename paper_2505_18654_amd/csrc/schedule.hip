@@ -4,6 +4,8 @@
 //    the user's first token), the segment flags and the time range that decide whether a
 //    (query tile, key tile) pair is fully visible, partially visible or fully masked under
 //    the dynamic mask of Sec. 4.2.  Fully masked pairs are skipped by the attention kernels.
+//    It also writes each token's mask code (static / real-time / dynamic / valid bits), which
+//    the attention kernels copy into LDS next to the tile's timestamps.
 // 2. build_schedule: one work item per (user, head, tile of `bm` rows).  Users are sorted
 //    longest first (jagged lengths are long-tailed, Sec. 5 "Load balance"), (user, head)
 //    groups are dealt round-robin to the 8 XCDs so that all tiles of one group run on one
@@ -17,7 +19,8 @@ namespace mtgr {
 __global__ __launch_bounds__(256) void tile_summaries_kernel(const int* __restrict__ offsets,
                                                              const int8_t* __restrict__ seg,
                                                              const int* __restrict__ ts, int ntile,
-                                                             int4* __restrict__ summ) {
+                                                             int4* __restrict__ summ,
+                                                             int* __restrict__ tok_code) {
     const int b = blockIdx.y;
     const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
     const int lane = threadIdx.x & 63;
@@ -30,6 +33,7 @@ __global__ __launch_bounds__(256) void tile_summaries_kernel(const int* __restri
     if (valid) {
         sg = seg[ob + rel];
         tv = ts[ob + rel];
+        tok_code[ob + rel] = token_code(sg);
     }
     const bool is_static = valid && sg <= SEG_HIST;
     const bool is_rt = valid && sg == SEG_RT;
@@ -157,10 +161,10 @@ long long schedule_slots(long long total_tokens, int num_users, int max_seqlen, 
 }
 
 hipError_t launch_tile_summaries(const int* offsets, const int8_t* seg, const int* ts, int num_users,
-                                 int ntile, int4* summ, hipStream_t s) {
+                                 int ntile, int4* summ, int* tok_code, hipStream_t s) {
     if (num_users == 0 || ntile == 0) return hipSuccess;
     dim3 grid((ntile + 3) / 4, num_users);
-    tile_summaries_kernel<<<grid, 256, 0, s>>>(offsets, seg, ts, ntile, summ);
+    tile_summaries_kernel<<<grid, 256, 0, s>>>(offsets, seg, ts, ntile, summ, tok_code);
     return hipGetLastError();
 }
 

@@ -90,29 +90,26 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
 #pragma unroll
     for (int i = 0; i < DBLK; i++) zero(dqacc[i]);
 
-    auto klass = [&](int t) {
+    auto class_of = [&](int t) {
         const bool overlap = (t * BN < q0 + BM) && (q0 < t * BN + BN);
-        return __builtin_amdgcn_readfirstlane(tile_class(sq, load_summary(summ, t), overlap));
+        return tile_class(sq, load_summary(summ, t), overlap);
     };
-    auto next_visible = [&](int t) {
-        while (t < ntk && klass(t) == TILE_MASKED) ++t;
-        return t;
-    };
+    TileWalker<decltype(class_of)> walk(class_of, ntk);
     auto issue = [&](int t, int buf) {
         tile_dma<DH>(buf ? sK1 : sK0, Kb, a.ld_k, t * BN, nb, h * DH, tid);
         tile_dma<DH>(buf ? sV1 : sV0, Vb, a.ld_v, t * BN, nb, h * DH, tid);
         codes_dma(sKts[buf], sKcode[buf], a.ts + ob, a.tok_code + ob, t * BN, nb, tid);
     };
 
-    int t = next_visible(0);
+    int cls, cls_n;
+    int t = walk.next(0, &cls);
     int cur = 0;
     if (t < ntk) issue(t, 0);
     while (t < ntk) {
-        const int cls = klass(t);
         wait_vmem();
         if (tid < BN && t * BN + tid >= nb) sKcode[cur][tid] = 0;
         __syncthreads();
-        const int tn = next_visible(t + 1);
+        const int tn = walk.next(t + 1, &cls_n);
         if (tn < ntk) issue(tn, cur ^ 1);
         const uint16_t* sK = cur ? sK1 : sK0;
         const uint16_t* sV = cur ? sV1 : sV0;
@@ -169,6 +166,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
         }
         __syncthreads();
         t = tn;
+        cls = cls_n;
         cur ^= 1;
     }
 
@@ -255,31 +253,27 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
 
     // A query tile that runs past the user's end holds copies of its last row; it must take
     // the masked path so that those rows contribute nothing.
-    auto klass = [&](int t) {
+    auto class_of = [&](int t) {
         const bool overlap = (t * BN < k0 + BM) && (k0 < t * BN + BN);
-        int c = tile_class(load_summary(summ, t), sk, overlap);
-        if (c == TILE_FULL && t * BN + BN > nb) c = TILE_PARTIAL;
-        return __builtin_amdgcn_readfirstlane(c);
+        const int c = tile_class(load_summary(summ, t), sk, overlap);
+        return (c == TILE_FULL && t * BN + BN > nb) ? TILE_PARTIAL : c;
     };
-    auto next_visible = [&](int t) {
-        while (t < ntq && klass(t) == TILE_MASKED) ++t;
-        return t;
-    };
+    TileWalker<decltype(class_of)> walk(class_of, ntq);
     auto issue = [&](int t, int buf) {
         tile_dma<DH>(buf ? sQ1 : sQ0, Qb, a.ld_q, t * BN, nb, h * DH, tid);
         tile_dma<DH>(buf ? sG1 : sG0, Gb, a.ld_o, t * BN, nb, h * DH, tid);
         codes_dma(sQts[buf], sQcode[buf], a.ts + ob, a.tok_code + ob, t * BN, nb, tid);
     };
 
-    int t = next_visible(0);
+    int cls, cls_n;
+    int t = walk.next(0, &cls);
     int cur = 0;
     if (t < ntq) issue(t, 0);
     while (t < ntq) {
-        const int cls = klass(t);
         wait_vmem();
         if (tid < BN && t * BN + tid >= nb) sQcode[cur][tid] = 0;
         __syncthreads();
-        const int tn = next_visible(t + 1);
+        const int tn = walk.next(t + 1, &cls_n);
         if (tn < ntq) issue(tn, cur ^ 1);
         const uint16_t* sQ = cur ? sQ1 : sQ0;
         const uint16_t* sG = cur ? sG1 : sG0;
@@ -341,6 +335,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
         }
         __syncthreads();
         t = tn;
+        cls = cls_n;
         cur ^= 1;
     }
 

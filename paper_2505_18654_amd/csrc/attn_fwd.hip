@@ -83,31 +83,26 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
 #pragma unroll
         for (int r = 0; r < 16; r++) oacc[i][r] = 0.f;
 
-    // Tile classes are wave-uniform: readfirstlane keeps them in scalar registers so the
-    // per-element mask test compiles to a scalar branch per tile.
-    auto klass = [&](int t) {
+    auto class_of = [&](int t) {
         const bool overlap = (t * BN < q0 + BM) && (q0 < t * BN + BN);
-        return __builtin_amdgcn_readfirstlane(tile_class(sq, load_summary(summ, t), overlap));
+        return tile_class(sq, load_summary(summ, t), overlap);
     };
-    auto next_visible = [&](int t) {
-        while (t < ntk && klass(t) == TILE_MASKED) ++t;
-        return t;
-    };
+    TileWalker<decltype(class_of)> walk(class_of, ntk);
     auto issue = [&](int t, int buf) {
         tile_dma<DH>(buf ? sK1 : sK0, Kb, a.ld_k, t * BN, nb, h * DH, tid);
         tile_dma<DH>(buf ? sV1 : sV0, Vb, a.ld_v, t * BN, nb, h * DH, tid);
         codes_dma(sKts[buf], sKcode[buf], a.ts + ob, a.tok_code + ob, t * BN, nb, tid);
     };
 
-    int t = next_visible(0);
+    int cls, cls_n;
+    int t = walk.next(0, &cls);
     int cur = 0;
     if (t < ntk) issue(t, 0);
     while (t < ntk) {
-        const int cls = klass(t);
         wait_vmem();                                   // this wave's copies of tile t landed
         if (tid < BN && t * BN + tid >= nb) sKcode[cur][tid] = 0;
         __syncthreads();                               // ... and every other wave's
-        const int tn = next_visible(t + 1);
+        const int tn = walk.next(t + 1, &cls_n);
         if (tn < ntk) issue(tn, cur ^ 1);              // overlaps the compute below
         const uint16_t* sK = cur ? sK1 : sK0;
         const uint16_t* sV = cur ? sV1 : sV0;
@@ -189,6 +184,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
             body(std::false_type{});
         __syncthreads();                               // buffer `cur` is refilled next round
         t = tn;
+        cls = cls_n;
         cur ^= 1;
     }
 

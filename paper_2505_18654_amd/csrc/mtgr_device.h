@@ -70,6 +70,46 @@ __device__ __forceinline__ int tile_class(TileSummary sq, TileSummary sk, bool o
     return overlap ? TILE_PARTIAL : TILE_MASKED;
 }
 
+// Walks, in increasing order, the 64-token tiles of one user whose class against a fixed
+// tile range is not MASKED.  The classes of 64 consecutive tiles are evaluated at once, one tile
+// per lane, and kept as two wave-uniform bit masks, so stepping to the next visible tile costs a
+// few scalar bit operations and one summary load per 64 tiles instead of a dependent global load
+// per tile.  `ClassFn(t)` returns the class of tile t (t < ntile); all lanes must call next().
+template <class ClassFn>
+struct TileWalker {
+    ClassFn class_of;
+    int ntile;
+    int base;                  // first tile of the current window (multiple of 64)
+    unsigned long long vis;    // bit j: tile base + j is not MASKED
+    unsigned long long part;   // bit j: tile base + j is PARTIAL
+
+    __device__ TileWalker(ClassFn f, int n) : class_of(f), ntile(n), base(-64), vis(0), part(0) {}
+
+    __device__ void load(int b) {
+        base = b;
+        const int t = b + (int)(threadIdx.x & 63);
+        const int c = t < ntile ? class_of(t) : TILE_MASKED;
+        vis = __ballot(c != TILE_MASKED);
+        part = __ballot(c == TILE_PARTIAL);
+    }
+
+    // First visible tile >= t (ntile if none); its class in *cls.
+    __device__ int next(int t, int* cls) {
+        while (t < ntile) {
+            if (t >= base + 64) load(t & ~63);
+            const unsigned long long m = vis >> (t - base);
+            if (m) {
+                t += __builtin_ctzll(m);
+                *cls = ((part >> (t - base)) & 1ull) ? TILE_PARTIAL : TILE_FULL;
+                return t;
+            }
+            t = base + 64;
+        }
+        *cls = TILE_MASKED;
+        return ntile;
+    }
+};
+
 // Per-token mask code: bit0 static, bit1 real-time, bit2 dynamic (RT or CAND), bit3 valid.
 constexpr int KC_STATIC = 1, KC_RT = 2, KC_DYN = 4, KC_VALID = 8;
 

@@ -68,6 +68,8 @@ enum {
 #define MTGR_MAX_RAB_BUCKETS 64
 #define MTGR_MAX_HEADS 255
 #define MTGR_MAX_GROUPS 127
+#define MTGR_MAX_LD (1ll << 24)   /* largest attention token stride (elements); larger strides
+                                     return MTGR_ERROR_UNSUPPORTED */
 
 typedef void* mtgr_stream_t;            /* hipStream_t */
 
@@ -77,7 +79,7 @@ typedef void* mtgr_stream_t;            /* hipStream_t */
  *   alpha: multiplier of q.k inside the SiLU (Eq. 5 has none: pass 1.0).
  *   num_rab_buckets: 0 = no relative bias, else 1..64 (rab is [H][num_rab_buckets] fp32;
  *     a gap whose log-time bucket is >= num_rab_buckets uses the last bucket).
- *   ld_*: token strides in ELEMENTS (>= H*dh); q, k, v may be views into one fused
+ *   ld_*: token strides in ELEMENTS (>= H*dh, <= MTGR_MAX_LD); q, k, v may be views into one fused
  *     projection output.  Gradients share the layout of their primal:
  *     dq uses ld_q, dk ld_k, dv ld_v, and dout uses ld_o.
  *   flags: see MTGR_ATTN_PLANNED and MTGR_BWD_SKIP_*.

@@ -99,6 +99,9 @@ mtgr_status_t check_problem(const mtgr_hstu_problem_t* p) {
         if ((lds[i] * esz) % 16 != 0)
             return fail(MTGR_ERROR_INVALID_ARGUMENT, "%s %lld is not a multiple of 16 bytes", names[i],
                         lds[i]);
+        if (lds[i] > MTGR_MAX_LD)
+            return fail(MTGR_ERROR_UNSUPPORTED, "%s %lld above %lld elements", names[i], lds[i],
+                        (long long)MTGR_MAX_LD);
     }
     if (mtgr::schedule_slots(p->total_tokens, p->num_users, p->max_seqlen, p->num_heads,
                              mtgr::ATTN_TILE_F32) >= (1ll << 31))
@@ -316,6 +319,9 @@ mtgr_status_t check_gln(const mtgr_gln_problem_t* p) {
         if ((lds[i] * esz) % 16 != 0)
             return fail(MTGR_ERROR_INVALID_ARGUMENT, "%s %lld is not a multiple of 16 bytes", names[i],
                         lds[i]);
+        if (lds[i] > MTGR_MAX_LD)
+            return fail(MTGR_ERROR_UNSUPPORTED, "%s %lld above %lld elements", names[i], lds[i],
+                        (long long)MTGR_MAX_LD);
     }
     return MTGR_SUCCESS;
 }

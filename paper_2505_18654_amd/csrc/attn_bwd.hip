@@ -108,7 +108,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
     while (t < ntk) {
         wait_vmem();
         if (tid < BN && t * BN + tid >= nb) sKcode[cur][tid] = 0;
-        __syncthreads();
+        lds_barrier();
         const int tn = walk.next(t + 1, &cls_n);
         if (tn < ntk) issue(tn, cur ^ 1);
         const uint16_t* sK = cur ? sK1 : sK0;
@@ -164,7 +164,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
                 }
             }
         }
-        __syncthreads();
+        lds_barrier();
         t = tn;
         cls = cls_n;
         cur ^= 1;
@@ -260,9 +260,9 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
     };
     TileWalker<decltype(class_of)> walk(class_of, ntq);
     auto issue = [&](int t, int buf) {
-        tile_dma<DH>(buf ? sQ1 : sQ0, Qb, a.ld_q, t * BN, nb, h * DH, tid);
-        tile_dma<DH>(buf ? sG1 : sG0, Gb, a.ld_o, t * BN, nb, h * DH, tid);
-        codes_dma(sQts[buf], sQcode[buf], a.ts + ob, a.tok_code + ob, t * BN, nb, tid);
+        tile_dma_tracked<DH>(buf ? sQ1 : sQ0, Qb, a.ld_q, t * BN, nb, h * DH, tid);
+        tile_dma_tracked<DH>(buf ? sG1 : sG0, Gb, a.ld_o, t * BN, nb, h * DH, tid);
+        codes_dma_tracked(sQts[buf], sQcode[buf], a.ts + ob, a.tok_code + ob, t * BN, nb, tid);
     };
 
     int cls, cls_n;
@@ -272,7 +272,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
     while (t < ntq) {
         wait_vmem();
         if (tid < BN && t * BN + tid >= nb) sQcode[cur][tid] = 0;
-        __syncthreads();
+        lds_barrier();
         const int tn = walk.next(t + 1, &cls_n);
         if (tn < ntq) issue(tn, cur ^ 1);
         const uint16_t* sQ = cur ? sQ1 : sQ0;
@@ -333,7 +333,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
                 }
             }
         }
-        __syncthreads();
+        lds_barrier();
         t = tn;
         cls = cls_n;
         cur ^= 1;

@@ -1,21 +1,34 @@
 // Forward of the jagged dynamic-mask SiLU attention (Eq. 5, Sec. 4.2).
 //
 // bf16 kernel: one workgroup = 4 waves = 128 query rows of one (user, head); each wave owns
-// 32 query rows.  The user's 64-key tiles that are not fully masked stream through two LDS
-// buffers: while the waves compute on one tile, the next tile's K and V rows (and its
-// timestamps and mask codes) are copied straight from global memory into the other buffer
-// (global_load_lds, no staging registers).  Per 32-key half of a tile each wave computes
+// 32 query rows and walks the user's 64-key tiles that are not fully masked, 32 keys (one
+// "half") at a time.  Per half each wave computes
 //     S^T (32 keys x 32 queries) = K Q^T          v_mfma_f32_32x32x16_bf16, Q held in VGPRs
-//     P = silu(alpha S + rab) / n_b, masked        in registers, straight from the accumulators
-//     O^T (dh x 32 queries)     += V^T P^T         V^T read with ds_read_b64_tr_b16
-// Computing the transposed products lets the accumulator layout of S^T (lane = query column,
-// registers = keys) serve directly as the B operand of the second product, so P never goes
-// through LDS, and the transposing LDS read gives V^T without a transposed copy.  The mask
-// is evaluated only on PARTIAL tiles.
+//     P' = silu(alpha S + rab) * (alpha or 1)^-1, masked     in registers
+//     O^T (dh x 32 queries)     += V^T P'^T        V^T read with ds_read_b64_tr_b16
+// and O is scaled once by alpha / n_b (1 / n_b with a relative bias) at the end.  Computing
+// the transposed products lets the accumulator layout of S^T (lane = query column, registers
+// = keys) serve directly as the B operand of the second product, so P never goes through LDS,
+// and the transposing LDS read gives V^T without a transposed copy.  The mask is evaluated
+// only on PARTIAL tiles.
+//
+// Software pipeline: while a wave turns S of one half into P' (VALU and transcendental work)
+// it issues, one by one in between, the MFMAs of the NEXT half's S and of the current half's
+// P'V product, so the matrix cores and the vector ALUs of a wave run side by side (a wave's
+// MFMA and VALU instructions overlap; separate waves doing one each barely do on gfx950).
+// K runs one tile ahead of V in two LDS buffers each, filled straight from global memory
+// (global_load_lds) about one tile before use; two barriers per tile.
 #include <type_traits>
 
 #include "mtgr_device.h"
 #include "mtgr_internal.h"
+
+#ifndef MTGR_FWD_PF
+#define MTGR_FWD_PF 3
+#endif
+#ifndef MTGR_FWD_SB
+#define MTGR_FWD_SB 4
+#endif
 
 namespace mtgr {
 
@@ -30,17 +43,21 @@ __device__ __forceinline__ uint4 ldg16(const uint16_t* p) { return *(const uint4
 
 template <int DH, bool RAB>
 __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
-    constexpr int CPR = DH / 8;       // 16-byte chunks per row
-    constexpr int KSTEPS = DH / 16;   // k-steps of S^T = K Q^T
-    constexpr int DBLK = DH / 32;     // 32-row blocks of O^T
-    constexpr int TILE = BN * DH;     // elements of one 64-row tile
+    constexpr int CPR = DH / 8;          // 16-byte chunks per row
+    constexpr int KSTEPS = DH / 16;      // k-steps of S^T = K Q^T per 32-key half
+    constexpr int DBLK = DH / 32;        // 32-row blocks of O^T (MFMAs per 16-key PV step)
+    constexpr int TILE = BN * DH;        // elements of one 64-row tile
+    constexpr int NM = 2 * DBLK + KSTEPS;   // MFMA slots of one half-step
+    constexpr int EPM = 16 / NM;         // P' elements computed per slot
+    static_assert(NM * EPM == 16, "slot plan");
+    constexpr int NK = DH / 32;          // LDS-DMA instructions per wave for one tile
+    constexpr int PF = MTGR_FWD_PF;      // operand prefetch distance in MFMA slots
+    constexpr int SB = MTGR_FWD_SB;      // MFMA slots per scheduling region
 
-    __shared__ __align__(16) uint16_t sK0[TILE];
-    __shared__ __align__(16) uint16_t sK1[TILE];
-    __shared__ __align__(16) uint16_t sV0[TILE];
-    __shared__ __align__(16) uint16_t sV1[TILE];
-    __shared__ int sKts[2][BN];
-    __shared__ int sKcode[2][BN];
+    __shared__ __align__(16) uint16_t sK[2][TILE];
+    __shared__ __align__(16) uint16_t sV[2][TILE];
+    __shared__ int sVts[2][BN];          // timestamps / mask codes travel with the V tile
+    __shared__ int sVcode[2][BN];
     __shared__ float sRab[MTGR_RAB_LDS];
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -77,6 +94,17 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
     }
     if (RAB && tid < MTGR_RAB_LDS) sRab[tid] = tid < a.nbuckets ? a.rab[h * a.nbuckets + tid] : 0.f;
 
+    // Per-lane LDS byte offsets of the MFMA operands, shared by every tile and buffer: the
+    // K operand of k-step kk (row col, chunk 2 kk + hh; rows 32..63 add 32 * CPR * 16 bytes)
+    // and the two transposing-read supplier addresses of V^T column block db (row blocks of
+    // 16 keys add 16 * CPR * 16 bytes).
+    uint32_t kofs[KSTEPS], vofs0[DBLK], vofs1[DBLK];
+#pragma unroll
+    for (int kk = 0; kk < KSTEPS; kk++) kofs[kk] = tile_ofs<CPR>(col, 2 * kk + hh);
+#pragma unroll
+    for (int db = 0; db < DBLK; db++) tile_ofs_tr<CPR>(32 * db, lane, vofs0[db], vofs1[db]);
+    constexpr uint32_t ROW16 = 16u * CPR * 16u;   // bytes of 16 tile rows
+
     floatx16 oacc[DBLK];
 #pragma unroll
     for (int i = 0; i < DBLK; i++)
@@ -88,117 +116,215 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
         return tile_class(sq, load_summary(summ, t), overlap);
     };
     TileWalker<decltype(class_of)> walk(class_of, ntk);
-    auto issue = [&](int t, int buf) {
-        tile_dma<DH>(buf ? sK1 : sK0, Kb, a.ld_k, t * BN, nb, h * DH, tid);
-        tile_dma<DH>(buf ? sV1 : sV0, Vb, a.ld_v, t * BN, nb, h * DH, tid);
-        codes_dma(sKts[buf], sKcode[buf], a.ts + ob, a.tok_code + ob, t * BN, nb, tid);
+
+    auto issue_k = [&](int t, int buf) { tile_dma<DH>(sK[buf], Kb, a.ld_k, t * BN, nb, h * DH, tid); };
+    auto issue_v = [&](int t, int buf) {
+        tile_dma<DH>(sV[buf], Vb, a.ld_v, t * BN, nb, h * DH, tid);
+        codes_dma(sVts[buf], sVcode[buf], a.ts + ob, a.tok_code + ob, t * BN, nb, tid);
     };
 
-    int cls, cls_n;
-    int t = walk.next(0, &cls);
-    int cur = 0;
-    if (t < ntk) issue(t, 0);
-    while (t < ntk) {
-        wait_vmem();                                   // this wave's copies of tile t landed
-        if (tid < BN && t * BN + tid >= nb) sKcode[cur][tid] = 0;
-        __syncthreads();                               // ... and every other wave's
-        const int tn = walk.next(t + 1, &cls_n);
-        if (tn < ntk) issue(tn, cur ^ 1);              // overlaps the compute below
-        const uint16_t* sK = cur ? sK1 : sK0;
-        const uint16_t* sV = cur ? sV1 : sV0;
-        const int* kts = sKts[cur];
-        const int* kcode = sKcode[cur];
+    // p' for the accumulator value sv of key kl (relative to the tile):
+    // silu(alpha s) / alpha = s / (1 + 2^(-alpha s log2 e)), or silu(alpha s + rab).
+    const float c_exp = -1.4426950408889634f * alpha;
+    // qrel = qi - (first key of the tile) - 4 hh; the key of element e of half HC is the
+    // tile's key 32 HC + 8 (e / 4) + 4 hh + e % 4, so the diagonal test compares qrel with a
+    // compile-time constant.
+    auto p_of = [&](auto masked_tag, float sv, int kl, int kc, const int* kts, const int* kcode, int qrel) {
+        constexpr bool MASKED = decltype(masked_tag)::value;
+        float p;
+        if (RAB) {
+            const float x = sv * alpha + sRab[rab_bucket(qts, kts[kl], a.nbuckets)];
+            float sg;
+            p = silu_sig(x, sg);
+        } else {
+            p = sv * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(sv * c_exp));
+        }
+        if (MASKED) p = visible_diag(qcode, qts, kcode[kl], kts[kl], qrel == kc) ? p : 0.f;
+        return p;
+    };
 
-        // One straight-line body per tile class (the branch is per tile, not per element), so
-        // the scheduler can overlap one half's SiLU epilogue with the other half's MFMAs.
-        auto body = [&](auto masked_tag) {
-            constexpr bool MASKED = decltype(masked_tag)::value;
-            // --- scores of both 32-key halves, operands read one k-step ahead
-            floatx16 sacc[2];
-#pragma unroll
-            for (int blk = 0; blk < 2; blk++)
-#pragma unroll
-                for (int r = 0; r < 16; r++) sacc[blk][r] = 0.f;
-            bf16x8 ka0 = tile_read8<CPR>(sK, col, hh);
-            bf16x8 ka1 = tile_read8<CPR>(sK, 32 + col, hh);
-#pragma unroll
-            for (int kk = 0; kk < KSTEPS; kk++) {
-                bf16x8 nx0 = ka0, nx1 = ka1;
-                if (kk + 1 < KSTEPS) {
-                    nx0 = tile_read8<CPR>(sK, col, 2 * kk + 2 + hh);
-                    nx1 = tile_read8<CPR>(sK, 32 + col, 2 * kk + 2 + hh);
-                }
-                sacc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka0, qreg[kk], sacc[0], 0, 0, 0);
-                sacc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka1, qreg[kk], sacc[1], 0, 0, 0);
-                ka0 = nx0;
-                ka1 = nx1;
-                __builtin_amdgcn_sched_barrier(0);
-            }
-            // --- SiLU epilogue in quarters (8 keys each), p = (alpha s / n_b) / (1 + 2^(-alpha s log2 e))
-            const float c_exp = -1.4426950408889634f * alpha;
-            const float c_out = alpha * inv_n;
-            auto epilogue = [&](int blk, int q4, uint32_t* dst) {
-#pragma unroll
-                for (int r = 8 * q4; r < 8 * q4 + 8; r += 2) {
-                    float pv[2];
-#pragma unroll
-                    for (int e = 0; e < 2; e++) {
-                        const int rr = r + e;
-                        const int kl = 32 * blk + 8 * (rr >> 2) + 4 * hh + (rr & 3);
-                        const float sv = sacc[blk][rr];
-                        float p;
-                        if (RAB) {
-                            const float x = sv * alpha + sRab[rab_bucket(qts, kts[kl], a.nbuckets)];
-                            float sg;
-                            p = silu_sig(x, sg) * inv_n;
-                        } else {
-                            p = (sv * c_out) * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(sv * c_exp));
-                        }
-                        if (MASKED) p = visible(qcode, qts, qi, kcode[kl], kts[kl], t * BN + kl) ? p : 0.f;
-                        pv[e] = p;
-                    }
-                    dst[(r & 7) >> 1] = pack_bf16x2(pv[0], pv[1]);
-                }
-            };
-            // --- O^T += V^T P^T, 16 keys (one k-step) at a time; each group of 4 MFMAs is
-            // followed by the epilogue of the next 16 keys, which the MFMAs do not depend on.
-            uint32_t pk[4][4];
-            epilogue(0, 0, pk[0]);
-            __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-            for (int ks = 0; ks < 4; ks++) {
-                const int blk = ks >> 1, kq = ks & 1;
-                const bf16x8 pb = as_bf16x8(make_uint4(pk[ks][0], pk[ks][1], pk[ks][2], pk[ks][3]));
-#pragma unroll
-                for (int db = 0; db < DBLK; db++) {
-                    const bf16x8 va = tile_read_tr<CPR>(sV, 32 * blk + 16 * kq, 32 * db, lane);
-                    oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb, oacc[db], 0, 0, 0);
-                }
-                if (ks + 1 < 4) epilogue((ks + 1) >> 1, (ks + 1) & 1, pk[ks + 1]);
-                __builtin_amdgcn_sched_barrier(0);
-            }
+    // One half-step.  Consumes S of the current half (`cur`, keys 32 HC .. 32 HC + 31 of the
+    // tile in V buffer VB), adds its first 16 keys' P'V to O, and leaves the packed P' of its
+    // last 16 keys in pk_out (their PV MFMAs are issued by the caller: carried into the next
+    // half-step or flushed).  With CARRY it first issues the carried PV MFMAs of keys 16 .. 31
+    // (pk_in) of the same tile; with HAS_NEXT it computes the next half's S into `nxt` from
+    // rows 32 HN .. 32 HN + 31 of K buffer KB.  Buffer indices and halves are compile-time
+    // constants, so every LDS address is a per-lane base plus an immediate offset.  MFMA slot
+    // m (in issue order):
+    //   [0, DBLK)                       carried PV (k-step 1 of half 0)
+    //   [DBLK, DBLK + KSTEPS/2)         next S, k-steps 0 .. KSTEPS/2 - 1
+    //   [DBLK + KSTEPS/2, 2 DBLK + ...) PV of keys 32 HC .. 32 HC + 15
+    //   [2 DBLK + KSTEPS/2, NM)         next S, remaining k-steps
+    // and slot m first computes P' elements m EPM .. m EPM + EPM - 1 (registers of `cur`).
+    auto half_step = [&](auto carry_tag, auto next_tag, auto masked_tag, auto vb_tag, auto hc_tag,
+                         auto kb_tag, auto hn_tag, const floatx16& cur, floatx16& nxt,
+                         const uint32_t* pk_in, uint32_t* pk_out, int qrel) {
+        constexpr bool CARRY = decltype(carry_tag)::value;
+        constexpr bool HAS_NEXT = decltype(next_tag)::value;
+        constexpr int VB = decltype(vb_tag)::value, HC = decltype(hc_tag)::value;
+        constexpr int KB = decltype(kb_tag)::value, HN = decltype(hn_tag)::value;
+        const uint16_t* Vc = sV[VB];
+        const uint16_t* Kn = sK[KB];
+        const int* kts = sVts[VB];
+        const int* kcode = sVcode[VB];
+        uint32_t pk0[4];
+        float pv[16];
+        auto active = [&](int m) {
+            if (m < DBLK) return CARRY;
+            if (m < DBLK + KSTEPS / 2) return HAS_NEXT;
+            if (m < 2 * DBLK + KSTEPS / 2) return true;
+            return HAS_NEXT;
         };
-        if (cls == TILE_PARTIAL)
-            body(std::true_type{});
-        else
-            body(std::false_type{});
-        __syncthreads();                               // buffer `cur` is refilled next round
-        t = tn;
-        cls = cls_n;
-        cur ^= 1;
+        auto operand = [&](int m) {
+            if (m < DBLK) return lds_read_tr(Vc, vofs0[m] + ROW16, vofs1[m] + ROW16);
+            if (m < DBLK + KSTEPS / 2) return lds_read16(Kn, kofs[m - DBLK] + 2 * HN * ROW16);
+            if (m < 2 * DBLK + KSTEPS / 2) {
+                const int db = m - DBLK - KSTEPS / 2;
+                return lds_read_tr(Vc, vofs0[db] + 2 * HC * ROW16, vofs1[db] + 2 * HC * ROW16);
+            }
+            return lds_read16(Kn, kofs[m - 2 * DBLK] + 2 * HN * ROW16);
+        };
+        bf16x8 op[NM];
+#pragma unroll
+        for (int m = 0; m < PF && m < NM; m++)
+            if (active(m)) op[m] = operand(m);
+#pragma unroll
+        for (int m = 0; m < NM; m++) {
+            if (m + PF < NM && active(m + PF)) op[m + PF] = operand(m + PF);   // PF slots ahead
+#pragma unroll
+            for (int e = m * EPM; e < m * EPM + EPM; e++) {
+                const int kc = 32 * HC + 8 * (e >> 2) + (e & 3);
+                pv[e] = p_of(masked_tag, cur[e], kc + 4 * hh, kc, kts, kcode, qrel);
+                if (e & 1) {
+                    const uint32_t pp = pack_bf16x2(pv[e - 1], pv[e]);
+                    if (e < 8) pk0[e >> 1] = pp; else pk_out[(e - 8) >> 1] = pp;
+                }
+            }
+            if (m < DBLK) {
+                if (CARRY) {
+                    const bf16x8 pb = as_bf16x8(make_uint4(pk_in[0], pk_in[1], pk_in[2], pk_in[3]));
+                    oacc[m] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(op[m], pb, oacc[m], 0, 0, 0);
+                }
+            } else if (m < DBLK + KSTEPS / 2) {
+                if (HAS_NEXT) {
+                    const int kk = m - DBLK;
+                    nxt = __builtin_amdgcn_mfma_f32_32x32x16_bf16(op[m], qreg[kk], kk == 0 ? floatx16{} : nxt, 0, 0, 0);
+                }
+            } else if (m < 2 * DBLK + KSTEPS / 2) {
+                const int db = m - DBLK - KSTEPS / 2;
+                const bf16x8 pb = as_bf16x8(make_uint4(pk0[0], pk0[1], pk0[2], pk0[3]));
+                oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(op[m], pb, oacc[db], 0, 0, 0);
+            } else {
+                if (HAS_NEXT) {
+                    const int kk = m - 2 * DBLK;
+                    nxt = __builtin_amdgcn_mfma_f32_32x32x16_bf16(op[m], qreg[kk], nxt, 0, 0, 0);
+                }
+            }
+            if ((m + 1) % SB == 0) __builtin_amdgcn_sched_barrier(0);   // scheduling region
+        }
+    };
+    // Without a relative bias, masked scores are zeroed before the SiLU (silu(0) = 0 exactly),
+    // in a pass of their own on PARTIAL tiles, so that one epilogue serves every tile.
+    auto premask = [&](floatx16& cur, auto hc_tag, const int* kts, const int* kcode, int qrel) {
+        constexpr int HC = decltype(hc_tag)::value;
+#pragma unroll
+        for (int e = 0; e < 16; e++) {
+            const int kc = 32 * HC + 8 * (e >> 2) + (e & 3);
+            const int kl = kc + 4 * hh;
+            cur[e] = visible_diag(qcode, qts, kcode[kl], kts[kl], qrel == kc) ? cur[e] : 0.f;
+        }
+    };
+    using C0 = std::integral_constant<int, 0>;
+    using C1 = std::integral_constant<int, 1>;
+    using T = std::true_type;
+    using F = std::false_type;
+
+    int cls0, cls1;
+    int t0 = walk.next(0, &cls0);                                // t_i
+    if (t0 < ntk) {
+        int t1 = walk.next(t0 + 1, &cls1);                       // t_{i+1}
+        issue_k(t0, 0);
+        issue_v(t0, 0);
+        if (t1 < ntk) issue_k(t1, 1);
+        wait_vmem();
+        lds_barrier();
+        floatx16 sA, sB;                                         // S(t_i, keys 0..31) in sA
+#pragma unroll
+        for (int kk = 0; kk < KSTEPS; kk++)
+            sA = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_read16(sK[0], kofs[kk]), qreg[kk],
+                                                        kk == 0 ? floatx16{} : sA, 0, 0, 0);
+        // Tile t_i, whose K and V sit in buffers P (the tile loop is unrolled by two so that P
+        // is a compile-time constant).  Returns false after the last tile.
+        auto tile = [&](auto par) {
+            constexpr int P = decltype(par)::value;
+            using CP = std::integral_constant<int, P>;
+            using CQ = std::integral_constant<int, P ^ 1>;
+            // top: V(t_i) (and its codes) landed; K(t_{i+1}) may still be in flight
+            if (t1 < ntk) wait_vmcnt<NK>(); else wait_vmem();
+            if (tid < BN && t0 * BN + tid >= nb) sVcode[P][tid] = 0;
+            lds_barrier();
+            if (t1 < ntk) issue_v(t1, P ^ 1);                      // V(t_{i-1})'s buffer
+            const bool partial = cls0 == TILE_PARTIAL;
+            const int qrel = qi - t0 * BN - 4 * hh;
+            uint32_t pkA[4], pkB[4];
+            // half 0 of t_i; next S = half 1 of t_i (same K buffer)
+            if (!RAB && partial) premask(sA, C0{}, sVts[P], sVcode[P], qrel);
+            if (RAB && partial)
+                half_step(F{}, T{}, T{}, CP{}, C0{}, CP{}, C1{}, sA, sB, pkA, pkA, qrel);
+            else
+                half_step(F{}, T{}, F{}, CP{}, C0{}, CP{}, C1{}, sA, sB, pkA, pkA, qrel);
+            int cls2 = TILE_MASKED;
+            int t2 = ntk;
+            if (t1 < ntk) {
+                // middle: K(t_{i+1}) landed everywhere and K(t_i) is no longer read -> K(t_{i+2})
+                if (w == 0) wait_vmcnt<NK + 2>(); else wait_vmcnt<NK>();
+                lds_barrier();
+                t2 = walk.next(t1 + 1, &cls2);
+                if (t2 < ntk) issue_k(t2, P);
+                // half 1 of t_i; next S = half 0 of t_{i+1}
+                if (!RAB && partial) premask(sB, C1{}, sVts[P], sVcode[P], qrel);
+                if (RAB && partial)
+                    half_step(T{}, T{}, T{}, CP{}, C1{}, CQ{}, C0{}, sB, sA, pkA, pkB, qrel);
+                else
+                    half_step(T{}, T{}, F{}, CP{}, C1{}, CQ{}, C0{}, sB, sA, pkA, pkB, qrel);
+            } else {
+                if (!RAB && partial) premask(sB, C1{}, sVts[P], sVcode[P], qrel);
+                if (RAB && partial)
+                    half_step(T{}, F{}, T{}, CP{}, C1{}, CP{}, C0{}, sB, sA, pkA, pkB, qrel);
+                else
+                    half_step(T{}, F{}, F{}, CP{}, C1{}, CP{}, C0{}, sB, sA, pkA, pkB, qrel);
+            }
+            // PV of keys 48 .. 63
+            const bf16x8 pb = as_bf16x8(make_uint4(pkB[0], pkB[1], pkB[2], pkB[3]));
+#pragma unroll
+            for (int db = 0; db < DBLK; db++)
+                oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                    lds_read_tr(sV[P], vofs0[db] + 3 * ROW16, vofs1[db] + 3 * ROW16), pb, oacc[db], 0, 0, 0);
+            const bool more = t1 < ntk;
+            t0 = t1;
+            cls0 = cls1;
+            t1 = t2;
+            cls1 = cls2;
+            return more;
+        };
+        while (tile(C0{}) && tile(C1{})) {
+        }
+        __syncthreads();                                         // K buffers are reused below
     }
 
-    // Output: O^T accumulators -> bf16 rows of this wave staged in LDS (swizzled 32-row
-    // tile inside the K buffers) -> 16-byte coalesced stores.
-    uint16_t* sO = (w < 2 ? sK0 : sK1) + (w & 1) * 32 * DH;
+    // Output: O^T accumulators scaled by alpha / n_b (1 / n_b with a relative bias) -> bf16
+    // rows of this wave staged in LDS (swizzled 32-row tile inside the K buffers) -> 16-byte
+    // coalesced stores.
+    const float oscale = RAB ? inv_n : alpha * inv_n;
+    uint16_t* sO = sK[w >> 1] + (w & 1) * 32 * DH;
 #pragma unroll
     for (int db = 0; db < DBLK; db++) {
 #pragma unroll
         for (int g = 0; g < 4; g++) {
             const int d = 32 * db + 8 * g + 4 * hh;
             *(uint2*)&sO[8 * tile_chunk<CPR>(col, d >> 3) + (d & 7)] =
-                make_uint2(pack_bf16x2(oacc[db][4 * g + 0], oacc[db][4 * g + 1]),
-                           pack_bf16x2(oacc[db][4 * g + 2], oacc[db][4 * g + 3]));
+                make_uint2(pack_bf16x2(oacc[db][4 * g + 0] * oscale, oacc[db][4 * g + 1] * oscale),
+                           pack_bf16x2(oacc[db][4 * g + 2] * oscale, oacc[db][4 * g + 3] * oscale));
         }
     }
     __syncthreads();

@@ -132,6 +132,14 @@ __device__ __forceinline__ bool visible(int qcode, int qts, int qidx, int kcode,
     return (seen != 0) & (both_valid != 0);
 }
 
+// visible() with the diagonal test i == j already evaluated by the caller.
+__device__ __forceinline__ bool visible_diag(int qcode, int qts, int kcode, int kts, bool diag) {
+    const int both_valid = kcode & qcode & KC_VALID;
+    const int rule2 = (kcode & KC_RT) & ((qcode & KC_DYN) >> 1) & (kts < qts ? KC_RT : 0);
+    const int seen = (kcode & KC_STATIC) | (diag ? 1 : 0) | (rule2 >> 1);
+    return (seen != 0) & (both_valid != 0);
+}
+
 // Half-octave log-time bucket of |a - b| (gap as uint32), clamped to nb - 1.
 __device__ __forceinline__ int rab_bucket(int a, int b, int nb) {
     uint32_t g = a >= b ? (uint32_t)a - (uint32_t)b : (uint32_t)b - (uint32_t)a;
@@ -191,12 +199,18 @@ typedef __attribute__((address_space(3))) void lds_void;
 
 // ---------------------------------------------------------------- swizzled LDS tiles
 // A tile holds 64 rows of DH bf16 without padding; row r's 16-byte chunk c is stored at chunk
-// position  r * CPR + (c ^ swz(r)),  CPR = DH / 8.  The XOR spreads a column of 16 rows over
-// all 16 four-bank groups (conflict-free 16-byte row reads) and 4 consecutive rows x 2 adjacent
-// chunks over 8 distinct groups (conflict-free transposing reads).
+// position  r * CPR + (c ^ swz(r)),  CPR = DH / 8.  LDS has 64 banks of 4 bytes; a 16-byte
+// read (ds_read_b128) is served 16 lanes at a time and an 8-byte read (ds_read_b64_tr_b16)
+// 32 lanes at a time.  swz depends on r mod 16 only and is chosen (per CPR, by exhaustive
+// search over linear maps of the row bits) so that both operand patterns are conflict-free:
+// 16 consecutive rows at one chunk (MFMA operand rows) and 4 consecutive rows x 4 adjacent
+// chunks x 2 halves (the suppliers of one transposing read).
 template <int CPR>
 __device__ __forceinline__ int swz(int row) {
-    return (((row & 7) << 1) | ((row >> 3) & 1)) & (CPR - 1);
+    if constexpr (CPR == 16) return ((row & 3) << 2) | ((row >> 2) & 3);
+    else if constexpr (CPR == 8)
+        return ((row >> 1) & 1) | (((row >> 2) & 1) << 1) | ((((row >> 1) ^ (row >> 3)) & 1) << 2);
+    else return (row >> 2) & (CPR - 1);
 }
 
 template <int CPR>
@@ -230,20 +244,142 @@ __device__ __forceinline__ bf16x8 tile_read_tr(const uint16_t* tile, int r0, int
     return __builtin_bit_cast(bf16x8, v);
 }
 
+// ---------------------------------------------------------------- global -> LDS copies
+// global_load_lds_dwordx4 / _dword (lane l of one instruction lands at the LDS address in M0
+// plus 16 l, resp. 4 l) are issued through inline asm: the compiler then neither inserts
+// conservative "wait for every copy" counters before unrelated LDS reads nor sees the LDS
+// writes, and the kernels order the copies themselves with wait_vmcnt + lds_barrier.  M0 is
+// written only here (the kernels use no other M0 consumer).
+__device__ __forceinline__ uint32_t lds_address(const void* p) {
+    return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_void*)p);
+}
+
+// Pointer known to be equal in all lanes, moved to scalar registers.
+template <class T>
+__device__ __forceinline__ const T* uniform_ptr(const T* p) {
+    const unsigned long long v = (unsigned long long)(uintptr_t)p;
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+    return (const T*)(uintptr_t)(((unsigned long long)hi << 32) | lo);
+}
+
+// One copy instruction: source address = sbase (wave-uniform) + voff (per lane, bytes).
+__device__ __forceinline__ void lds_dma16(uint32_t lds_base, const void* sbase, uint32_t voff) {
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
+                 :: "s"(lds_base), "v"(voff), "s"(sbase) : "memory");
+}
+
+__device__ __forceinline__ void lds_dma4(uint32_t lds_base, const void* sbase, uint32_t voff) {
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dword %1, %2"
+                 :: "s"(lds_base), "v"(voff), "s"(sbase) : "memory");
+}
+
+// Wait until at most N vector-memory operations of this wave are outstanding; they complete
+// in issue order, so everything issued before the last N has landed (copies included).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    asm volatile("s_waitcnt vmcnt(%0)" :: "n"(N) : "memory");
+}
+
+__device__ __forceinline__ void wait_vmem() { wait_vmcnt<0>(); }
+
+// Workgroup barrier for LDS hand-offs: this wave's LDS reads and writes have completed, and
+// no other wave passes until all waves arrive.  Copies into LDS must be waited for first.
+__device__ __forceinline__ void lds_barrier() {
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// Byte offset, within a swizzled tile, of 16-byte chunk `chunk` of row `row`.
+template <int CPR>
+__device__ __forceinline__ uint32_t tile_ofs(int row, int chunk) {
+    return 16u * (uint32_t)tile_chunk<CPR>(row, chunk);
+}
+
+// Byte offsets of this lane's two ds_read_b64_tr_b16 supplier addresses for tile_read_tr with
+// r0 = 0 and column block c0 (a multiple of 32).  Since the swizzle depends on the row modulo
+// 16 only, the reads for row block r0 (a multiple of 16) are at these offsets plus
+// r0 * CPR * 16 bytes.
+template <int CPR>
+__device__ __forceinline__ void tile_ofs_tr(int c0, int lane, uint32_t& o0, uint32_t& o1) {
+    const int j = lane & 15;
+    const int row = 4 * (lane >> 5) + (j >> 2);
+    const int colx = c0 + 16 * ((lane >> 4) & 1) + 4 * (j & 3);
+    o0 = tile_ofs<CPR>(row, colx >> 3) + 2u * (uint32_t)(colx & 7);
+    o1 = tile_ofs<CPR>(row + 8, colx >> 3) + 2u * (uint32_t)(colx & 7);
+}
+
+// 16 bytes at byte offset `off` of an LDS tile.
+__device__ __forceinline__ bf16x8 lds_read16(const uint16_t* tile, uint32_t off) {
+    return *(const bf16x8*)((const char*)tile + off);
+}
+
+// tile_read_tr from precomputed supplier offsets (o0, o1) plus a constant byte offset.
+__device__ __forceinline__ bf16x8 lds_read_tr(const uint16_t* tile, uint32_t o0, uint32_t o1) {
+    const short4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4*)((const char*)tile + o0));
+    const short4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4*)((const char*)tile + o1));
+    const short __attribute__((ext_vector_type(8))) v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    return __builtin_bit_cast(bf16x8, v);
+}
+
 // Asynchronous copy of rows [row0, row0 + 64) of a [.., ld] bf16 matrix (columns col0 ..
-// col0 + DH) into a swizzled tile, straight from global memory to LDS (global_load_lds_dwordx4:
-// lane l of an instruction lands at the instruction's LDS base + 16 l).  Rows at or past
-// `nrows` are replaced by row nrows - 1, a valid row whose values the mask or a zero
-// multiplier neutralises.  Every wave of the 256-thread workgroup issues DH / 32 instructions.
+// col0 + DH) into a swizzled tile.  Rows at or past `nrows` are replaced by row nrows - 1, a
+// valid row whose values the mask or a zero multiplier neutralises.  Every wave of the
+// 256-thread workgroup issues DH / 32 instructions; instruction i of wave w fills the 64
+// chunks (16 bytes each) of LDS block 4 i + w, i.e. tile rows RPI i + (64 / CPR) w + lane / CPR
+// with RPI = 256 / CPR.  A lane's row within the block and its chunk (the swizzle depends on
+// row mod 16 only) are the same for every instruction, so each instruction needs one
+// wave-uniform base address and one per-lane 32-bit offset.  The caller guarantees
+// 64 * ld * 2 < 2^31.
 template <int DH>
 __device__ __forceinline__ void tile_dma(uint16_t* tile, const uint16_t* base, long long ld, int row0,
                                          int nrows, int col0, int tid) {
+    constexpr int CPR = DH / 8, RPI = 256 / CPR;
+    const int lane = tid & 63, w = tid >> 6;
+    const int rl = w * (64 / CPR) + lane / CPR;             // row within block 0 of this wave
+    const int cl = (lane % CPR) ^ swz<CPR>(rl);             // source chunk
+    const uint16_t* tbase = base + (long long)row0 * ld + col0;
+    const uint32_t ltile = __builtin_amdgcn_readfirstlane(lds_address(tile) + (uint32_t)w * 1024u);
+    if (row0 + 64 <= nrows) {
+        const uint32_t voff = (uint32_t)(rl * ld + cl * 8) * 2u;
+#pragma unroll
+        for (int i = 0; i < DH / 32; i++)
+            lds_dma16(ltile + (uint32_t)i * 4096u, uniform_ptr(tbase + (long long)i * RPI * ld), voff);
+    } else {
+        const int last = nrows - 1 - row0;                  // >= 0: the tile holds a valid row
+#pragma unroll
+        for (int i = 0; i < DH / 32; i++) {
+            const uint32_t voff = (uint32_t)(min(i * RPI + rl, last) * ld + cl * 8) * 2u;
+            lds_dma16(ltile + (uint32_t)i * 4096u, uniform_ptr(tbase), voff);
+        }
+    }
+}
+
+// Timestamps and mask codes of 64 consecutive tokens into LDS (two 4-byte-per-lane copies
+// issued by wave 0).  Tokens at or past `ntok` are copied from token ntok - 1; the caller
+// zeroes their codes once the copy has landed.
+__device__ __forceinline__ void codes_dma(int* dst_ts, int* dst_code, const int* ts, const int* code,
+                                          int tok0, int ntok, int tid) {
+    if (tid < 64) {
+        const uint32_t voff = (uint32_t)min(tid, ntok - 1 - tok0) * 4u;
+        lds_dma4(lds_address(dst_ts), uniform_ptr(ts + tok0), voff);
+        lds_dma4(lds_address(dst_code), uniform_ptr(code + tok0), voff);
+    }
+}
+
+// The same copies issued with the compiler builtin: the compiler then tracks them and waits for
+// every outstanding copy before the next LDS read it cannot prove disjoint.  Kept for the dK/dV
+// kernel, whose registers are at the limit: there the builtin form measured faster (its
+// addresses need fewer live registers than the scalar-base form above).
+template <int DH>
+__device__ __forceinline__ void tile_dma_tracked(uint16_t* tile, const uint16_t* base, long long ld,
+                                                 int row0, int nrows, int col0, int tid) {
     constexpr int CPR = DH / 8;
     const int lane = tid & 63, w = tid >> 6;
 #pragma unroll
     for (int i = 0; i < DH / 32; i++) {
-        const int blk = __builtin_amdgcn_readfirstlane(i * 4 + w);   // 64-chunk block of the tile
-        const int pos = blk * 64 + lane;                              // chunk position in LDS
+        const int blk = __builtin_amdgcn_readfirstlane(i * 4 + w);
+        const int pos = blk * 64 + lane;
         const int row = pos / CPR;
         const int chunk = (pos % CPR) ^ swz<CPR>(row);
         const int grow = min(row0 + row, nrows - 1);
@@ -252,19 +388,13 @@ __device__ __forceinline__ void tile_dma(uint16_t* tile, const uint16_t* base, l
     }
 }
 
-// Timestamps and mask codes of 64 consecutive tokens into LDS (two 4-byte-per-lane DMA
-// instructions issued by wave 0).  Tokens at or past `ntok` are copied from token ntok - 1;
-// the caller zeroes their codes once the copy has landed.
-__device__ __forceinline__ void codes_dma(int* dst_ts, int* dst_code, const int* ts, const int* code,
-                                          int tok0, int ntok, int tid) {
+__device__ __forceinline__ void codes_dma_tracked(int* dst_ts, int* dst_code, const int* ts,
+                                                  const int* code, int tok0, int ntok, int tid) {
     if (tid < 64) {
         const int t = min(tok0 + tid, ntok - 1);
         __builtin_amdgcn_global_load_lds((const void*)(ts + t), (lds_void*)dst_ts, 4, 0, 0);
         __builtin_amdgcn_global_load_lds((const void*)(code + t), (lds_void*)dst_code, 4, 0, 0);
     }
 }
-
-// Wait for every outstanding vector-memory operation of this wave (including LDS DMA).
-__device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
 }  // namespace mtgr

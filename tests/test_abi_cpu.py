@@ -63,6 +63,7 @@ def prob(**kw):
     (dict(rab_buckets=65), hstu.MTGR_ERROR_INVALID_ARGUMENT),
     (dict(ld_q=100), hstu.MTGR_ERROR_INVALID_ARGUMENT),        # below H*dh = 128
     (dict(ld_k=132), hstu.MTGR_ERROR_INVALID_ARGUMENT),        # 264 bytes: not 16-byte multiple
+    (dict(ld_v=(1 << 24) + 8), hstu.MTGR_ERROR_UNSUPPORTED),   # above MTGR_MAX_LD
     (dict(alpha=float("nan")), hstu.MTGR_ERROR_INVALID_ARGUMENT),
 ])
 def test_problem_validation(mutate, status):

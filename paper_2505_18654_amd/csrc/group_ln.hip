@@ -12,7 +12,7 @@ namespace mtgr {
 
 namespace {
 constexpr int WAVES = 4;            // forward: waves per workgroup
-constexpr int TOKENS_PER_WAVE = 16;  // forward: consecutive tokens per wave
+constexpr int TOKENS_PER_WAVE = 4;   // forward: consecutive tokens per wave
 constexpr int BWD_WAVES = 8;         // backward: waves per workgroup
 
 template <bool BF16>
@@ -73,24 +73,34 @@ __global__ __launch_bounds__(WAVES * 64) void gln_fwd_kernel(GlnArgs a) {
     const float inv_d = 1.0f / (float)d;
     float gam[NCH][N], bet[NCH][N];
     int gcur = -1;
-    for (long long t = t0; t < t0 + TOKENS_PER_WAVE && t < a.T; t++) {
-        float z[NCH][N];
-        float sum = 0.f;
+    // raw rows of the next token, loaded while the current one is normalised
+    float xr[NCH][N] = {}, ur[NCH][N] = {};
+    auto load_rows = [&](long long t) {
 #pragma unroll
         for (int c = 0; c < NCH; c++) {
             const int ch = lane + 64 * c;
             if (ch < nch) {
-                V::load(a.x, t * a.ld_x + ch * N, z[c]);
-                if (GATE) {
-                    float uu[N];
-                    V::load(a.u, t * a.ld_u + ch * N, uu);
+                V::load(a.x, t * a.ld_x + ch * N, xr[c]);
+                if (GATE) V::load(a.u, t * a.ld_u + ch * N, ur[c]);
+            }
+        }
+    };
+    const long long t_end = min(t0 + TOKENS_PER_WAVE, a.T);
+    if (t0 < t_end) load_rows(t0);
+    for (long long t = t0; t < t_end; t++) {
+        float z[NCH][N];
+        float sum = 0.f;
 #pragma unroll
-                    for (int i = 0; i < N; i++) z[c][i] *= uu[i];
-                }
+        for (int c = 0; c < NCH; c++) {
+#pragma unroll
+            for (int i = 0; i < N; i++) z[c][i] = GATE ? xr[c][i] * ur[c][i] : xr[c][i];
+            if (lane + 64 * c < nch) {
 #pragma unroll
                 for (int i = 0; i < N; i++) sum += z[c][i];
             }
         }
+        const int g = a.gid[t];
+        if (t + 1 < t_end) load_rows(t + 1);
         const float mean = wave_sum(sum) * inv_d;
         float sq = 0.f;
 #pragma unroll
@@ -105,7 +115,6 @@ __global__ __launch_bounds__(WAVES * 64) void gln_fwd_kernel(GlnArgs a) {
         }
         const float var = wave_sum(sq) * inv_d;
         const float rstd = rsqrtf(var + a.eps);
-        const int g = a.gid[t];
         if (g != gcur) {
             gcur = g;
 #pragma unroll
@@ -174,8 +183,10 @@ __global__ __launch_bounds__(BWD_WAVES * 64) void gln_bwd_kernel(GlnArgs a, floa
             }
         }
     };
-    // raw rows of the token being processed and of the next one
-    float xr[NCH][N], ur[NCH][N], yr[NCH][N];
+    // raw rows and statistics of the token being processed and of the next one
+    float xr[NCH][N] = {}, ur[NCH][N] = {}, yr[NCH][N] = {};
+    int gnext = 0;
+    float mnext = 0.f, rnext = 0.f;
     auto load_rows = [&](long long t) {
 #pragma unroll
         for (int c = 0; c < NCH; c++) {
@@ -186,6 +197,9 @@ __global__ __launch_bounds__(BWD_WAVES * 64) void gln_bwd_kernel(GlnArgs a, floa
                 if (GATE) V::load(a.u, t * a.ld_u + ch * N, ur[c]);
             }
         }
+        gnext = a.gid[t];
+        mnext = a.mean[t];
+        rnext = a.rstd[t];
     };
     if (t0 < t1) load_rows(t0);
     for (long long t = t0; t < t1; t++) {
@@ -198,8 +212,8 @@ __global__ __launch_bounds__(BWD_WAVES * 64) void gln_bwd_kernel(GlnArgs a, floa
                 dy[c][i] = yr[c][i];
                 uu[c][i] = GATE ? ur[c][i] : 1.f;
             }
-        const int g = a.gid[t];
-        const float mean = a.mean[t], rstd = a.rstd[t];
+        const int g = gnext;
+        const float mean = mnext, rstd = rnext;
         if (t + 1 < t1) load_rows(t + 1);
         if (g != gcur) {
             flush();

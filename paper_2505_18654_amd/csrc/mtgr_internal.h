@@ -71,7 +71,7 @@ struct GlnArgs {
     float* workspace;   // backward: per-workgroup dgamma/dbeta partials
 };
 
-constexpr int GLN_BWD_SLOTS = 512;            // target workgroups of the backward
+constexpr int GLN_BWD_SLOTS = 256;            // target workgroups of the backward (one per CU)
 constexpr int GLN_LDS_ACC_BYTES = 64 * 1024;  // largest per-workgroup accumulator kept in LDS
 void gln_bwd_partition(long long T, int* nslots, int* tokens_per_wave);
 size_t gln_bwd_workspace_bytes(long long T, int d, int G);

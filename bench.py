@@ -196,10 +196,11 @@ def main():
     db = torch.empty_like(gamma)
     dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
     drab = torch.empty_like(rab) if rab is not None else None
-    ws = ops.workspace_for(ops.attn_problem(jag, q, k, v, o, rab), "cuda")
+    ws = ops.workspace_for(ops.attn_problem(jag, q, k, v, o, rab), "cuda", backward=not fwd_only)
     gws = ops.gln_workspace(y, gamma.shape[0])
 
-    stages = ["plan", "attn_fwd", "gln_fwd"] + ([] if fwd_only else ["gln_bwd", "attn_bwd_dq", "attn_bwd_dkdv"])
+    # backward: the dK/dV kernel stores dS, then dQ is formed from it (two calls, timed apart)
+    stages = ["plan", "attn_fwd", "gln_fwd"] + ([] if fwd_only else ["gln_bwd", "attn_bwd_dkdv", "attn_bwd_dq"])
 
     def run(name):
         if name == "plan":
@@ -211,12 +212,12 @@ def main():
         elif name == "gln_bwd":
             ops.gln_bwd(inp["dy"], o.view(T, d), u, seg, gamma, mean, rstd, grads=(dx, du, dg, db),
                         workspace=gws)
-        elif name == "attn_bwd_dq":
-            ops.attn_bwd(q, k, v, dx.view(T, H, dh), jag, rab, grads=(dq, dk, dv, drab), workspace=ws,
-                         planned=True, parts="dq")
         elif name == "attn_bwd_dkdv":
             ops.attn_bwd(q, k, v, dx.view(T, H, dh), jag, rab, grads=(dq, dk, dv, drab), workspace=ws,
-                         planned=True, parts="dkdv")
+                         planned=True, parts="dkdv_keep_ds")
+        elif name == "attn_bwd_dq":
+            ops.attn_bwd(q, k, v, dx.view(T, H, dh), jag, rab, grads=(dq, dk, dv, drab), workspace=ws,
+                         planned=True, parts="dq_from_ds")
 
     for _ in range(args.warmup):
         for s in stages:
@@ -243,8 +244,10 @@ def main():
     tflops = (f_fwd + f_bwd) / (ms_step * 1e-3) / 1e12
 
     # dominant kernel and its roofline (algorithmic flops per launch / event-timed duration)
-    kflops = {"attn_fwd": f_fwd, "attn_bwd_dq": f_bwd / 2, "attn_bwd_dkdv": f_bwd / 2}
-    kname = {"attn_fwd": "attn_fwd_bf16_kernel", "attn_bwd_dq": "attn_bwd_dq_bf16_kernel",
+    # algorithmic split of F_bwd = 8 dh per pair: the dK/dV kernel forms dP, dV and dK (6 dh),
+    # the dQ kernel dQ (2 dh); recomputation of S is not counted
+    kflops = {"attn_fwd": f_fwd, "attn_bwd_dkdv": f_bwd * 3 / 4, "attn_bwd_dq": f_bwd / 4}
+    kname = {"attn_fwd": "attn_fwd_bf16_kernel", "attn_bwd_dq": "attn_bwd_dq_ds_bf16_kernel",
              "attn_bwd_dkdv": "attn_bwd_dkdv_bf16_kernel"}
     dom = max((s for s in kflops if s in stage_ms), key=lambda s: stage_ms[s])
     achieved = kflops[dom] / (stage_ms[dom] * 1e-3)

@@ -64,6 +64,13 @@ enum {
                                   (mtgr_hstu_attn_plan); skip rebuilding it */
 #define MTGR_BWD_SKIP_DQ 2u    /* backward: do not form dq (dq may be NULL) */
 #define MTGR_BWD_SKIP_DKDV 4u  /* backward: do not form dk, dv (both may be NULL) */
+#define MTGR_BWD_KEEP_DS 8u    /* backward with MTGR_BWD_SKIP_DQ: also leave dS in the
+                                  workspace (needs the backward = 1 workspace size) for a
+                                  later dq-only call with MTGR_BWD_DS_READY */
+#define MTGR_BWD_DS_READY 16u  /* backward with MTGR_BWD_SKIP_DKDV: form dq from the dS that
+                                  a previous MTGR_BWD_KEEP_DS call left in this workspace for
+                                  the same batch, plan and inputs; drab must be NULL (that
+                                  call formed it) */
 
 #define MTGR_MAX_RAB_BUCKETS 64
 #define MTGR_MAX_HEADS 255
@@ -111,8 +118,13 @@ typedef struct {
     int64_t ld_x, ld_u, ld_y;
 } mtgr_gln_problem_t;
 
-/* Bytes of device workspace needed by mtgr_hstu_attn_fwd (backward = 0) or
- * mtgr_hstu_attn_bwd (backward = 1) for problem `p`.  Pure host arithmetic. */
+/* Bytes of device workspace for problem `p`.  Pure host arithmetic.
+ *   backward = 0: the plan; enough for mtgr_hstu_attn_plan, _fwd and a backward that
+ *     recomputes S and dP in its dq kernel.
+ *   backward = 1: the plan plus room for dS as bf16 64 x 64 blocks (an upper bound of
+ *     H * sum_b ceil(n_b / 64)^2 blocks of 8 KB, from T, B and max_seqlen).  With it the
+ *     bf16 backward stores dS from its dk/dv kernel and forms dq from it (fewer operations;
+ *     the same values).  The first bytes have the backward = 0 layout, so one plan serves. */
 mtgr_status_t mtgr_hstu_attn_workspace_size(const mtgr_hstu_problem_t* p, int backward,
                                             size_t* bytes);
 
@@ -152,8 +164,16 @@ mtgr_status_t mtgr_hstu_attn_fwd(const mtgr_hstu_problem_t* p, const int32_t* of
  *   dv_j = sum_i M_ij silu(s_ij)/n_b dout_i,  dq_i = alpha sum_j dS_ij k_j,
  *   dk_j = alpha sum_i dS_ij q_i,  drab[h, x] = sum over pairs in bucket x of dS_ij.
  * The forward saves nothing (no softmax statistics), so the same inputs are passed.
- * dq and (dk, dv) come from two independent kernels; MTGR_BWD_SKIP_DQ / _DKDV launch
- * only one of them (drab is formed with dq).  The workspace is the forward's. */
+ * Two kernels, no atomics on dq/dk/dv (results are deterministic):
+ *   - workspace of at least mtgr_hstu_attn_workspace_size(p, 1) bytes (bf16): the dk/dv
+ *     kernel also stores dS (bf16, the operand of its dk product) in the workspace and a
+ *     second kernel forms dq = alpha sum_j dS_ij k_j from it;
+ *   - otherwise (at least the backward = 0 size; always for fp32): the dq kernel
+ *     recomputes S, dP and dS itself.
+ * MTGR_BWD_SKIP_DQ / _DKDV form only one side; with MTGR_BWD_KEEP_DS / _DS_READY the two
+ * halves of the stored-dS path can be issued as two calls.  drab is formed by the call
+ * that runs the dk/dv kernel, or by a dq-only call without MTGR_BWD_DS_READY (fp32: by the
+ * call that forms dq). */
 mtgr_status_t mtgr_hstu_attn_bwd(const mtgr_hstu_problem_t* p, const int32_t* offsets,
                                  const int8_t* seg, const int32_t* ts, const void* q,
                                  const void* k, const void* v, const float* rab,

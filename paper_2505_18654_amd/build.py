@@ -19,7 +19,8 @@ CSRC = os.path.join(HERE, "csrc")
 OBJ_DIR = os.path.join(HERE, "_build")
 LIB_NAME = "libmtgr_hstu.so"
 LIB_PATH = os.path.join(HERE, LIB_NAME)
-SOURCES = ["api.hip", "schedule.hip", "attn_fwd.hip", "attn_bwd.hip", "group_ln.hip"]
+SOURCES = ["api.hip", "schedule.hip", "attn_fwd.hip", "attn_bwd.hip", "attn_bwd_dq.hip",
+           "attn_bwd_dkdv.hip", "attn_bwd_dqds.hip", "group_ln.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 

@@ -42,7 +42,8 @@ struct AttnLayout {
     int tile;            // rows per work item
     int ntile;           // 64-token summary tiles per user
     long long slots;     // physical work-list entries (= grid size)
-    size_t off_summ, off_items, off_sorted, off_code, total;
+    size_t off_summ, off_items, off_sorted, off_code, off_dsoff, total;
+    size_t off_ds, total_bwd;   // stored-dS region (backward = 1 size)
 };
 
 AttnLayout attn_layout(const mtgr_hstu_problem_t* p) {
@@ -54,7 +55,13 @@ AttnLayout attn_layout(const mtgr_hstu_problem_t* p) {
     L.off_items = align256((size_t)p->num_users * L.ntile * sizeof(int4));
     L.off_sorted = L.off_items + align256((size_t)L.slots * sizeof(int2));
     L.off_code = L.off_sorted + align256((size_t)p->num_users * sizeof(int));
-    L.total = L.off_code + align256((size_t)p->total_tokens * sizeof(int));
+    L.off_dsoff = L.off_code + align256((size_t)p->total_tokens * sizeof(int));
+    L.total = L.off_dsoff + align256((size_t)(p->num_users + 1) * sizeof(long long));
+    // sum_b ceil(n_b/64)^2 <= ceil(max_seqlen/64) * sum_b ceil(n_b/64) <= ntile * (T/64 + B)
+    L.off_ds = L.total;
+    const size_t blocks = (size_t)p->num_heads * (size_t)L.ntile *
+                          (size_t)((p->total_tokens + 63) / 64 + p->num_users);
+    L.total_bwd = p->dtype == MTGR_DTYPE_BF16 ? L.off_ds + blocks * mtgr::DS_BLOCK_BYTES : L.total;
     return L;
 }
 
@@ -85,7 +92,8 @@ mtgr_status_t check_problem(const mtgr_hstu_problem_t* p) {
     if (p->num_rab_buckets < 0 || p->num_rab_buckets > MTGR_MAX_RAB_BUCKETS)
         return fail(MTGR_ERROR_INVALID_ARGUMENT, "num_rab_buckets %d outside 0..%d",
                     p->num_rab_buckets, MTGR_MAX_RAB_BUCKETS);
-    if (p->flags & ~(MTGR_ATTN_PLANNED | MTGR_BWD_SKIP_DQ | MTGR_BWD_SKIP_DKDV))
+    if (p->flags & ~(MTGR_ATTN_PLANNED | MTGR_BWD_SKIP_DQ | MTGR_BWD_SKIP_DKDV | MTGR_BWD_KEEP_DS |
+                     MTGR_BWD_DS_READY))
         return fail(MTGR_ERROR_INVALID_ARGUMENT, "unknown flags 0x%x", p->flags);
     if (!std::isfinite(p->alpha)) return fail(MTGR_ERROR_INVALID_ARGUMENT, "alpha is not finite");
     const long long row = (long long)p->num_heads * dh;
@@ -161,6 +169,8 @@ mtgr::AttnArgs make_args(const mtgr_hstu_problem_t* p, const AttnLayout& L, cons
     a.summ = (const int4*)(ws + L.off_summ);
     a.tok_code = (const int*)(ws + L.off_code);
     a.items = (const int2*)(ws + L.off_items);
+    a.ds_off = (const long long*)(ws + L.off_dsoff);
+    a.ds = (uint16_t*)(ws + L.off_ds);
     a.ntile = L.ntile;
     a.heads = p->num_heads;
     a.alpha = p->alpha;
@@ -178,6 +188,8 @@ mtgr_status_t schedule(const mtgr_hstu_problem_t* p, const AttnLayout& L, const 
     e = mtgr::launch_build_schedule(offsets, p->num_users, p->num_heads, L.tile,
                                     (int2*)(ws + L.off_items), (int)L.slots, (int*)(ws + L.off_sorted), s);
     if (e != hipSuccess) return device_fail(e, "schedule");
+    e = mtgr::launch_ds_offsets(offsets, p->num_users, p->num_heads, (long long*)(ws + L.off_dsoff), s);
+    if (e != hipSuccess) return device_fail(e, "dS offsets");
     return MTGR_SUCCESS;
 }
 
@@ -197,11 +209,11 @@ mtgr_status_t mtgr_hstu_attn_plan(const mtgr_hstu_problem_t* p, const int32_t* o
 }
 
 mtgr_status_t mtgr_hstu_attn_workspace_size(const mtgr_hstu_problem_t* p, int backward, size_t* bytes) {
-    (void)backward;
     if (!bytes) return fail(MTGR_ERROR_NULL_POINTER, "bytes is NULL");
     mtgr_status_t st = check_problem(p);
     if (st != MTGR_SUCCESS) return st;
-    *bytes = (p->num_users > 0 && p->total_tokens > 0) ? attn_layout(p).total : 0;
+    const AttnLayout L = attn_layout(p);
+    *bytes = (p->num_users > 0 && p->total_tokens > 0) ? (backward ? L.total_bwd : L.total) : 0;
     return ok();
 }
 
@@ -255,6 +267,14 @@ mtgr_status_t mtgr_hstu_attn_bwd(const mtgr_hstu_problem_t* p, const int32_t* of
     }
     const bool want_dq = !(p->flags & MTGR_BWD_SKIP_DQ);
     const bool want_dkdv = !(p->flags & MTGR_BWD_SKIP_DKDV);
+    const bool keep_ds = (p->flags & MTGR_BWD_KEEP_DS) != 0;
+    const bool ds_ready = (p->flags & MTGR_BWD_DS_READY) != 0;
+    if (keep_ds && want_dq)
+        return fail(MTGR_ERROR_INVALID_ARGUMENT, "MTGR_BWD_KEEP_DS needs MTGR_BWD_SKIP_DQ");
+    if (ds_ready && want_dkdv)
+        return fail(MTGR_ERROR_INVALID_ARGUMENT, "MTGR_BWD_DS_READY needs MTGR_BWD_SKIP_DKDV");
+    if (ds_ready && drab)
+        return fail(MTGR_ERROR_INVALID_ARGUMENT, "drab is formed by the MTGR_BWD_KEEP_DS call");
     REQUIRE_PTR(q, "q");
     REQUIRE_PTR(k, "k");
     REQUIRE_PTR(v, "v");
@@ -265,11 +285,23 @@ mtgr_status_t mtgr_hstu_attn_bwd(const mtgr_hstu_problem_t* p, const int32_t* of
         REQUIRE_PTR(dv, "dv");
     }
     const AttnLayout L = attn_layout(p);
+    // Stored-dS path: bf16 and a backward-size workspace.
+    const bool ds_path = p->dtype == MTGR_DTYPE_BF16 && L.total_bwd > L.total && workspace_bytes >= L.total_bwd;
+    if ((keep_ds || ds_ready) && !ds_path)
+        return fail(MTGR_ERROR_WORKSPACE_TOO_SMALL,
+                    "MTGR_BWD_KEEP_DS / _DS_READY need a bf16 problem and %zu workspace bytes", L.total_bwd);
     if (!(p->flags & MTGR_ATTN_PLANNED)) {
         st = schedule(p, L, offsets, seg, ts, workspace, s);
         if (st != MTGR_SUCCESS) return st;
     }
-    float* drab_out = want_dq ? drab : nullptr;
+    mtgr::BwdPlan plan{};
+    plan.dkdv = want_dkdv;
+    plan.store_ds = want_dkdv && ds_path && (want_dq || keep_ds);
+    plan.dq_from_ds = want_dq && (ds_ready || (want_dkdv && ds_path));
+    plan.dq_recompute = want_dq && !plan.dq_from_ds;
+    // drab comes from the dk/dv kernel when it runs (bf16), else from the recomputing dq kernel
+    float* drab_out = p->dtype == MTGR_DTYPE_BF16 ? ((want_dkdv || plan.dq_recompute) ? drab : nullptr)
+                                                  : (want_dq ? drab : nullptr);
     if (drab_out) {
         hipError_t e = mtgr::launch_fill_f32(drab_out, (long long)p->num_heads * p->num_rab_buckets, 0.f, s);
         if (e != hipSuccess) return device_fail(e, "drab fill");
@@ -285,7 +317,7 @@ mtgr_status_t mtgr_hstu_attn_bwd(const mtgr_hstu_problem_t* p, const int32_t* of
     a.dv = dv;
     a.drab = drab_out;
     hipError_t e = p->dtype == MTGR_DTYPE_BF16
-                       ? mtgr::launch_attn_bwd_bf16(a, p->head_dim, (int)L.slots, want_dq, want_dkdv, s)
+                       ? mtgr::launch_attn_bwd_bf16(a, p->head_dim, (int)L.slots, plan, s)
                        : mtgr::launch_attn_bwd_f32(a, p->head_dim, (int)L.slots, want_dq, want_dkdv, s);
     if (e != hipSuccess) return device_fail(e, "attention backward");
     return ok();

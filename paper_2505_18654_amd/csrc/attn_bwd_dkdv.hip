@@ -1,0 +1,252 @@
+// dK, dV (and drab, and optionally the stored dS blocks) of the attention backward (bf16).
+#include "attn_bwd_common.h"
+
+namespace mtgr {
+using bwd::BM;
+using bwd::BN;
+using bwd::ldg16;
+using bwd::zero;
+
+// ------------------------------------------------------------------ dK, dV, bf16
+// A workgroup owns 128 keys (32 per wave) of one (user, head).  K of those keys stays in LDS
+// for the whole kernel and V in VGPRs; the visible queries stream through LDS 32 at a time
+// (Q and dO rows plus their timestamps and mask codes, double-buffered, copied with
+// global_load_lds one unit ahead).  Per unit a wave forms S and dP (32 queries x its 32 keys),
+// then P and dS in registers, and accumulates dV += P^T dO and dK += dS^T Q.  Reading K from
+// LDS instead of registers keeps the wave within 256 VGPRs without spilling: a scratch reload
+// issued after a prefetch would have to wait for that prefetch (vector-memory operations
+// complete in issue order), serialising copy and compute.
+// With STORE it also writes dS (bf16, the A operand of its dK product) as 64 x 64 blocks
+// for the dQ-from-dS kernel; it forms drab when a.drab is set.
+template <int DH, bool RAB, bool STORE>
+__global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) {
+    constexpr int CPR = DH / 8, KSTEPS = DH / 16, DBLK = DH / 32, UNIT = 32 * DH;
+    __shared__ __align__(16) uint16_t sK[BM * DH];
+    __shared__ __align__(16) uint16_t sQ0[UNIT];
+    __shared__ __align__(16) uint16_t sQ1[UNIT];
+    __shared__ __align__(16) uint16_t sG0[UNIT];
+    __shared__ __align__(16) uint16_t sG1[UNIT];
+    __shared__ int sQts[2][32];
+    __shared__ int sQcode[2][32];
+    __shared__ float sRab[MTGR_RAB_LDS];
+    __shared__ float sHist[MTGR_RAB_LDS];
+
+    const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int2 item = a.items[blockIdx.x];
+    if (item.x < 0) return;
+    const int b = item.x, kt = item.y >> 8, h = item.y & 255;
+    const bool want_drab = RAB && a.drab != nullptr;
+    const int ob = a.offsets[b], nb = a.offsets[b + 1] - ob;
+    const int k0 = kt * BM;
+    const int ntq = (nb + BN - 1) / BN;
+    const float inv_n = 1.0f / (float)nb;
+    const float alpha = a.alpha;
+    const int4* summ = a.summ + (long long)b * a.ntile;
+    TileSummary sk = load_summary(summ, 2 * kt);
+    if (2 * kt + 1 < ntq) sk = combine(sk, load_summary(summ, 2 * kt + 1));
+    else sk.flags &= ~TS_ALL_STATIC;   // a lone half tile is never fully visible
+
+    const int col = lane & 31, hh = lane >> 5;
+    const int kj = k0 + w * 32 + col;
+    const bool kvalid = kj < nb;
+    int kcode = 0, kts = 0;
+    if (kvalid) {
+        kcode = token_code(a.seg[ob + kj]);
+        kts = a.ts[ob + kj];
+    }
+    const uint16_t* V = (const uint16_t*)a.v;
+    const uint16_t* Kb = (const uint16_t*)a.k + (long long)ob * a.ld_k;
+    const uint16_t* Qb = (const uint16_t*)a.q + (long long)ob * a.ld_q;
+    const uint16_t* Gb = (const uint16_t*)a.dout + (long long)ob * a.ld_o;
+    bf16x8 vreg[KSTEPS];
+#pragma unroll
+    for (int kk = 0; kk < KSTEPS; kk++) {
+        uint4 g = make_uint4(0, 0, 0, 0);
+        if (kvalid) g = ldg16(V + (long long)(ob + kj) * a.ld_v + h * DH + 16 * kk + 8 * hh);
+        vreg[kk] = as_bf16x8(g);
+    }
+    if (RAB && tid < MTGR_RAB_LDS) {
+        sRab[tid] = tid < a.nbuckets ? a.rab[h * a.nbuckets + tid] : 0.f;
+        sHist[tid] = 0.f;
+    }
+    // stored dS: block (query tile q, key tile k) of this (user, head) is ds_blk + q ntq + k;
+    // this wave's 32 keys are keys 32 (w & 1) .. 32 (w & 1) + 31 of key tile kblk.
+    const int kblk = (k0 + 32 * w) >> 6;
+    const bool store_rows = STORE && kblk < ntq;
+    const long long ds_blk = STORE ? a.ds_off[b] + (long long)h * ntq * ntq + kblk : 0;
+    floatx16 dkacc[DBLK], dvacc[DBLK];
+#pragma unroll
+    for (int i = 0; i < DBLK; i++) {
+        zero(dkacc[i]);
+        zero(dvacc[i]);
+    }
+
+    // A query tile that runs past the user's end holds copies of its last row; it must take
+    // the masked path so that those rows contribute nothing.
+    auto class_of = [&](int t) {
+        const bool overlap = (t * BN < k0 + BM) && (k0 < t * BN + BN);
+        const int c = tile_class(load_summary(summ, t), sk, overlap);
+        return (c == TILE_FULL && t * BN + BN > nb) ? TILE_PARTIAL : c;
+    };
+    TileWalker<decltype(class_of)> walk(class_of, ntq);
+    // Unit (t, half): queries 64 t + 32 half .. + 31 (the second half of a tile is skipped
+    // when it starts past the user's end, so every copied unit holds a valid row).
+    auto issue = [&](int t, int half, int buf) {
+        const int r0 = t * BN + 32 * half;
+        tile_dma<DH, 32>(buf ? sQ1 : sQ0, Qb, a.ld_q, r0, nb, h * DH, tid);
+        tile_dma<DH, 32>(buf ? sG1 : sG0, Gb, a.ld_o, r0, nb, h * DH, tid);
+        codes_dma<32>(sQts[buf], sQcode[buf], a.ts + ob, a.tok_code + ob, r0, nb, tid);
+    };
+
+    int cls, cls_n;
+    int t = walk.next(0, &cls), half = 0, buf = 0;
+    if (t < ntq) {
+        tile_dma<DH, BM>(sK, Kb, a.ld_k, k0, nb, h * DH, tid);
+        issue(t, 0, 0);
+    }
+    wait_vmcnt_seen<0>();   // K, V, the first unit
+    bool first = true;
+    while (t < ntq) {
+        // The copy of this unit was issued before the previous unit's 4 dS stores.
+        if (!first) {
+            if (STORE && store_rows) wait_vmcnt_seen<4>();
+            else wait_vmcnt_seen<0>();
+        }
+        first = false;
+        const int qb = t * BN + 32 * half;
+        if (tid < 32 && qb + tid >= nb) sQcode[buf][tid] = 0;
+        lds_barrier();
+        int tn = t, hn = 1;
+        cls_n = cls;
+        if (half == 1 || t * BN + 32 >= nb) {
+            tn = walk.next(t + 1, &cls_n);
+            hn = 0;
+        }
+        if (tn < ntq) issue(tn, hn, buf ^ 1);
+        const uint16_t* sQ = buf ? sQ1 : sQ0;
+        const uint16_t* sG = buf ? sG1 : sG0;
+        const int* qts = sQts[buf];
+        const int* qcode = sQcode[buf];
+
+        // S (32 q x 32 keys) = Q K^T and dP = dO V^T: lane = key column, registers = queries.
+        floatx16 sacc, dpacc;
+        zero(sacc);
+        zero(dpacc);
+#pragma unroll
+        for (int kk = 0; kk < KSTEPS; kk++) {
+            const bf16x8 qa = tile_read8<CPR>(sQ, col, 2 * kk + hh);
+            const bf16x8 ga = tile_read8<CPR>(sG, col, 2 * kk + hh);
+            const bf16x8 kb = tile_read8<CPR>(sK, 32 * w + col, 2 * kk + hh);
+            sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa, kb, sacc, 0, 0, 0);
+            dpacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ga, vreg[kk], dpacc, 0, 0, 0);
+        }
+        uint32_t pk[2][4], dsk[2][4];
+#pragma unroll
+        for (int r = 0; r < 16; r += 2) {
+            float pv[2], dv[2];
+#pragma unroll
+            for (int e = 0; e < 2; e++) {
+                const int rr = r + e;
+                const int ql = 8 * (rr >> 2) + 4 * hh + (rr & 3);
+                float x = sacc[rr] * alpha;
+                int bk = 0;
+                if (RAB) {
+                    bk = rab_bucket(qts[ql], kts, a.nbuckets);
+                    x += sRab[bk];
+                }
+                float sg;
+                float p = silu_sig(x, sg) * inv_n;
+                float ds = dpacc[rr] * sg * (1.0f + x * (1.0f - sg)) * inv_n;
+                if (cls == TILE_PARTIAL) {
+                    const bool vis = visible(qcode[ql], qts[ql], qb + ql, kcode, kts, kj);
+                    p = vis ? p : 0.f;
+                    ds = vis ? ds : 0.f;
+                }
+                if (want_drab && ds != 0.f) atomicAdd(&sHist[bk], ds);
+                pv[e] = p;
+                dv[e] = ds;
+            }
+            pk[r >> 3][(r & 7) >> 1] = pack_bf16x2(pv[0], pv[1]);
+            dsk[r >> 3][(r & 7) >> 1] = pack_bf16x2(dv[0], dv[1]);
+        }
+        if (store_rows) {
+            // Sub-block (query half, key half) of block (t, kblk), 2 KB in register-fragment
+            // order: chunk (kq, g, lane) = 4 bf16 of dS for key 32 (w & 1) + lane % 32 and
+            // queries 32 half + 16 kq + 8 g + 4 (lane / 32) + 0..3, i.e. dsk[kq][2g], dsk[kq][2g+1].
+            // Each of the 4 store instructions writes 512 contiguous bytes.
+            uint2* sub = (uint2*)(a.ds + ((ds_blk + (long long)t * ntq) << 12)) + (2 * half + (w & 1)) * 256;
+#pragma unroll
+            for (int kq = 0; kq < 2; kq++)
+#pragma unroll
+                for (int g = 0; g < 2; g++)
+                    sub[(2 * kq + g) * 64 + lane] = make_uint2(dsk[kq][2 * g], dsk[kq][2 * g + 1]);
+        }
+        // dV (32 keys x dh) += P^T dO ; dK += dS^T Q.  A = P^T / dS^T from registers,
+        // B = dO / Q read transposed (lane = feature column, slots = queries).
+#pragma unroll
+        for (int kq = 0; kq < 2; kq++) {
+            const bf16x8 pa = as_bf16x8(make_uint4(pk[kq][0], pk[kq][1], pk[kq][2], pk[kq][3]));
+            const bf16x8 da = as_bf16x8(make_uint4(dsk[kq][0], dsk[kq][1], dsk[kq][2], dsk[kq][3]));
+#pragma unroll
+            for (int d = 0; d < DBLK; d++) {
+                const bf16x8 gb = tile_read_tr<CPR>(sG, 16 * kq, 32 * d, lane);
+                const bf16x8 qbv = tile_read_tr<CPR>(sQ, 16 * kq, 32 * d, lane);
+                dvacc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pa, gb, dvacc[d], 0, 0, 0);
+                dkacc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(da, qbv, dkacc[d], 0, 0, 0);
+            }
+        }
+        t = tn;
+        half = hn;
+        cls = cls_n;
+        buf ^= 1;
+    }
+
+    if (want_drab) {
+        __syncthreads();   // every wave's histogram updates have landed
+        if (tid < a.nbuckets && sHist[tid] != 0.f) atomicAdd(&a.drab[h * a.nbuckets + tid], sHist[tid]);
+    }
+    // dK / dV accumulators: lane = feature column, registers = key rows.  Each wave stages
+    // its 32 rows in a swizzled 32-row tile inside the K tile.
+    uint16_t* sO = sK + w * 32 * DH;
+    uint16_t* DK = (uint16_t*)a.dk;
+    uint16_t* DV = (uint16_t*)a.dv;
+#pragma unroll
+    for (int which = 0; which < 2; which++) {
+        __syncthreads();
+#pragma unroll
+        for (int d = 0; d < DBLK; d++) {
+#pragma unroll
+            for (int r = 0; r < 16; r++) {
+                const int krow = 8 * (r >> 2) + 4 * hh + (r & 3);
+                const int dd = 32 * d + col;
+                const float val = which == 0 ? alpha * dkacc[d][r] : dvacc[d][r];
+                sO[8 * tile_chunk<CPR>(krow, dd >> 3) + (dd & 7)] = (uint16_t)f32_to_bf16_bits(val);
+            }
+        }
+        __syncthreads();
+        uint16_t* dst = which == 0 ? DK : DV;
+        const long long ld = which == 0 ? a.ld_k : a.ld_v;
+#pragma unroll
+        for (int i = 0; i < 32 * CPR / 64; i++) {
+            const int c = lane + 64 * i, row = c / CPR, cc = c % CPR;
+            const int kr = k0 + w * 32 + row;
+            if (kr < nb)
+                *(uint4*)(dst + (long long)(ob + kr) * ld + h * DH + cc * 8) =
+                    *(const uint4*)&sO[8 * tile_chunk<CPR>(row, cc)];
+        }
+    }
+}
+
+template __global__ void attn_bwd_dkdv_bf16_kernel<32, false, false>(AttnArgs);
+template __global__ void attn_bwd_dkdv_bf16_kernel<32, false, true>(AttnArgs);
+template __global__ void attn_bwd_dkdv_bf16_kernel<32, true, false>(AttnArgs);
+template __global__ void attn_bwd_dkdv_bf16_kernel<32, true, true>(AttnArgs);
+template __global__ void attn_bwd_dkdv_bf16_kernel<64, false, false>(AttnArgs);
+template __global__ void attn_bwd_dkdv_bf16_kernel<64, false, true>(AttnArgs);
+template __global__ void attn_bwd_dkdv_bf16_kernel<64, true, false>(AttnArgs);
+template __global__ void attn_bwd_dkdv_bf16_kernel<64, true, true>(AttnArgs);
+template __global__ void attn_bwd_dkdv_bf16_kernel<128, false, false>(AttnArgs);
+template __global__ void attn_bwd_dkdv_bf16_kernel<128, false, true>(AttnArgs);
+template __global__ void attn_bwd_dkdv_bf16_kernel<128, true, false>(AttnArgs);
+template __global__ void attn_bwd_dkdv_bf16_kernel<128, true, true>(AttnArgs);
+}  // namespace mtgr

@@ -1,0 +1,178 @@
+// dQ (and drab) of the attention backward, recomputing S, dP and dS (bf16).
+#include "attn_bwd_common.h"
+
+namespace mtgr {
+using bwd::BM;
+using bwd::BN;
+using bwd::ldg16;
+using bwd::zero;
+
+// ------------------------------------------------------------------ dQ (+ drab), bf16
+template <int DH, bool RAB>
+__global__ __launch_bounds__(256, 2) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
+    constexpr int CPR = DH / 8, KSTEPS = DH / 16, DBLK = DH / 32, TILE = BN * DH;
+    __shared__ __align__(16) uint16_t sK0[TILE];
+    __shared__ __align__(16) uint16_t sK1[TILE];
+    __shared__ __align__(16) uint16_t sV0[TILE];
+    __shared__ __align__(16) uint16_t sV1[TILE];
+    __shared__ int sKts[2][BN];
+    __shared__ int sKcode[2][BN];
+    __shared__ float sRab[MTGR_RAB_LDS];
+    __shared__ float sHist[MTGR_RAB_LDS];
+
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int2 item = a.items[blockIdx.x];
+    if (item.x < 0) return;
+    const int b = item.x, qt = item.y >> 8, h = item.y & 255;
+    const bool want_drab = RAB && a.drab != nullptr;
+    const int ob = a.offsets[b], nb = a.offsets[b + 1] - ob;
+    const int q0 = qt * BM;
+    const int ntk = (nb + BN - 1) / BN;
+    const float inv_n = 1.0f / (float)nb;
+    const float alpha = a.alpha;
+    const int4* summ = a.summ + (long long)b * a.ntile;
+    TileSummary sq = load_summary(summ, 2 * qt);
+    if (2 * qt + 1 < ntk) sq = combine(sq, load_summary(summ, 2 * qt + 1));
+
+    const int col = lane & 31, hh = lane >> 5;
+    const int qi = q0 + w * 32 + col;
+    const bool qvalid = qi < nb;
+    int qcode = 0, qts = 0;
+    if (qvalid) {
+        qcode = token_code(a.seg[ob + qi]);
+        qts = a.ts[ob + qi];
+    }
+    const uint16_t* Q = (const uint16_t*)a.q;
+    const uint16_t* DO = (const uint16_t*)a.dout;
+    const uint16_t* Kb = (const uint16_t*)a.k + (long long)ob * a.ld_k;
+    const uint16_t* Vb = (const uint16_t*)a.v + (long long)ob * a.ld_v;
+    bf16x8 qreg[KSTEPS], doreg[KSTEPS];
+#pragma unroll
+    for (int kk = 0; kk < KSTEPS; kk++) {
+        uint4 u = make_uint4(0, 0, 0, 0), g = make_uint4(0, 0, 0, 0);
+        if (qvalid) {
+            u = ldg16(Q + (long long)(ob + qi) * a.ld_q + h * DH + 16 * kk + 8 * hh);
+            g = ldg16(DO + (long long)(ob + qi) * a.ld_o + h * DH + 16 * kk + 8 * hh);
+        }
+        qreg[kk] = as_bf16x8(u);
+        doreg[kk] = as_bf16x8(g);
+    }
+    if (RAB && tid < MTGR_RAB_LDS) {
+        sRab[tid] = tid < a.nbuckets ? a.rab[h * a.nbuckets + tid] : 0.f;
+        sHist[tid] = 0.f;
+    }
+    floatx16 dqacc[DBLK];
+#pragma unroll
+    for (int i = 0; i < DBLK; i++) zero(dqacc[i]);
+
+    auto class_of = [&](int t) {
+        const bool overlap = (t * BN < q0 + BM) && (q0 < t * BN + BN);
+        return tile_class(sq, load_summary(summ, t), overlap);
+    };
+    TileWalker<decltype(class_of)> walk(class_of, ntk);
+    auto issue = [&](int t, int buf) {
+        tile_dma<DH>(buf ? sK1 : sK0, Kb, a.ld_k, t * BN, nb, h * DH, tid);
+        tile_dma<DH>(buf ? sV1 : sV0, Vb, a.ld_v, t * BN, nb, h * DH, tid);
+        codes_dma(sKts[buf], sKcode[buf], a.ts + ob, a.tok_code + ob, t * BN, nb, tid);
+    };
+
+    int cls, cls_n;
+    int t = walk.next(0, &cls);
+    int cur = 0;
+    if (t < ntk) issue(t, 0);
+    while (t < ntk) {
+        wait_vmem();
+        if (tid < BN && t * BN + tid >= nb) sKcode[cur][tid] = 0;
+        lds_barrier();
+        const int tn = walk.next(t + 1, &cls_n);
+        if (tn < ntk) issue(tn, cur ^ 1);
+        const uint16_t* sK = cur ? sK1 : sK0;
+        const uint16_t* sV = cur ? sV1 : sV0;
+        const int* kts = sKts[cur];
+        const int* kcode = sKcode[cur];
+
+#pragma unroll
+        for (int blk = 0; blk < 2; blk++) {
+            floatx16 sacc, dpacc;
+            zero(sacc);
+            zero(dpacc);
+#pragma unroll
+            for (int kk = 0; kk < KSTEPS; kk++) {
+                const bf16x8 ka = tile_read8<CPR>(sK, 32 * blk + col, 2 * kk + hh);
+                const bf16x8 va = tile_read8<CPR>(sV, 32 * blk + col, 2 * kk + hh);
+                sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qreg[kk], sacc, 0, 0, 0);
+                dpacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, doreg[kk], dpacc, 0, 0, 0);
+            }
+            uint32_t dsk[2][4];
+#pragma unroll
+            for (int r = 0; r < 16; r += 2) {
+                float dv[2];
+#pragma unroll
+                for (int e = 0; e < 2; e++) {
+                    const int rr = r + e;
+                    const int kl = 32 * blk + 8 * (rr >> 2) + 4 * hh + (rr & 3);
+                    float x = sacc[rr] * alpha;
+                    int bk = 0;
+                    if (RAB) {
+                        bk = rab_bucket(qts, kts[kl], a.nbuckets);
+                        x += sRab[bk];
+                    }
+                    float sg;
+                    silu_sig(x, sg);
+                    float ds = dpacc[rr] * sg * (1.0f + x * (1.0f - sg)) * inv_n;
+                    if (cls == TILE_PARTIAL)
+                        ds = visible(qcode, qts, qi, kcode[kl], kts[kl], t * BN + kl) ? ds : 0.f;
+                    else if (!qvalid)
+                        ds = 0.f;
+                    if (want_drab && ds != 0.f) atomicAdd(&sHist[bk], ds);
+                    dv[e] = ds;
+                }
+                dsk[r >> 3][(r & 7) >> 1] = pack_bf16x2(dv[0], dv[1]);
+            }
+#pragma unroll
+            for (int kq = 0; kq < 2; kq++) {
+                const bf16x8 db = as_bf16x8(make_uint4(dsk[kq][0], dsk[kq][1], dsk[kq][2], dsk[kq][3]));
+#pragma unroll
+                for (int d = 0; d < DBLK; d++) {
+                    const bf16x8 kt = tile_read_tr<CPR>(sK, 32 * blk + 16 * kq, 32 * d, lane);
+                    dqacc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kt, db, dqacc[d], 0, 0, 0);
+                }
+            }
+        }
+        lds_barrier();
+        t = tn;
+        cls = cls_n;
+        cur ^= 1;
+    }
+
+    if (want_drab && tid < a.nbuckets && sHist[tid] != 0.f) atomicAdd(&a.drab[h * a.nbuckets + tid], sHist[tid]);
+    uint16_t* sO = (w < 2 ? sK0 : sK1) + (w & 1) * 32 * DH;
+#pragma unroll
+    for (int d = 0; d < DBLK; d++) {
+#pragma unroll
+        for (int g = 0; g < 4; g++) {
+            const int dd = 32 * d + 8 * g + 4 * hh;
+            *(uint2*)&sO[8 * tile_chunk<CPR>(col, dd >> 3) + (dd & 7)] =
+                make_uint2(pack_bf16x2(alpha * dqacc[d][4 * g + 0], alpha * dqacc[d][4 * g + 1]),
+                           pack_bf16x2(alpha * dqacc[d][4 * g + 2], alpha * dqacc[d][4 * g + 3]));
+        }
+    }
+    __syncthreads();
+    uint16_t* DQ = (uint16_t*)a.dq;
+#pragma unroll
+    for (int i = 0; i < 32 * CPR / 64; i++) {
+        const int c = lane + 64 * i, row = c / CPR, cc = c % CPR;
+        const int qr = q0 + w * 32 + row;
+        if (qr < nb)
+            *(uint4*)(DQ + (long long)(ob + qr) * a.ld_q + h * DH + cc * 8) =
+                *(const uint4*)&sO[8 * tile_chunk<CPR>(row, cc)];
+    }
+}
+
+template __global__ void attn_bwd_dq_bf16_kernel<32, false>(AttnArgs);
+template __global__ void attn_bwd_dq_bf16_kernel<32, true>(AttnArgs);
+template __global__ void attn_bwd_dq_bf16_kernel<64, false>(AttnArgs);
+template __global__ void attn_bwd_dq_bf16_kernel<64, true>(AttnArgs);
+template __global__ void attn_bwd_dq_bf16_kernel<128, false>(AttnArgs);
+template __global__ void attn_bwd_dq_bf16_kernel<128, true>(AttnArgs);
+}  // namespace mtgr

@@ -299,6 +299,17 @@ __device__ __forceinline__ void wait_vmcnt() {
 
 __device__ __forceinline__ void wait_vmem() { wait_vmcnt<0>(); }
 
+// The same wait as a real s_waitcnt instruction (gfx9 encoding: vmcnt in bits 3:0 and 15:14,
+// expcnt and lgkmcnt left at their maxima).  The compiler's own counter bookkeeping sees it, so
+// loads it issued earlier (e.g. before a loop) are known complete afterwards and get no extra
+// wait inside the loop, where such a wait would also cover the copies in flight.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt_seen() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0F70);
+    asm volatile("" ::: "memory");
+}
+
 // Workgroup barrier for LDS hand-offs: this wave's LDS reads and writes have completed, and
 // no other wave passes until all waves arrive.  Copies into LDS must be waited for first.
 __device__ __forceinline__ void lds_barrier() {
@@ -337,45 +348,49 @@ __device__ __forceinline__ bf16x8 lds_read_tr(const uint16_t* tile, uint32_t o0,
     return __builtin_bit_cast(bf16x8, v);
 }
 
-// Asynchronous copy of rows [row0, row0 + 64) of a [.., ld] bf16 matrix (columns col0 ..
+// Asynchronous copy of rows [row0, row0 + ROWS) of a [.., ld] bf16 matrix (columns col0 ..
 // col0 + DH) into a swizzled tile.  Rows at or past `nrows` are replaced by row nrows - 1, a
-// valid row whose values the mask or a zero multiplier neutralises.  Every wave of the
-// 256-thread workgroup issues DH / 32 instructions; instruction i of wave w fills the 64
-// chunks (16 bytes each) of LDS block 4 i + w, i.e. tile rows RPI i + (64 / CPR) w + lane / CPR
-// with RPI = 256 / CPR.  A lane's row within the block and its chunk (the swizzle depends on
-// row mod 16 only) are the same for every instruction, so each instruction needs one
-// wave-uniform base address and one per-lane 32-bit offset.  The caller guarantees
-// 64 * ld * 2 < 2^31.
-template <int DH>
+// valid row whose values the mask or a zero multiplier neutralises; the caller guarantees
+// row0 < nrows.  Instruction i of wave w of the 256-thread workgroup fills the 64 chunks
+// (16 bytes each) of LDS block 4 i + w, i.e. tile rows RPI i + (64 / CPR) w + lane / CPR with
+// RPI = 256 / CPR; when the tile has fewer than 256 chunks only the first waves issue.  A
+// lane's row within the block and its chunk (the swizzle depends on row mod 16 only) are the
+// same for every instruction, so each instruction needs one wave-uniform base address and one
+// per-lane 32-bit offset.  The caller guarantees ROWS * ld * 2 < 2^31.
+template <int DH, int ROWS = 64>
 __device__ __forceinline__ void tile_dma(uint16_t* tile, const uint16_t* base, long long ld, int row0,
                                          int nrows, int col0, int tid) {
-    constexpr int CPR = DH / 8, RPI = 256 / CPR;
+    constexpr int CPR = DH / 8, RPI = 256 / CPR, NCH = ROWS * CPR;
+    static_assert(NCH % 64 == 0, "whole LDS blocks");
     const int lane = tid & 63, w = tid >> 6;
     const int rl = w * (64 / CPR) + lane / CPR;             // row within block 0 of this wave
     const int cl = (lane % CPR) ^ swz<CPR>(rl);             // source chunk
     const uint16_t* tbase = base + (long long)row0 * ld + col0;
     const uint32_t ltile = __builtin_amdgcn_readfirstlane(lds_address(tile) + (uint32_t)w * 1024u);
-    if (row0 + 64 <= nrows) {
+    if (NCH < 256 && w * 64 >= NCH) return;
+    if (row0 + ROWS <= nrows) {
         const uint32_t voff = (uint32_t)(rl * ld + cl * 8) * 2u;
 #pragma unroll
-        for (int i = 0; i < DH / 32; i++)
+        for (int i = 0; i < (NCH + 255) / 256; i++)
             lds_dma16(ltile + (uint32_t)i * 4096u, uniform_ptr(tbase + (long long)i * RPI * ld), voff);
     } else {
         const int last = nrows - 1 - row0;                  // >= 0: the tile holds a valid row
 #pragma unroll
-        for (int i = 0; i < DH / 32; i++) {
+        for (int i = 0; i < (NCH + 255) / 256; i++) {
             const uint32_t voff = (uint32_t)(min(i * RPI + rl, last) * ld + cl * 8) * 2u;
             lds_dma16(ltile + (uint32_t)i * 4096u, uniform_ptr(tbase), voff);
         }
     }
 }
 
-// Timestamps and mask codes of 64 consecutive tokens into LDS (two 4-byte-per-lane copies
-// issued by wave 0).  Tokens at or past `ntok` are copied from token ntok - 1; the caller
-// zeroes their codes once the copy has landed.
+// Timestamps and mask codes of N (at most 64) consecutive tokens into LDS (two 4-byte-per-lane
+// copies issued by wave 0).  Tokens at or past `ntok` are copied from token ntok - 1
+// (tok0 < ntok); the caller zeroes their codes once the copy has landed.
+template <int N = 64>
 __device__ __forceinline__ void codes_dma(int* dst_ts, int* dst_code, const int* ts, const int* code,
                                           int tok0, int ntok, int tid) {
-    if (tid < 64) {
+    static_assert(N <= 64, "one wave");
+    if (tid < N) {
         const uint32_t voff = (uint32_t)min(tid, ntok - 1 - tok0) * 4u;
         lds_dma4(lds_address(dst_ts), uniform_ptr(ts + tok0), voff);
         lds_dma4(lds_address(dst_code), uniform_ptr(code + tok0), voff);

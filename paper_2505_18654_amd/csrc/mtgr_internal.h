@@ -26,6 +26,8 @@ struct AttnArgs {
     const int4* summ;     // [B][ntile] per-64-token tile summaries
     const int* tok_code;  // [T] per-token mask code (token_code of seg)
     const int2* items;    // work list: {user, (tile << 8) | head}, user < 0 = empty slot
+    const long long* ds_off;  // [B+1] first stored-dS block of each user (H ceil(n_b/64)^2 blocks each)
+    uint16_t* ds;             // stored dS: 64 x 64 bf16 blocks, key-major
     int ntile;
     int heads;
     float alpha;
@@ -44,8 +46,19 @@ hipError_t launch_fill_f32(float* p, long long n, float value, hipStream_t s);
 
 hipError_t launch_attn_fwd_bf16(const AttnArgs& a, int head_dim, int slots, hipStream_t s);
 hipError_t launch_attn_fwd_f32(const AttnArgs& a, int head_dim, int slots, hipStream_t s);
-hipError_t launch_attn_bwd_bf16(const AttnArgs& a, int head_dim, int slots, bool dq, bool dkdv,
+// Which backward kernels run (bf16).
+struct BwdPlan {
+    bool dkdv;          // dk/dv kernel (forms drab when a.drab is set)
+    bool store_ds;      // ... also writes dS blocks to a.ds
+    bool dq_from_ds;    // dq = alpha dS k from the stored blocks
+    bool dq_recompute;  // dq kernel recomputing S, dP, dS (forms drab when a.drab is set)
+};
+constexpr size_t DS_BLOCK_BYTES = 64 * 64 * 2;   // one stored-dS block (64 keys x 64 queries bf16)
+
+hipError_t launch_attn_bwd_bf16(const AttnArgs& a, int head_dim, int slots, const BwdPlan& plan,
                                 hipStream_t s);
+hipError_t launch_ds_offsets(const int* offsets, int num_users, int heads, long long* ds_off,
+                             hipStream_t s);
 hipError_t launch_attn_bwd_f32(const AttnArgs& a, int head_dim, int slots, bool dq, bool dkdv,
                                hipStream_t s);
 

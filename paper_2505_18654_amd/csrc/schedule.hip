@@ -146,6 +146,50 @@ __global__ __launch_bounds__(1024) void build_schedule_kernel(const int* __restr
     }
 }
 
+// First stored-dS block of every user: exclusive prefix sum of H * ceil(n_b / 64)^2.
+__global__ __launch_bounds__(1024) void ds_offsets_kernel(const int* __restrict__ offsets, int num_users,
+                                                          int heads, long long* __restrict__ ds_off) {
+    __shared__ long long scratch[17];
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    long long carry = 0;
+    for (int base = 0; base < num_users; base += 1024) {
+        const int b = base + tid;
+        long long v = 0;
+        if (b < num_users) {
+            const long long nt = (offsets[b + 1] - offsets[b] + 63) / 64;
+            v = (long long)heads * nt * nt;
+        }
+        long long incl = v;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const long long o = __shfl_up(incl, off, 64);
+            if (lane >= off) incl += o;
+        }
+        if (lane == 63) scratch[w] = incl;
+        __syncthreads();
+        if (tid == 0) {
+            long long run = 0;
+            for (int i = 0; i < 16; i++) {
+                const long long x = scratch[i];
+                scratch[i] = run;
+                run += x;
+            }
+            scratch[16] = run;
+        }
+        __syncthreads();
+        if (b < num_users) ds_off[b] = carry + scratch[w] + incl - v;
+        carry += scratch[16];
+        __syncthreads();
+    }
+    if (tid == 0) ds_off[num_users] = carry;
+}
+
+hipError_t launch_ds_offsets(const int* offsets, int num_users, int heads, long long* ds_off,
+                             hipStream_t s) {
+    ds_offsets_kernel<<<1, 1024, 0, s>>>(offsets, num_users, heads, ds_off);
+    return hipGetLastError();
+}
+
 __global__ void fill_f32_kernel(float* __restrict__ p, long long n, float value) {
     for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < n;
          i += (long long)gridDim.x * blockDim.x)

@@ -28,6 +28,8 @@ MTGR_MAX_LD = 1 << 24
 MTGR_ATTN_PLANNED = 1
 MTGR_BWD_SKIP_DQ = 2
 MTGR_BWD_SKIP_DKDV = 4
+MTGR_BWD_KEEP_DS = 8
+MTGR_BWD_DS_READY = 16
 
 EXPORTED = (
     "mtgr_hstu_attn_workspace_size", "mtgr_hstu_attn_plan", "mtgr_hstu_attn_fwd", "mtgr_hstu_attn_bwd",

@@ -76,12 +76,13 @@ def attn_problem(jag: Jagged, q, k, v, out, rab=None, alpha: float = 1.0,
                              _token_stride(out, row), flags)
 
 
-def attn_plan(q, jag: Jagged, workspace=None, rab=None):
+def attn_plan(q, jag: Jagged, workspace=None, rab=None, backward: bool = False):
     """Builds the batch plan (tile summaries + work list) once; pass the returned workspace
-    with planned=True to attn_fwd / attn_bwd for every layer on the same batch."""
+    with planned=True to attn_fwd / attn_bwd for every layer on the same batch.  backward=True
+    allocates the larger workspace with which the backward stores dS instead of recomputing."""
     p = attn_problem(jag, q, q, q, q, rab)
     if workspace is None:
-        workspace = workspace_for(p, q.device)
+        workspace = workspace_for(p, q.device, backward)
     hstu.mtgr_hstu_attn_plan(p, jag.offsets, jag.seg, jag.ts, workspace, workspace.numel())
     return workspace
 
@@ -106,14 +107,24 @@ def attn_fwd(q, k, v, jag: Jagged, rab=None, alpha: float = 1.0, out=None, works
 
 def attn_bwd(q, k, v, dout, jag: Jagged, rab=None, alpha: float = 1.0, need_drab: bool = True,
              grads=None, workspace=None, planned: bool = False, parts: str = "all"):
-    """Backward of Eq. 5: returns (dq, dk, dv, drab-or-None).  parts: "all", "dq" or "dkdv"."""
-    flags = (hstu.MTGR_ATTN_PLANNED if planned else 0) | \
-        {"all": 0, "dq": hstu.MTGR_BWD_SKIP_DKDV, "dkdv": hstu.MTGR_BWD_SKIP_DQ}[parts]
+    """Backward of Eq. 5: returns (dq, dk, dv, drab-or-None).
+
+    parts: "all"; "dq" or "dkdv" (one side only); or the two halves of the stored-dS path as
+    two calls on one backward-size workspace: "dkdv_keep_ds" (dk, dv, drab and the dS blocks)
+    then "dq_from_ds" (dq from them; drab is not formed again)."""
+    flags = (hstu.MTGR_ATTN_PLANNED if planned else 0) | {
+        "all": 0, "dq": hstu.MTGR_BWD_SKIP_DKDV, "dkdv": hstu.MTGR_BWD_SKIP_DQ,
+        "dkdv_keep_ds": hstu.MTGR_BWD_SKIP_DQ | hstu.MTGR_BWD_KEEP_DS,
+        "dq_from_ds": hstu.MTGR_BWD_SKIP_DKDV | hstu.MTGR_BWD_DS_READY}[parts]
+    if parts == "dq_from_ds":
+        need_drab = False
     if grads is None:
         dq, dk, dv = (_like_layout(x) for x in (q, k, v))
         drab = torch.empty_like(rab) if (rab is not None and need_drab) else None
     else:
         dq, dk, dv, drab = grads
+        if not need_drab:
+            drab = None
     p = attn_problem(jag, q, k, v, dout, rab, alpha, flags)
     if _token_stride(dq, q.shape[1] * q.shape[2]) != p.ld_q or \
             _token_stride(dk, q.shape[1] * q.shape[2]) != p.ld_k or \

@@ -76,7 +76,7 @@ def test_problem_validation(mutate, status):
 
 def test_unknown_flags_rejected():
     p = prob()
-    p.flags = 8
+    p.flags = 32
     with pytest.raises(hstu.MtgrError) as e:
         hstu.mtgr_hstu_attn_workspace_size(p)
     assert e.value.status == hstu.MTGR_ERROR_INVALID_ARGUMENT
@@ -155,6 +155,52 @@ def test_bwd_argument_checks():
                                 FAKE, FAKE, 1 << 30, 0)
     assert e.value.status == hstu.MTGR_ERROR_NULL_POINTER
     assert len(args) == 12
+
+
+def test_backward_workspace_sizes():
+    """backward = 1 adds the stored-dS blocks for bf16: H * ntile * (T/64 + B) blocks of 8 KB
+    on top of the plan; fp32 always recomputes, so its size does not grow."""
+    p = prob(num_users=4, total_tokens=100, max_seqlen=40, heads=2, head_dim=64)
+    base = hstu.mtgr_hstu_attn_workspace_size(p, False)
+    big = hstu.mtgr_hstu_attn_workspace_size(p, True)
+    ntile = (40 + 63) // 64
+    assert big - base == 2 * ntile * ((100 + 63) // 64 + 4) * 64 * 64 * 2
+    pf = prob(dtype=FP32, head_dim=64)
+    assert hstu.mtgr_hstu_attn_workspace_size(pf, True) == hstu.mtgr_hstu_attn_workspace_size(pf, False)
+
+
+def bwd_call(p, drab=None, workspace_bytes=1 << 30):
+    hstu.mtgr_hstu_attn_bwd(p, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE if p.num_rab_buckets else None,
+                            FAKE, FAKE, FAKE, FAKE, drab, FAKE, workspace_bytes, 0)
+
+
+@pytest.mark.parametrize("flags,drab,status", [
+    (hstu.MTGR_BWD_KEEP_DS, None, hstu.MTGR_ERROR_INVALID_ARGUMENT),            # needs SKIP_DQ
+    (hstu.MTGR_BWD_DS_READY, None, hstu.MTGR_ERROR_INVALID_ARGUMENT),           # needs SKIP_DKDV
+    (hstu.MTGR_BWD_DS_READY | hstu.MTGR_BWD_SKIP_DKDV, FAKE, hstu.MTGR_ERROR_INVALID_ARGUMENT),
+])
+def test_stored_ds_flag_checks(flags, drab, status):
+    p = prob(rab_buckets=64 if drab else 0)
+    p.flags = flags
+    with pytest.raises(hstu.MtgrError) as e:
+        bwd_call(p, drab=drab)
+    assert e.value.status == status
+
+
+@pytest.mark.parametrize("flags", [hstu.MTGR_BWD_KEEP_DS | hstu.MTGR_BWD_SKIP_DQ,
+                                   hstu.MTGR_BWD_DS_READY | hstu.MTGR_BWD_SKIP_DKDV])
+def test_stored_ds_flags_need_backward_workspace(flags):
+    p = prob()
+    base = hstu.mtgr_hstu_attn_workspace_size(p, False)
+    p.flags = flags
+    with pytest.raises(hstu.MtgrError) as e:
+        bwd_call(p, workspace_bytes=base)
+    assert e.value.status == hstu.MTGR_ERROR_WORKSPACE_TOO_SMALL
+    pf = prob(dtype=FP32)
+    pf.flags = flags
+    with pytest.raises(hstu.MtgrError) as e:                    # fp32 has no stored-dS path
+        bwd_call(pf)
+    assert e.value.status == hstu.MTGR_ERROR_WORKSPACE_TOO_SMALL
 
 
 @pytest.mark.parametrize("mutate,status", [

@@ -97,12 +97,12 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
     // Per-lane LDS byte offsets of the MFMA operands, shared by every tile and buffer: the
     // K operand of k-step kk (row col, chunk 2 kk + hh; rows 32..63 add 32 * CPR * 16 bytes)
     // and the two transposing-read supplier addresses of V^T column block db (row blocks of
-    // 16 keys add 16 * CPR * 16 bytes).
-    uint32_t kofs[KSTEPS], vofs0[DBLK], vofs1[DBLK];
-#pragma unroll
-    for (int kk = 0; kk < KSTEPS; kk++) kofs[kk] = tile_ofs<CPR>(col, 2 * kk + hh);
-#pragma unroll
-    for (int db = 0; db < DBLK; db++) tile_ofs_tr<CPR>(32 * db, lane, vofs0[db], vofs1[db]);
+    // 16 keys add 16 * CPR * 16 bytes).  The swizzle XORs the chunk index with a per-row
+    // constant, and a row's chunks fill an aligned block of CPR * 16 bytes, so the offset of
+    // k-step kk is that of k-step 0 XOR 32 kk, and that of column block db the one of block 0
+    // XOR 64 db: three live registers instead of KSTEPS + 2 DBLK.
+    uint32_t kofs0 = tile_ofs<CPR>(col, hh), vofs0 = 0, vofs1 = 0;
+    tile_ofs_tr<CPR>(0, lane, vofs0, vofs1);
     constexpr uint32_t ROW16 = 16u * CPR * 16u;   // bytes of 16 tile rows
 
     floatx16 oacc[DBLK];
@@ -165,6 +165,11 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
         constexpr int KB = decltype(kb_tag)::value, HN = decltype(hn_tag)::value;
         const uint16_t* Vc = sV[VB];
         const uint16_t* Kn = sK[KB];
+        // Derive the operand offsets afresh in every half-step (one XOR per read) instead of
+        // letting the compiler keep all of them live across the loop.
+        uint32_t kb0 = kofs0, vb0 = vofs0, vb1 = vofs1;
+        asm volatile("" : "+v"(kb0), "+v"(vb0), "+v"(vb1));
+        auto kofs = [&](int kk) { return kb0 ^ (32u * (uint32_t)kk); };
         const int* kts = sVts[VB];
         const int* kcode = sVcode[VB];
         uint32_t pk0[4];
@@ -176,13 +181,13 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
             return HAS_NEXT;
         };
         auto operand = [&](int m) {
-            if (m < DBLK) return lds_read_tr(Vc, vofs0[m] + ROW16, vofs1[m] + ROW16);
-            if (m < DBLK + KSTEPS / 2) return lds_read16(Kn, kofs[m - DBLK] + 2 * HN * ROW16);
+            if (m < DBLK) return lds_read_tr(Vc, (vb0 ^ (64u * m)) + ROW16, (vb1 ^ (64u * m)) + ROW16);
+            if (m < DBLK + KSTEPS / 2) return lds_read16(Kn, kofs(m - DBLK) + 2 * HN * ROW16);
             if (m < 2 * DBLK + KSTEPS / 2) {
-                const int db = m - DBLK - KSTEPS / 2;
-                return lds_read_tr(Vc, vofs0[db] + 2 * HC * ROW16, vofs1[db] + 2 * HC * ROW16);
+                const uint32_t db = m - DBLK - KSTEPS / 2;
+                return lds_read_tr(Vc, (vb0 ^ (64u * db)) + 2 * HC * ROW16, (vb1 ^ (64u * db)) + 2 * HC * ROW16);
             }
-            return lds_read16(Kn, kofs[m - 2 * DBLK] + 2 * HN * ROW16);
+            return lds_read16(Kn, kofs(m - 2 * DBLK) + 2 * HN * ROW16);
         };
         bf16x8 op[NM];
 #pragma unroll
@@ -246,12 +251,12 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
         issue_k(t0, 0);
         issue_v(t0, 0);
         if (t1 < ntk) issue_k(t1, 1);
-        wait_vmem();
+        wait_vmcnt_seen<0>();                                    // Q, K, V, codes
         lds_barrier();
         floatx16 sA, sB;                                         // S(t_i, keys 0..31) in sA
 #pragma unroll
         for (int kk = 0; kk < KSTEPS; kk++)
-            sA = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_read16(sK[0], kofs[kk]), qreg[kk],
+            sA = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_read16(sK[0], kofs0 ^ (32u * kk)), qreg[kk],
                                                         kk == 0 ? floatx16{} : sA, 0, 0, 0);
         // Tile t_i, whose K and V sit in buffers P (the tile loop is unrolled by two so that P
         // is a compile-time constant).  Returns false after the last tile.
@@ -299,7 +304,8 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
 #pragma unroll
             for (int db = 0; db < DBLK; db++)
                 oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                    lds_read_tr(sV[P], vofs0[db] + 3 * ROW16, vofs1[db] + 3 * ROW16), pb, oacc[db], 0, 0, 0);
+                    lds_read_tr(sV[P], (vofs0 ^ (64u * db)) + 3 * ROW16, (vofs1 ^ (64u * db)) + 3 * ROW16), pb,
+                    oacc[db], 0, 0, 0);
             const bool more = t1 < ntk;
             t0 = t1;
             cls0 = cls1;

@@ -362,7 +362,11 @@ __device__ __forceinline__ void tile_dma(uint16_t* tile, const uint16_t* base, l
                                          int nrows, int col0, int tid) {
     constexpr int CPR = DH / 8, RPI = 256 / CPR, NCH = ROWS * CPR;
     static_assert(NCH % 64 == 0, "whole LDS blocks");
-    const int lane = tid & 63, w = tid >> 6;
+    // The per-lane offsets are recomputed at every call (a few VALU instructions) rather than
+    // hoisted out of the caller's loop, where they would hold VGPRs for the whole loop.
+    int lane = tid & 63;
+    asm volatile("" : "+v"(lane));
+    const int w = tid >> 6;
     const int rl = w * (64 / CPR) + lane / CPR;             // row within block 0 of this wave
     const int cl = (lane % CPR) ^ swz<CPR>(rl);             // source chunk
     const uint16_t* tbase = base + (long long)row0 * ld + col0;
@@ -394,36 +398,6 @@ __device__ __forceinline__ void codes_dma(int* dst_ts, int* dst_code, const int*
         const uint32_t voff = (uint32_t)min(tid, ntok - 1 - tok0) * 4u;
         lds_dma4(lds_address(dst_ts), uniform_ptr(ts + tok0), voff);
         lds_dma4(lds_address(dst_code), uniform_ptr(code + tok0), voff);
-    }
-}
-
-// The same copies issued with the compiler builtin: the compiler then tracks them and waits for
-// every outstanding copy before the next LDS read it cannot prove disjoint.  Kept for the dK/dV
-// kernel, whose registers are at the limit: there the builtin form measured faster (its
-// addresses need fewer live registers than the scalar-base form above).
-template <int DH>
-__device__ __forceinline__ void tile_dma_tracked(uint16_t* tile, const uint16_t* base, long long ld,
-                                                 int row0, int nrows, int col0, int tid) {
-    constexpr int CPR = DH / 8;
-    const int lane = tid & 63, w = tid >> 6;
-#pragma unroll
-    for (int i = 0; i < DH / 32; i++) {
-        const int blk = __builtin_amdgcn_readfirstlane(i * 4 + w);
-        const int pos = blk * 64 + lane;
-        const int row = pos / CPR;
-        const int chunk = (pos % CPR) ^ swz<CPR>(row);
-        const int grow = min(row0 + row, nrows - 1);
-        const uint16_t* src = base + (long long)grow * ld + col0 + chunk * 8;
-        __builtin_amdgcn_global_load_lds((const void*)src, (lds_void*)(tile + blk * 512), 16, 0, 0);
-    }
-}
-
-__device__ __forceinline__ void codes_dma_tracked(int* dst_ts, int* dst_code, const int* ts,
-                                                  const int* code, int tok0, int ntok, int tid) {
-    if (tid < 64) {
-        const int t = min(tok0 + tid, ntok - 1);
-        __builtin_amdgcn_global_load_lds((const void*)(ts + t), (lds_void*)dst_ts, 4, 0, 0);
-        __builtin_amdgcn_global_load_lds((const void*)(code + t), (lds_void*)dst_code, 4, 0, 0);
     }
 }
 

@@ -124,7 +124,8 @@ typedef struct {
  *   backward = 1: the plan plus room for dS as bf16 64 x 64 blocks (an upper bound of
  *     H * sum_b ceil(n_b / 64)^2 blocks of 8 KB, from T, B and max_seqlen).  With it the
  *     bf16 backward stores dS from its dk/dv kernel and forms dq from it (fewer operations;
- *     the same values).  The first bytes have the backward = 0 layout, so one plan serves. */
+ *     the same dS operand, so dq differs from the recomputing form only in the order of its
+ *     float sums).  The first bytes have the backward = 0 layout, so one plan serves. */
 mtgr_status_t mtgr_hstu_attn_workspace_size(const mtgr_hstu_problem_t* p, int backward,
                                             size_t* bytes);
 

@@ -16,8 +16,8 @@ using bwd::zero;
 // LDS instead of registers keeps the wave within 256 VGPRs without spilling: a scratch reload
 // issued after a prefetch would have to wait for that prefetch (vector-memory operations
 // complete in issue order), serialising copy and compute.
-// With STORE it also writes dS (bf16, the A operand of its dK product) as 64 x 64 blocks
-// for the dQ-from-dS kernel; it forms drab when a.drab is set.
+// With STORE it also writes dS (bf16, the A operand of its dK product, masked but without the
+// factor 1 / n_b) as 64 x 64 blocks for the dQ-from-dS kernel; it forms drab when a.drab is set.
 template <int DH, bool RAB, bool STORE>
 __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) {
     constexpr int CPR = DH / 8, KSTEPS = DH / 16, DBLK = DH / 32, UNIT = 32 * DH;
@@ -41,6 +41,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
     const int ntq = (nb + BN - 1) / BN;
     const float inv_n = 1.0f / (float)nb;
     const float alpha = a.alpha;
+    const float c_exp = -1.4426950408889634f * alpha;   // sigmoid(alpha s) = 1 / (1 + 2^(c_exp s))
     const int4* summ = a.summ + (long long)b * a.ntile;
     TileSummary sk = load_summary(summ, 2 * kt);
     if (2 * kt + 1 < ntq) sk = combine(sk, load_summary(summ, 2 * kt + 1));
@@ -148,15 +149,23 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
             for (int e = 0; e < 2; e++) {
                 const int rr = r + e;
                 const int ql = 8 * (rr >> 2) + 4 * hh + (rr & 3);
-                float x = sacc[rr] * alpha;
+                // p and ds are P and dS without the per-user factor 1 / n_b (and, without a
+                // relative bias, P without alpha): the factors are applied once to dK, dV, dQ
+                // and drab.  silu'(x) = sg (1 + x (1 - sg)) and alpha s (1 - sg) = alpha (s - p).
                 int bk = 0;
+                float p, ds;
                 if (RAB) {
                     bk = rab_bucket(qts[ql], kts, a.nbuckets);
-                    x += sRab[bk];
+                    const float x = sacc[rr] * alpha + sRab[bk];
+                    float sg;
+                    p = silu_sig(x, sg);
+                    ds = dpacc[rr] * sg * (1.0f + x * (1.0f - sg));
+                } else {
+                    const float sv = sacc[rr];
+                    const float sg = __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(sv * c_exp));
+                    p = sv * sg;
+                    ds = (dpacc[rr] * sg) * __builtin_fmaf(alpha, sv - p, 1.0f);
                 }
-                float sg;
-                float p = silu_sig(x, sg) * inv_n;
-                float ds = dpacc[rr] * sg * (1.0f + x * (1.0f - sg)) * inv_n;
                 if (cls == TILE_PARTIAL) {
                     const bool vis = visible(qcode[ql], qts[ql], qb + ql, kcode, kts, kj);
                     p = vis ? p : 0.f;
@@ -203,11 +212,13 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
 
     if (want_drab) {
         __syncthreads();   // every wave's histogram updates have landed
-        if (tid < a.nbuckets && sHist[tid] != 0.f) atomicAdd(&a.drab[h * a.nbuckets + tid], sHist[tid]);
+        if (tid < a.nbuckets && sHist[tid] != 0.f)
+            atomicAdd(&a.drab[h * a.nbuckets + tid], sHist[tid] * inv_n);
     }
     // dK / dV accumulators: lane = feature column, registers = key rows.  Each wave stages
     // its 32 rows in a swizzled 32-row tile inside the K tile.
     uint16_t* sO = sK + w * 32 * DH;
+    const float dk_scale = alpha * inv_n, dv_scale = RAB ? inv_n : alpha * inv_n;
     uint16_t* DK = (uint16_t*)a.dk;
     uint16_t* DV = (uint16_t*)a.dv;
 #pragma unroll
@@ -219,7 +230,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
             for (int r = 0; r < 16; r++) {
                 const int krow = 8 * (r >> 2) + 4 * hh + (r & 3);
                 const int dd = 32 * d + col;
-                const float val = which == 0 ? alpha * dkacc[d][r] : dvacc[d][r];
+                const float val = which == 0 ? dk_scale * dkacc[d][r] : dv_scale * dvacc[d][r];
                 sO[8 * tile_chunk<CPR>(krow, dd >> 3) + (dd & 7)] = (uint16_t)f32_to_bf16_bits(val);
             }
         }

@@ -30,6 +30,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
     const int ntk = (nb + BN - 1) / BN;
     const float inv_n = 1.0f / (float)nb;
     const float alpha = a.alpha;
+    const float c_exp = -1.4426950408889634f * alpha;   // sigmoid(alpha s) = 1 / (1 + 2^(c_exp s))
     const int4* summ = a.summ + (long long)b * a.ntile;
     TileSummary sq = load_summary(summ, 2 * qt);
     if (2 * qt + 1 < ntk) sq = combine(sq, load_summary(summ, 2 * qt + 1));
@@ -111,15 +112,20 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
                 for (int e = 0; e < 2; e++) {
                     const int rr = r + e;
                     const int kl = 32 * blk + 8 * (rr >> 2) + 4 * hh + (rr & 3);
-                    float x = sacc[rr] * alpha;
+                    // ds is dS without the per-user factor 1 / n_b, applied once to dQ and drab.
                     int bk = 0;
+                    float ds;
                     if (RAB) {
                         bk = rab_bucket(qts, kts[kl], a.nbuckets);
-                        x += sRab[bk];
+                        const float x = sacc[rr] * alpha + sRab[bk];
+                        float sg;
+                        silu_sig(x, sg);
+                        ds = dpacc[rr] * sg * (1.0f + x * (1.0f - sg));
+                    } else {
+                        const float sv = sacc[rr];
+                        const float sg = __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(sv * c_exp));
+                        ds = (dpacc[rr] * sg) * __builtin_fmaf(alpha, __builtin_fmaf(-sv, sg, sv), 1.0f);
                     }
-                    float sg;
-                    silu_sig(x, sg);
-                    float ds = dpacc[rr] * sg * (1.0f + x * (1.0f - sg)) * inv_n;
                     if (cls == TILE_PARTIAL)
                         ds = visible(qcode, qts, qi, kcode[kl], kts[kl], t * BN + kl) ? ds : 0.f;
                     else if (!qvalid)
@@ -145,16 +151,18 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
         cur ^= 1;
     }
 
-    if (want_drab && tid < a.nbuckets && sHist[tid] != 0.f) atomicAdd(&a.drab[h * a.nbuckets + tid], sHist[tid]);
+    if (want_drab && tid < a.nbuckets && sHist[tid] != 0.f)
+        atomicAdd(&a.drab[h * a.nbuckets + tid], sHist[tid] * inv_n);
     uint16_t* sO = (w < 2 ? sK0 : sK1) + (w & 1) * 32 * DH;
+    const float dq_scale = alpha * inv_n;
 #pragma unroll
     for (int d = 0; d < DBLK; d++) {
 #pragma unroll
         for (int g = 0; g < 4; g++) {
             const int dd = 32 * d + 8 * g + 4 * hh;
             *(uint2*)&sO[8 * tile_chunk<CPR>(col, dd >> 3) + (dd & 7)] =
-                make_uint2(pack_bf16x2(alpha * dqacc[d][4 * g + 0], alpha * dqacc[d][4 * g + 1]),
-                           pack_bf16x2(alpha * dqacc[d][4 * g + 2], alpha * dqacc[d][4 * g + 3]));
+                make_uint2(pack_bf16x2(dq_scale * dqacc[d][4 * g + 0], dq_scale * dqacc[d][4 * g + 1]),
+                           pack_bf16x2(dq_scale * dqacc[d][4 * g + 2], dq_scale * dqacc[d][4 * g + 3]));
         }
     }
     __syncthreads();

@@ -9,7 +9,7 @@ using bwd::zero;
 
 // ------------------------------------------------------------------ dQ from stored dS, bf16
 // dQ^T (dh x 32 queries) += K^T dS^T over the user's visible 64-key tiles, with dS read from the
-// blocks the dK/dV kernel stored (64 keys x 64 queries, already masked and scaled by 1 / n_b,
+// blocks the dK/dV kernel stored (64 keys x 64 queries, already masked; 1 / n_b is applied here,
 // in that kernel's register-fragment order: four 2 KB sub-blocks (query half, key half), each
 // chunk (kq, g, lane) holding 4 queries 16 kq + 8 g + 4 (lane / 32) + 0..3 of key lane % 32).
 // Per key tile the K tile and the two dS blocks of the workgroup's 128 queries stream through
@@ -32,7 +32,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_ds_bf16_kernel(AttnArgs a)
     const int ob = a.offsets[b], nb = a.offsets[b + 1] - ob;
     const int q0 = qt * BM;
     const int ntk = (nb + BN - 1) / BN;
-    const float alpha = a.alpha;
+    const float scale = a.alpha / (float)nb;   // the stored dS lacks the factor 1 / n_b
     const int4* summ = a.summ + (long long)b * a.ntile;
     TileSummary sq = load_summary(summ, 2 * qt);
     if (2 * qt + 1 < ntk) sq = combine(sq, load_summary(summ, 2 * qt + 1));
@@ -133,8 +133,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_ds_bf16_kernel(AttnArgs a)
         for (int g = 0; g < 4; g++) {
             const int dd = 32 * d + 8 * g + 4 * hh;
             *(uint2*)&sO[8 * tile_chunk<CPR>(col, dd >> 3) + (dd & 7)] =
-                make_uint2(pack_bf16x2(alpha * dqacc[d][4 * g + 0], alpha * dqacc[d][4 * g + 1]),
-                           pack_bf16x2(alpha * dqacc[d][4 * g + 2], alpha * dqacc[d][4 * g + 3]));
+                make_uint2(pack_bf16x2(scale * dqacc[d][4 * g + 0], scale * dqacc[d][4 * g + 1]),
+                           pack_bf16x2(scale * dqacc[d][4 * g + 2], scale * dqacc[d][4 * g + 3]));
         }
     }
     __syncthreads();

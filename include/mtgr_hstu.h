@@ -19,7 +19,8 @@
  *     offsets[0] = 0, offsets[b] <= offsets[b+1], offsets[B] = total_tokens and
  *     offsets[b+1] - offsets[b] <= max_seqlen; seg[t] must lie in 0..3 and
  *     group ids in 0..G-1.  These device-resident preconditions are not checked
- *     (checking them would need a synchronisation); violating them is undefined.
+ *     by the hot-path calls (checking them would need a synchronisation);
+ *     violating them is undefined.  mtgr_debug_validate_inputs checks them.
  *   - B = 0 or T = 0 is a successful no-op (outputs of size zero; parameter
  *     gradients are zero-filled).
  *   - Every function is stateless and may be called concurrently from several
@@ -210,6 +211,27 @@ mtgr_status_t mtgr_group_layernorm_bwd(const mtgr_gln_problem_t* p, const void* 
                                        const float* mean, const float* rstd, void* dx, void* du,
                                        float* dgamma, float* dbeta, void* workspace,
                                        size_t workspace_bytes, mtgr_stream_t stream);
+
+/* Bytes of device scratch that mtgr_debug_validate_inputs needs. */
+#define MTGR_VALIDATE_SCRATCH_BYTES 64
+
+/* Debugging aid, not for the hot path: checks the device-resident preconditions that the
+ * other calls assume of a jagged batch (the layout of Sec. 4.1, Eq. 3 and Eq. 4) and
+ * WAITS for the result (it synchronises `stream`).
+ *   offsets [B+1] int32: offsets[0] = 0, offsets[b] <= offsets[b+1], offsets[B] = T and
+ *     offsets[b+1] - offsets[b] <= max_seqlen, with B, T, max_seqlen from `p`;
+ *   seg [T] int8 in 0..3 (MTGR_SEG_*);
+ *   group_ids [T] int8 in 0..num_groups-1, checked only when group_ids is not NULL.
+ * scratch: device memory of at least MTGR_VALIDATE_SCRATCH_BYTES, 8-byte aligned; its
+ * contents are overwritten.  Returns MTGR_SUCCESS when every condition holds, else
+ * MTGR_ERROR_INVALID_ARGUMENT with mtgr_last_error_message() naming the first index of each
+ * violated condition.  Only p->num_users, p->total_tokens and p->max_seqlen are read.
+ * Reads offsets[0..B] and seg[0..T-1] (group_ids[0..T-1]) only, so invalid values cannot
+ * make it read out of bounds. */
+mtgr_status_t mtgr_debug_validate_inputs(const mtgr_hstu_problem_t* p, const int32_t* offsets,
+                                         const int8_t* seg, const int8_t* group_ids,
+                                         int32_t num_groups, void* scratch, size_t scratch_bytes,
+                                         mtgr_stream_t stream);
 
 /* Static string for a status code. */
 const char* mtgr_status_string(mtgr_status_t status);

@@ -461,6 +461,46 @@ mtgr_status_t mtgr_group_layernorm_bwd(const mtgr_gln_problem_t* p, const void* 
     return ok();
 }
 
+mtgr_status_t mtgr_debug_validate_inputs(const mtgr_hstu_problem_t* p, const int32_t* offsets,
+                                         const int8_t* seg, const int8_t* group_ids,
+                                         int32_t num_groups, void* scratch, size_t scratch_bytes,
+                                         mtgr_stream_t stream) {
+    static_assert(MTGR_VALIDATE_SCRATCH_BYTES >= mtgr::VALIDATE_CONDITIONS * 8, "scratch size");
+    if (p == nullptr) return fail(MTGR_ERROR_NULL_POINTER, "p is NULL");
+    if (p->num_users < 0 || p->total_tokens < 0 || p->max_seqlen < 0)
+        return fail(MTGR_ERROR_INVALID_ARGUMENT, "num_users, total_tokens and max_seqlen must be >= 0");
+    if (offsets == nullptr) return fail(MTGR_ERROR_NULL_POINTER, "offsets is NULL");
+    if (p->total_tokens > 0 && seg == nullptr) return fail(MTGR_ERROR_NULL_POINTER, "seg is NULL");
+    if (group_ids != nullptr && (num_groups < 1 || num_groups > 127))
+        return fail(MTGR_ERROR_INVALID_ARGUMENT, "num_groups = %d outside 1..127", num_groups);
+    if (scratch == nullptr) return fail(MTGR_ERROR_NULL_POINTER, "scratch is NULL");
+    if (scratch_bytes < MTGR_VALIDATE_SCRATCH_BYTES)
+        return fail(MTGR_ERROR_WORKSPACE_TOO_SMALL, "scratch has %zu bytes, needs %d", scratch_bytes,
+                    MTGR_VALIDATE_SCRATCH_BYTES);
+    if (((uintptr_t)scratch & 7u) != 0) return fail(MTGR_ERROR_INVALID_ARGUMENT, "scratch is not 8-byte aligned");
+    hipStream_t s = (hipStream_t)stream;
+    unsigned long long* first = (unsigned long long*)scratch;
+    hipError_t e = mtgr::launch_validate(offsets, p->num_users, p->total_tokens, p->max_seqlen, seg,
+                                         group_ids, num_groups, first, s);
+    if (e != hipSuccess) return device_fail(e, "validate inputs");
+    unsigned long long h[mtgr::VALIDATE_CONDITIONS];
+    e = hipMemcpyAsync(h, first, sizeof(h), hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return device_fail(e, "validate inputs (copy back)");
+    static const char* const what[mtgr::VALIDATE_CONDITIONS] = {
+        "offsets[0] != 0", "offsets decrease after user", "offsets[num_users] != total_tokens",
+        "sequence longer than max_seqlen: user", "seg outside 0..3 at token", "group id outside 0..G-1 at token"};
+    std::string msg;
+    for (int c = 0; c < mtgr::VALIDATE_CONDITIONS; c++) {
+        if (h[c] == ~0ull) continue;
+        char buf[96];
+        snprintf(buf, sizeof(buf), "%s%s %llu", msg.empty() ? "" : "; ", what[c], h[c]);
+        msg += buf;
+    }
+    if (!msg.empty()) return fail(MTGR_ERROR_INVALID_ARGUMENT, "%s", msg.c_str());
+    return ok();
+}
+
 const char* mtgr_status_string(mtgr_status_t status) {
     switch (status) {
         case MTGR_SUCCESS: return "success";

@@ -97,4 +97,11 @@ constexpr int ATTN_TILE_F32 = 64;     // rows per work item, fp32 kernels
 constexpr int SCHED_BUCKETS = 4096;   // length buckets of the heavy-first sort
 constexpr int XCDS = 8;               // accelerator complex dies of an MI355X
 
+// Debug validation of a jagged batch: `first` (VALIDATE_CONDITIONS 64-bit slots of device
+// memory) receives per condition the smallest failing index, ~0 if none.
+constexpr int VALIDATE_CONDITIONS = 6;
+hipError_t launch_validate(const int* offsets, int num_users, long long total, int max_seqlen,
+                           const int8_t* seg, const int8_t* group_ids, int groups,
+                           unsigned long long* first, hipStream_t s);
+
 }  // namespace mtgr

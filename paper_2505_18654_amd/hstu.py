@@ -30,11 +30,12 @@ MTGR_BWD_SKIP_DQ = 2
 MTGR_BWD_SKIP_DKDV = 4
 MTGR_BWD_KEEP_DS = 8
 MTGR_BWD_DS_READY = 16
+MTGR_VALIDATE_SCRATCH_BYTES = 64
 
 EXPORTED = (
     "mtgr_hstu_attn_workspace_size", "mtgr_hstu_attn_plan", "mtgr_hstu_attn_fwd", "mtgr_hstu_attn_bwd",
     "mtgr_group_layernorm_workspace_size", "mtgr_group_layernorm_fwd", "mtgr_group_layernorm_bwd",
-    "mtgr_status_string", "mtgr_last_error_message", "mtgr_version",
+    "mtgr_debug_validate_inputs", "mtgr_status_string", "mtgr_last_error_message", "mtgr_version",
 )
 
 
@@ -87,10 +88,11 @@ def lib() -> ctypes.CDLL:
         L.mtgr_group_layernorm_workspace_size.argtypes = [G, ctypes.c_int, ctypes.POINTER(sz)]
         L.mtgr_group_layernorm_fwd.argtypes = [G, vp, vp, vp, vp, vp, vp, vp, vp, vp]
         L.mtgr_group_layernorm_bwd.argtypes = [G, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.mtgr_debug_validate_inputs.argtypes = [P, vp, vp, vp, i32, vp, sz, vp]
         for name in ("mtgr_hstu_attn_workspace_size", "mtgr_hstu_attn_plan", "mtgr_hstu_attn_fwd",
                      "mtgr_hstu_attn_bwd",
                      "mtgr_group_layernorm_workspace_size", "mtgr_group_layernorm_fwd",
-                     "mtgr_group_layernorm_bwd"):
+                     "mtgr_group_layernorm_bwd", "mtgr_debug_validate_inputs"):
             getattr(L, name).restype = ctypes.c_int
         L.mtgr_status_string.argtypes = [ctypes.c_int]
         L.mtgr_status_string.restype = ctypes.c_char_p
@@ -186,6 +188,13 @@ def mtgr_group_layernorm_bwd(problem, dy, x, u, group_ids, gamma, mean, rstd, dx
                                           _ptr(group_ids), _ptr(gamma), _ptr(mean), _ptr(rstd),
                                           _ptr(dx), _ptr(du), _ptr(dgamma), _ptr(dbeta),
                                           _ptr(workspace), int(workspace_bytes), _stream(stream)))
+
+
+def mtgr_debug_validate_inputs(problem, offsets, seg, group_ids, num_groups, scratch, scratch_bytes,
+                               stream=None) -> None:
+    _check(lib().mtgr_debug_validate_inputs(ctypes.byref(problem), _ptr(offsets), _ptr(seg),
+                                            _ptr(group_ids), int(num_groups), _ptr(scratch),
+                                            int(scratch_bytes), _stream(stream)))
 
 
 # ------------------------------------------------------------------ problem builders

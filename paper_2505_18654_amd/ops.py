@@ -76,6 +76,15 @@ def attn_problem(jag: Jagged, q, k, v, out, rab=None, alpha: float = 1.0,
                              _token_stride(out, row), flags)
 
 
+def validate_batch(jag: Jagged, group_ids=None, num_groups: int = 0, scratch=None) -> None:
+    """Debugging aid (synchronises): checks offsets, seg and optional group ids on the device
+    through mtgr_debug_validate_inputs; raises hstu.MtgrError naming the first bad index."""
+    p = hstu.attn_problem(jag.num_users, jag.total_tokens, jag.max_seqlen, 1, 16)
+    if scratch is None:
+        scratch = torch.empty(hstu.MTGR_VALIDATE_SCRATCH_BYTES, dtype=torch.uint8, device=jag.offsets.device)
+    hstu.mtgr_debug_validate_inputs(p, jag.offsets, jag.seg, group_ids, num_groups, scratch, scratch.numel())
+
+
 def attn_plan(q, jag: Jagged, workspace=None, rab=None, backward: bool = False):
     """Builds the batch plan (tile summaries + work list) once; pass the returned workspace
     with planned=True to attn_fwd / attn_bwd for every layer on the same batch.  backward=True

@@ -245,3 +245,30 @@ def test_missing_library_fails_loudly(monkeypatch, tmp_path):
     monkeypatch.setattr(hstu, "LIB_PATH", str(tmp_path / "absent.so"))
     with pytest.raises(hstu.MtgrLibraryMissing):
         hstu.lib()
+
+
+def validate(p, **over):
+    args = dict(offsets=FAKE, seg=FAKE, group_ids=None, num_groups=0, scratch=FAKE,
+                scratch_bytes=hstu.MTGR_VALIDATE_SCRATCH_BYTES)
+    args.update(over)
+    hstu.mtgr_debug_validate_inputs(p, args["offsets"], args["seg"], args["group_ids"], args["num_groups"],
+                                    args["scratch"], args["scratch_bytes"], 0)
+
+
+@pytest.mark.parametrize("over,status", [
+    (dict(offsets=None), hstu.MTGR_ERROR_NULL_POINTER),
+    (dict(seg=None), hstu.MTGR_ERROR_NULL_POINTER),
+    (dict(scratch=None), hstu.MTGR_ERROR_NULL_POINTER),
+    (dict(scratch_bytes=hstu.MTGR_VALIDATE_SCRATCH_BYTES - 1), hstu.MTGR_ERROR_WORKSPACE_TOO_SMALL),
+    (dict(scratch=FAKE + 4), hstu.MTGR_ERROR_INVALID_ARGUMENT),
+    (dict(group_ids=FAKE, num_groups=0), hstu.MTGR_ERROR_INVALID_ARGUMENT),
+    (dict(group_ids=FAKE, num_groups=128), hstu.MTGR_ERROR_INVALID_ARGUMENT),
+])
+def test_validate_inputs_host_checks(over, status):
+    """Host-side argument checks of the debug validator (before any device work)."""
+    with pytest.raises(hstu.MtgrError) as e:
+        validate(prob(), **over)
+    assert e.value.status == status
+    with pytest.raises(hstu.MtgrError) as e:
+        validate(prob(num_users=-1))
+    assert e.value.status == hstu.MTGR_ERROR_INVALID_ARGUMENT

@@ -29,7 +29,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
     __shared__ int sQts[2][32];
     __shared__ int sQcode[2][32];
     __shared__ float sRab[MTGR_RAB_LDS];
-    __shared__ float sHist[MTGR_RAB_LDS];
+    __shared__ float sHist[RAB ? bwd::HIST_WORDS : 1];
 
     const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int2 item = a.items[blockIdx.x];
@@ -66,9 +66,9 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
         if (kvalid) g = ldg16(V + (long long)(ob + kj) * a.ld_v + h * DH + 16 * kk + 8 * hh);
         vreg[kk] = as_bf16x8(g);
     }
-    if (RAB && tid < MTGR_RAB_LDS) {
-        sRab[tid] = tid < a.nbuckets ? a.rab[h * a.nbuckets + tid] : 0.f;
-        sHist[tid] = 0.f;
+    if (RAB) {
+        if (tid < MTGR_RAB_LDS) sRab[tid] = tid < a.nbuckets ? a.rab[h * a.nbuckets + tid] : 0.f;
+        bwd::hist_zero(sHist, tid);
     }
     // stored dS: block (query tile q, key tile k) of this (user, head) is ds_blk + q ntq + k;
     // this wave's 32 keys are keys 32 (w & 1) .. 32 (w & 1) + 31 of key tile kblk.
@@ -106,6 +106,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
         issue(t, 0, 0);
     }
     wait_vmcnt_seen<0>();   // K, V, the first unit
+    bwd::HistRun run;   // drab: this lane's current run of equal buckets
     bool first = true;
     while (t < ntq) {
         // The copy of this unit was issued before the previous unit's 4 dS stores.
@@ -142,21 +143,31 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
             dpacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ga, vreg[kk], dpacc, 0, 0, 0);
         }
         uint32_t pk[2][4], dsk[2][4];
+        // Elements 4 q4 .. 4 q4 + 3 belong to queries 8 q4 + 4 hh + 0..3.  Work in groups of
+        // four, each LDS access kind issued for the whole group before its results are used:
+        // one round trip per group for the timestamps and one for the bias values, instead of
+        // a chain of dependent LDS reads (and histogram atomics) per element.
 #pragma unroll
-        for (int r = 0; r < 16; r += 2) {
-            float pv[2], dv[2];
+        for (int q4 = 0; q4 < 4; q4++) {
+            const int ql0 = 8 * q4 + 4 * hh;
+            int bk[4] = {0, 0, 0, 0};
+            float rb[4] = {0.f, 0.f, 0.f, 0.f};
+            if (RAB) {
 #pragma unroll
-            for (int e = 0; e < 2; e++) {
-                const int rr = r + e;
-                const int ql = 8 * (rr >> 2) + 4 * hh + (rr & 3);
+                for (int e = 0; e < 4; e++) bk[e] = rab_bucket(qts[ql0 + e], kts, a.nbuckets);
+#pragma unroll
+                for (int e = 0; e < 4; e++) rb[e] = sRab[bk[e]];
+            }
+            float pv[4], dv[4];
+#pragma unroll
+            for (int e = 0; e < 4; e++) {
+                const int rr = 4 * q4 + e;
                 // p and ds are P and dS without the per-user factor 1 / n_b (and, without a
                 // relative bias, P without alpha): the factors are applied once to dK, dV, dQ
                 // and drab.  silu'(x) = sg (1 + x (1 - sg)) and alpha s (1 - sg) = alpha (s - p).
-                int bk = 0;
                 float p, ds;
                 if (RAB) {
-                    bk = rab_bucket(qts[ql], kts, a.nbuckets);
-                    const float x = sacc[rr] * alpha + sRab[bk];
+                    const float x = sacc[rr] * alpha + rb[e];
                     float sg;
                     p = silu_sig(x, sg);
                     ds = dpacc[rr] * sg * (1.0f + x * (1.0f - sg));
@@ -167,16 +178,22 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
                     ds = (dpacc[rr] * sg) * __builtin_fmaf(alpha, sv - p, 1.0f);
                 }
                 if (cls == TILE_PARTIAL) {
+                    const int ql = ql0 + e;
                     const bool vis = visible(qcode[ql], qts[ql], qb + ql, kcode, kts, kj);
                     p = vis ? p : 0.f;
                     ds = vis ? ds : 0.f;
                 }
-                if (want_drab && ds != 0.f) atomicAdd(&sHist[bk], ds);
                 pv[e] = p;
                 dv[e] = ds;
             }
-            pk[r >> 3][(r & 7) >> 1] = pack_bf16x2(pv[0], pv[1]);
-            dsk[r >> 3][(r & 7) >> 1] = pack_bf16x2(dv[0], dv[1]);
+            pk[q4 >> 1][2 * (q4 & 1)] = pack_bf16x2(pv[0], pv[1]);
+            pk[q4 >> 1][2 * (q4 & 1) + 1] = pack_bf16x2(pv[2], pv[3]);
+            dsk[q4 >> 1][2 * (q4 & 1)] = pack_bf16x2(dv[0], dv[1]);
+            dsk[q4 >> 1][2 * (q4 & 1) + 1] = pack_bf16x2(dv[2], dv[3]);
+            if (want_drab) {
+#pragma unroll
+                for (int e = 0; e < 4; e++) run.add(sHist, lane, bk[e], dv[e]);
+            }
         }
         if (store_rows) {
             // Sub-block (query half, key half) of block (t, kblk), 2 KB in register-fragment
@@ -211,9 +228,12 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
     }
 
     if (want_drab) {
+        run.flush(sHist, lane);
         __syncthreads();   // every wave's histogram updates have landed
-        if (tid < a.nbuckets && sHist[tid] != 0.f)
-            atomicAdd(&a.drab[h * a.nbuckets + tid], sHist[tid] * inv_n);
+        if (tid < a.nbuckets) {
+            const float v = bwd::hist_total(sHist, tid);
+            if (v != 0.f) atomicAdd(&a.drab[h * a.nbuckets + tid], v * inv_n);
+        }
     }
     // dK / dV accumulators: lane = feature column, registers = key rows.  Each wave stages
     // its 32 rows in a swizzled 32-row tile inside the K tile.

@@ -18,7 +18,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
     __shared__ int sKts[2][BN];
     __shared__ int sKcode[2][BN];
     __shared__ float sRab[MTGR_RAB_LDS];
-    __shared__ float sHist[MTGR_RAB_LDS];
+    __shared__ float sHist[RAB ? bwd::HIST_WORDS : 1];
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int2 item = a.items[blockIdx.x];
@@ -58,9 +58,9 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
         qreg[kk] = as_bf16x8(u);
         doreg[kk] = as_bf16x8(g);
     }
-    if (RAB && tid < MTGR_RAB_LDS) {
-        sRab[tid] = tid < a.nbuckets ? a.rab[h * a.nbuckets + tid] : 0.f;
-        sHist[tid] = 0.f;
+    if (RAB) {
+        if (tid < MTGR_RAB_LDS) sRab[tid] = tid < a.nbuckets ? a.rab[h * a.nbuckets + tid] : 0.f;
+        bwd::hist_zero(sHist, tid);
     }
     floatx16 dqacc[DBLK];
 #pragma unroll
@@ -80,6 +80,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
     int cls, cls_n;
     int t = walk.next(0, &cls);
     int cur = 0;
+    bwd::HistRun run;   // drab: this lane's current run of equal buckets
     if (t < ntk) issue(t, 0);
     while (t < ntk) {
         wait_vmem();
@@ -105,19 +106,28 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
                 dpacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, doreg[kk], dpacc, 0, 0, 0);
             }
             uint32_t dsk[2][4];
+            // Elements 4 q4 .. 4 q4 + 3 belong to keys 32 blk + 8 q4 + 4 hh + 0..3; groups of
+            // four issue their LDS reads (timestamps, bias values) before using them.
 #pragma unroll
-            for (int r = 0; r < 16; r += 2) {
-                float dv[2];
+            for (int q4 = 0; q4 < 4; q4++) {
+                const int kl0 = 32 * blk + 8 * q4 + 4 * hh;
+                int bk[4] = {0, 0, 0, 0};
+                float rb[4] = {0.f, 0.f, 0.f, 0.f};
+                if (RAB) {
 #pragma unroll
-                for (int e = 0; e < 2; e++) {
-                    const int rr = r + e;
-                    const int kl = 32 * blk + 8 * (rr >> 2) + 4 * hh + (rr & 3);
+                    for (int e = 0; e < 4; e++) bk[e] = rab_bucket(qts, kts[kl0 + e], a.nbuckets);
+#pragma unroll
+                    for (int e = 0; e < 4; e++) rb[e] = sRab[bk[e]];
+                }
+                float dv[4];
+#pragma unroll
+                for (int e = 0; e < 4; e++) {
+                    const int rr = 4 * q4 + e;
+                    const int kl = kl0 + e;
                     // ds is dS without the per-user factor 1 / n_b, applied once to dQ and drab.
-                    int bk = 0;
                     float ds;
                     if (RAB) {
-                        bk = rab_bucket(qts, kts[kl], a.nbuckets);
-                        const float x = sacc[rr] * alpha + sRab[bk];
+                        const float x = sacc[rr] * alpha + rb[e];
                         float sg;
                         silu_sig(x, sg);
                         ds = dpacc[rr] * sg * (1.0f + x * (1.0f - sg));
@@ -130,10 +140,14 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
                         ds = visible(qcode, qts, qi, kcode[kl], kts[kl], t * BN + kl) ? ds : 0.f;
                     else if (!qvalid)
                         ds = 0.f;
-                    if (want_drab && ds != 0.f) atomicAdd(&sHist[bk], ds);
                     dv[e] = ds;
                 }
-                dsk[r >> 3][(r & 7) >> 1] = pack_bf16x2(dv[0], dv[1]);
+                dsk[q4 >> 1][2 * (q4 & 1)] = pack_bf16x2(dv[0], dv[1]);
+                dsk[q4 >> 1][2 * (q4 & 1) + 1] = pack_bf16x2(dv[2], dv[3]);
+                if (want_drab) {
+#pragma unroll
+                    for (int e = 0; e < 4; e++) run.add(sHist, lane, bk[e], dv[e]);
+                }
             }
 #pragma unroll
             for (int kq = 0; kq < 2; kq++) {
@@ -151,8 +165,14 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
         cur ^= 1;
     }
 
-    if (want_drab && tid < a.nbuckets && sHist[tid] != 0.f)
-        atomicAdd(&a.drab[h * a.nbuckets + tid], sHist[tid] * inv_n);
+    if (want_drab) {
+        run.flush(sHist, lane);
+        __syncthreads();   // zeroing (when no tile was visited) and every histogram update
+        if (tid < a.nbuckets) {
+            const float v = bwd::hist_total(sHist, tid);
+            if (v != 0.f) atomicAdd(&a.drab[h * a.nbuckets + tid], v * inv_n);
+        }
+    }
     uint16_t* sO = (w < 2 ? sK0 : sK1) + (w & 1) * 32 * DH;
     const float dq_scale = alpha * inv_n;
 #pragma unroll

@@ -260,6 +260,25 @@ def main():
     res = {"o": o}
     err = sampled_parity(layout, inp, res, check_users)
 
+    # Serving: the candidate rows alone (one pass per user scoring all of its candidates),
+    # timed apart from the step above; reported as an extra field, not as `value`.
+    cand_rows = None
+    if fwd_only:
+        o_c = torch.empty_like(q)
+        for _ in range(max(args.warmup, 1)):
+            ops.attn_fwd(q, k, v, jag, rab, out=o_c, workspace=ws, planned=True, cand_rows=True)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(args.steps):
+            ops.attn_fwd(q, k, v, jag, rab, out=o_c, workspace=ws, planned=True, cand_rows=True)
+        e1.record()
+        torch.cuda.synchronize()
+        ms_c = e0.elapsed_time(e1) / args.steps
+        n_cand = int(np.sum(layout.seg == 3))
+        cand_rows = {"attn_fwd_cand_rows_ms": ms_c, "candidates": n_cand,
+                     "candidates_per_s": n_cand / (ms_c * 1e-3),
+                     "full_attn_fwd_ms": stage_ms["attn_fwd"]}
+
     line = {
         "metric": METRIC,
         "value": T * args.steps / elapsed,
@@ -284,6 +303,8 @@ def main():
         "roofline": roofline,
         "parity_sampled_fwd": {"users": check_users, "max_err_over_rms": err},
     }
+    if cand_rows is not None:
+        line["serving_cand_rows"] = cand_rows
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(layout, args.cpu_seconds)
     print(json.dumps(line), flush=True)

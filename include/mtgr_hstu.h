@@ -72,6 +72,10 @@ enum {
                                   a previous MTGR_BWD_KEEP_DS call left in this workspace for
                                   the same batch, plan and inputs; drab must be NULL (that
                                   call formed it) */
+#define MTGR_FWD_CAND_ROWS 32u /* forward only: form and write only the output rows of
+                                  candidate tokens (seg = MTGR_SEG_CAND); every other row of
+                                  out is left untouched.  Work is skipped for 128-row query
+                                  tiles without a candidate.  Not valid for the backward. */
 
 #define MTGR_MAX_RAB_BUCKETS 64
 #define MTGR_MAX_HEADS 255
@@ -153,7 +157,11 @@ mtgr_status_t mtgr_hstu_attn_plan(const mtgr_hstu_problem_t* p, const int32_t* o
  * bucket(g) = g for g < 2, else 2e + [g >= 1.5 * 2^e] with e = floor(log2 g), g as uint32.
  *   offsets [B+1] int32, seg [T] int8, ts [T] int32 (seconds; any epoch).
  *   q, k, v [T, H, dh] (dtype), out [T, H, dh] (dtype, stride ld_o).
- *   workspace: at least mtgr_hstu_attn_workspace_size(p, 0) bytes, 256-byte aligned. */
+ *   workspace: at least mtgr_hstu_attn_workspace_size(p, 0) bytes, 256-byte aligned.
+ * With MTGR_FWD_CAND_ROWS only the candidates' rows are formed: the one pass per user that
+ * scores all of its candidates (user sample aggregation, Sec. 4.1, Eq. 3), e.g. at serving
+ * time when the user-side rows of the layer are not needed.  Each candidate row is the same
+ * as in a full forward of the batch (n_b still counts every token of the user). */
 mtgr_status_t mtgr_hstu_attn_fwd(const mtgr_hstu_problem_t* p, const int32_t* offsets,
                                  const int8_t* seg, const int32_t* ts, const void* q,
                                  const void* k, const void* v, const float* rab, void* out,

@@ -93,7 +93,7 @@ mtgr_status_t check_problem(const mtgr_hstu_problem_t* p) {
         return fail(MTGR_ERROR_INVALID_ARGUMENT, "num_rab_buckets %d outside 0..%d",
                     p->num_rab_buckets, MTGR_MAX_RAB_BUCKETS);
     if (p->flags & ~(MTGR_ATTN_PLANNED | MTGR_BWD_SKIP_DQ | MTGR_BWD_SKIP_DKDV | MTGR_BWD_KEEP_DS |
-                     MTGR_BWD_DS_READY))
+                     MTGR_BWD_DS_READY | MTGR_FWD_CAND_ROWS))
         return fail(MTGR_ERROR_INVALID_ARGUMENT, "unknown flags 0x%x", p->flags);
     if (!std::isfinite(p->alpha)) return fail(MTGR_ERROR_INVALID_ARGUMENT, "alpha is not finite");
     const long long row = (long long)p->num_heads * dh;
@@ -240,6 +240,7 @@ mtgr_status_t mtgr_hstu_attn_fwd(const mtgr_hstu_problem_t* p, const int32_t* of
     a.v = v;
     a.rab = rab;
     a.out = out;
+    a.cand_rows = (p->flags & MTGR_FWD_CAND_ROWS) ? 1 : 0;
     hipError_t e = p->dtype == MTGR_DTYPE_BF16
                        ? mtgr::launch_attn_fwd_bf16(a, p->head_dim, (int)L.slots, s)
                        : mtgr::launch_attn_fwd_f32(a, p->head_dim, (int)L.slots, s);
@@ -254,6 +255,8 @@ mtgr_status_t mtgr_hstu_attn_bwd(const mtgr_hstu_problem_t* p, const int32_t* of
                                  size_t workspace_bytes, mtgr_stream_t stream) {
     mtgr_status_t st = check_attn_common(p, offsets, seg, ts, rab, workspace, workspace_bytes);
     if (st != MTGR_SUCCESS) return st;
+    if (p->flags & MTGR_FWD_CAND_ROWS)
+        return fail(MTGR_ERROR_INVALID_ARGUMENT, "MTGR_FWD_CAND_ROWS applies to the forward only");
     if (drab && !rab) return fail(MTGR_ERROR_INVALID_ARGUMENT, "drab given without rab");
     if (drab && ((uintptr_t)drab & 3u) != 0)
         return fail(MTGR_ERROR_INVALID_ARGUMENT, "drab is not 4-byte aligned");

@@ -73,6 +73,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
 
     TileSummary sq = load_summary(summ, 2 * qt);
     if (2 * qt + 1 < ntk) sq = combine(sq, load_summary(summ, 2 * qt + 1));
+    if (a.cand_rows && !(sq.flags & TS_ANY_CAND)) return;   // no candidate row to form
 
     const int col = lane & 31, hh = lane >> 5;
     const int qi = q0 + w * 32 + col;
@@ -339,7 +340,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
     for (int i = 0; i < 32 * CPR / 64; i++) {
         const int c = lane + 64 * i, row = c / CPR, cc = c % CPR;
         const int qr = q0 + w * 32 + row;
-        if (qr < nb)
+        if (qr < nb && (!a.cand_rows || a.seg[ob + qr] == SEG_CAND))
             *(uint4*)(O + (long long)(ob + qr) * a.ld_o + h * DH + cc * 8) =
                 *(const uint4*)&sO[8 * tile_chunk<CPR>(row, cc)];
     }
@@ -365,6 +366,7 @@ __global__ __launch_bounds__(256) void attn_fwd_f32_kernel(AttnArgs a) {
     const float inv_n = 1.0f / (float)nb;
     const int4* summ = a.summ + (long long)b * a.ntile;
     const TileSummary sq = load_summary(summ, qt);
+    if (a.cand_rows && !(sq.flags & TS_ANY_CAND)) return;   // no candidate row to form
 
     const int qi = q0 + (tid >> 2), part = tid & 3;
     const bool qvalid = qi < nb;
@@ -419,7 +421,7 @@ __global__ __launch_bounds__(256) void attn_fwd_f32_kernel(AttnArgs a) {
             }
         }
     }
-    if (qvalid) {
+    if (qvalid && (!a.cand_rows || a.seg[ob + qi] == SEG_CAND)) {
         float* O = (float*)a.out;
 #pragma unroll
         for (int c = 0; c < Q4; c++) O[(long long)(ob + qi) * a.ld_o + h * DH + part * Q4 + c] = ov[c];

@@ -20,6 +20,7 @@ constexpr int TS_ANY_STATIC = 1;   // some valid token is USER/HIST
 constexpr int TS_ALL_STATIC = 2;   // all 64 slots are valid USER/HIST tokens
 constexpr int TS_ANY_RT = 4;       // some valid token is RT
 constexpr int TS_ANY_DYN = 8;      // some valid token is RT or CAND
+constexpr int TS_ANY_CAND = 16;    // some valid token is CAND
 constexpr int SUMMARY_TILE = 64;
 
 // Tile classes of a (query range, key range) pair.

@@ -27,11 +27,12 @@ struct AttnArgs {
     const int* tok_code;  // [T] per-token mask code (token_code of seg)
     const int2* items;    // work list: {user, (tile << 8) | head}, user < 0 = empty slot
     const long long* ds_off;  // [B+1] first stored-dS block of each user (H ceil(n_b/64)^2 blocks each)
-    uint16_t* ds;             // stored dS: 64 x 64 bf16 blocks, key-major
+    uint16_t* ds;             // stored dS: 64 x 64 bf16 blocks in the dK/dV kernel's fragment order
     int ntile;
     int heads;
     float alpha;
     int nbuckets;
+    int cand_rows;            // forward: write candidate rows only
 };
 
 // Number of physical work-list slots for tiles of `bm` rows (see build_schedule).

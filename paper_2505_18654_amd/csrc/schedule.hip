@@ -44,6 +44,7 @@ __global__ __launch_bounds__(256) void tile_summaries_kernel(const int* __restri
     if (st == ~0ull) flags |= TS_ALL_STATIC;
     if (__ballot(is_rt)) flags |= TS_ANY_RT;
     if (__ballot(is_dyn)) flags |= TS_ANY_DYN;
+    if (__ballot(valid && sg == SEG_CAND)) flags |= TS_ANY_CAND;
     const int mn = wave_min(is_rt ? tv : 0x7fffffff);
     const int mx = wave_max(is_dyn ? tv : (int)0x80000000);
     if (lane == 0) summ[(long long)b * ntile + t] = make_int4(flags, mn, mx, 0);

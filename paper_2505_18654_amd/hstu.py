@@ -30,6 +30,7 @@ MTGR_BWD_SKIP_DQ = 2
 MTGR_BWD_SKIP_DKDV = 4
 MTGR_BWD_KEEP_DS = 8
 MTGR_BWD_DS_READY = 16
+MTGR_FWD_CAND_ROWS = 32
 MTGR_VALIDATE_SCRATCH_BYTES = 64
 
 EXPORTED = (

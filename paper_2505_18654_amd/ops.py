@@ -102,11 +102,13 @@ def workspace_for(problem: hstu.HstuProblem, device, backward: bool = False) -> 
 
 
 def attn_fwd(q, k, v, jag: Jagged, rab=None, alpha: float = 1.0, out=None, workspace=None,
-             planned: bool = False):
-    """Eq. 5 forward: returns out [T, H, dh] (same dtype as q)."""
+             planned: bool = False, cand_rows: bool = False):
+    """Eq. 5 forward: returns out [T, H, dh] (same dtype as q).  cand_rows=True forms only the
+    candidate tokens' rows (the other rows of `out` are left as they were)."""
     if out is None:
         out = torch.empty_like(q, memory_format=torch.contiguous_format)
-    p = attn_problem(jag, q, k, v, out, rab, alpha, hstu.MTGR_ATTN_PLANNED if planned else 0)
+    flags = (hstu.MTGR_ATTN_PLANNED if planned else 0) | (hstu.MTGR_FWD_CAND_ROWS if cand_rows else 0)
+    p = attn_problem(jag, q, k, v, out, rab, alpha, flags)
     if workspace is None:
         workspace = workspace_for(p, q.device)
     hstu.mtgr_hstu_attn_fwd(p, jag.offsets, jag.seg, jag.ts, q, k, v, rab, out, workspace,

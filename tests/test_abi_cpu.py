@@ -76,7 +76,7 @@ def test_problem_validation(mutate, status):
 
 def test_unknown_flags_rejected():
     p = prob()
-    p.flags = 32
+    p.flags = 64
     with pytest.raises(hstu.MtgrError) as e:
         hstu.mtgr_hstu_attn_workspace_size(p)
     assert e.value.status == hstu.MTGR_ERROR_INVALID_ARGUMENT
@@ -272,3 +272,13 @@ def test_validate_inputs_host_checks(over, status):
     with pytest.raises(hstu.MtgrError) as e:
         validate(prob(num_users=-1))
     assert e.value.status == hstu.MTGR_ERROR_INVALID_ARGUMENT
+
+
+def test_cand_rows_flag_is_forward_only():
+    p = prob()
+    p.flags = hstu.MTGR_FWD_CAND_ROWS
+    assert hstu.mtgr_hstu_attn_workspace_size(p) > 0
+    with pytest.raises(hstu.MtgrError) as e:
+        bwd_call(p)
+    assert e.value.status == hstu.MTGR_ERROR_INVALID_ARGUMENT
+    assert "forward only" in hstu.mtgr_last_error_message()

@@ -149,7 +149,7 @@ def test_schedule_covers_every_tile_once():
         for t in range((n[b] + 63) // 64):
             s_, t_ = sg[64 * t:64 * t + 64], tsv[64 * t:64 * t + 64]
             flags = (1 if np.any(s_ <= S) else 0) | (2 if len(s_) == 64 and np.all(s_ <= S) else 0) | \
-                (4 if np.any(s_ == R) else 0) | (8 if np.any(s_ >= R) else 0)
+                (4 if np.any(s_ == R) else 0) | (8 if np.any(s_ >= R) else 0) | (16 if np.any(s_ == R + 1) else 0)
             mn = int(t_[s_ == R].min()) if np.any(s_ == R) else 2**31 - 1
             mx = int(t_[s_ >= R].max()) if np.any(s_ >= R) else -2**31
             assert tuple(summ[b, t, :3]) == (flags, mn, mx), (b, t)

@@ -147,6 +147,10 @@ def main():
                     choices=["tiny", "small", "mtgr_small", "mtgr_large", "serving"])
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--layer", action="store_true",
+                    help="time one whole encoder layer (Group-LN, projection GEMM, bias + SiLU, "
+                         "attention, gate + Group-LN, output GEMM; forward and backward) instead "
+                         "of the attention path, and print its own JSON line")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB three times (scale of the "
                          "FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -173,6 +177,8 @@ def main():
 
     layout = make_layout(args.workload)
     spec = layout.spec
+    if args.layer:
+        return bench_layer(args, layout)
     H, dh = spec.heads, spec.head_dim
     d = H * dh
     T = layout.total_tokens
@@ -307,6 +313,59 @@ def main():
         line["serving_cand_rows"] = cand_rows
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(layout, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
+def bench_layer(args, layout):
+    """One encoder layer (Sec. 4.2) forward + backward on the workload's batch: synthetic
+    bf16 input and seeded parameters; the GEMMs go to the BLAS library."""
+    import torch
+    from paper_2505_18654_amd import layer, ops
+    spec = layout.spec
+    H, dh = spec.heads, spec.head_dim
+    d, T = H * dh, layout.total_tokens
+    G = 4
+    g = torch.Generator(device="cuda")
+    g.manual_seed(11)
+    rnd = lambda *shape, scale=1.0: torch.randn(*shape, generator=g, device="cuda").mul_(scale)
+    x = rnd(T, d).bfloat16()
+    dxo = rnd(T, d).bfloat16()
+    P = layer.LayerParams(1 + rnd(G, d, scale=0.1), rnd(G, d, scale=0.1), rnd(d, 4 * d, scale=d ** -0.5).bfloat16(),
+                          rnd(4 * d, scale=0.1), 1 + rnd(G, d, scale=0.1), rnd(G, d, scale=0.1),
+                          rnd(d, d, scale=d ** -0.5).bfloat16(), rnd(d, scale=0.1))
+    jag = ops.Jagged.from_host(layout.offsets, layout.seg, layout.ts)
+    q_like = torch.empty((T, H, dh), dtype=torch.bfloat16, device="cuda")
+    ws = ops.attn_plan(q_like, jag, backward=True)
+    fwd_only = spec.fwd_only
+
+    def step():
+        out, ctx = layer.layer_fwd(x, jag, P, H, workspace=ws, planned=True)
+        if not fwd_only:
+            layer.layer_bwd(dxo, ctx, jag, P, H, workspace=ws, planned=True)
+        return out
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record()
+    for _ in range(args.steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ms = e0.elapsed_time(e1) / args.steps
+    pairs = int(visible_pairs(layout).sum())
+    f_attn = (4.0 if fwd_only else 12.0) * dh * H * pairs
+    f_gemm = (1 if fwd_only else 3) * 2.0 * T * d * 5 * d      # [d, 4d] and [d, d] products
+    line = {"metric": "MTGR encoder layer fwd+bwd tokens/s, 1 MI355X", "value": T * args.steps / elapsed,
+            "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+            "ms_per_step": ms, "higher_is_better": True, "dtype": "bf16", "data": "synthetic",
+            "config": {"workload": args.workload, "tokens": T, "heads": H, "head_dim": dh, "d": d,
+                       "pass": "fwd" if fwd_only else "fwd+bwd", "layer": True},
+            "tflops": (f_attn + f_gemm) / (ms * 1e-3) / 1e12,
+            "flop_split": {"attention": f_attn, "gemm": f_gemm}}
     print(json.dumps(line), flush=True)
 
 

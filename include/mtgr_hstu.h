@@ -220,6 +220,26 @@ mtgr_status_t mtgr_group_layernorm_bwd(const mtgr_gln_problem_t* p, const void* 
                                        float* dgamma, float* dbeta, void* workspace,
                                        size_t workspace_bytes, mtgr_stream_t stream);
 
+/* Projection activation of the encoder layer built around the attention (Sec. 4.2: the
+ * Group-LN'd input is projected to K, Q, V, U by MLPs; read here as one fused linear map
+ * followed by SiLU, as in HSTU, with the GEMM left to a BLAS library):
+ *   out[r, c] = silu(h[r, c] + bias[c])        (bias may be NULL: no bias)
+ *   h, out [rows, cols] (dtype), row strides ld_h, ld_out in elements (>= cols; out may be h
+ *   with ld_out = ld_h); bias [cols] fp32.  cols a multiple of 8 (bf16) or 4 (fp32); h, out
+ *   16-byte aligned and their rows too (ld * element size a multiple of 16). */
+mtgr_status_t mtgr_bias_silu_fwd(int64_t rows, int32_t cols, mtgr_dtype_t dtype, const void* h,
+                                 int64_t ld_h, const float* bias, void* out, int64_t ld_out,
+                                 mtgr_stream_t stream);
+
+/* Backward of mtgr_bias_silu_fwd:
+ *   dh[r, c] = dout[r, c] * silu'(z),  z = h[r, c] + bias[c],
+ *   silu'(z) = s (1 + z (1 - s)),  s = 1 / (1 + exp(-z)).
+ * Same layout rules as the forward (dh may be dout with equal strides); the bias gradient
+ * (the column sums of dh) is left to the caller. */
+mtgr_status_t mtgr_bias_silu_bwd(int64_t rows, int32_t cols, mtgr_dtype_t dtype, const void* h,
+                                 int64_t ld_h, const float* bias, const void* dout, int64_t ld_dout,
+                                 void* dh, int64_t ld_dh, mtgr_stream_t stream);
+
 /* Bytes of device scratch that mtgr_debug_validate_inputs needs. */
 #define MTGR_VALIDATE_SCRATCH_BYTES 64
 

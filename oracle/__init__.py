@@ -150,3 +150,60 @@ def gln_bwd(x, u, gid, gamma, dy, eps: float = 1e-5):
     lib().mtgr_oracle_gln_bwd(T, d, G, float(eps), _p(x), _p(u), _p(gid), _p(gamma), _p(dy),
                               _p(dx), _p(du), _p(dgamma), _p(dbeta))
     return dx, du, dgamma, dbeta
+
+
+# ------------------------------------------------------------------ encoder layer (Sec. 4.2)
+# The layer around the attention, read as (Sec. 4.2): Xt = GroupLN_in(X);
+# [Q | K | V | U] = silu(Xt W_in + b_in) (the four projection MLPs as one fused linear map
+# with SiLU, as in HSTU); Vt = Eq. 5 attention; X' = GroupLN(Vt (*) U) W_out + b_out + X
+# (Eq. 6 with the top MLP read as one linear map).  Plain fp64 composition of the functions
+# above and numpy matmuls; params: dict of gamma_in, beta_in [G, d], w_in [d, 4d], b_in [4d],
+# gamma, beta [G, d], w_out [d, d], b_out [d].
+
+def _silu(z):
+    return z / (1.0 + np.exp(-z))
+
+
+def layer_fwd(offsets, seg, ts, x, params, heads: int, rab=None, alpha: float = 1.0, eps: float = 1e-5):
+    """One encoder layer forward.  x [T, d].  Returns (x_out, cache)."""
+    x = _f64(x)
+    T, d = x.shape
+    dh = d // heads
+    P = {k: _f64(v) for k, v in params.items()}
+    xt, m0, r0 = gln_fwd(x, None, seg, P["gamma_in"], P["beta_in"], eps)
+    h = xt @ P["w_in"] + P["b_in"]
+    a = _silu(h)
+    q, k, v, u = (a[:, i * d:(i + 1) * d] for i in range(4))
+    o = attn_fwd(offsets, seg, ts, q.reshape(T, heads, dh), k.reshape(T, heads, dh),
+                 v.reshape(T, heads, dh), rab, alpha).reshape(T, d)
+    y, m1, r1 = gln_fwd(o, u, seg, P["gamma"], P["beta"], eps)
+    x_out = y @ P["w_out"] + P["b_out"] + x
+    cache = dict(x=x, xt=xt, h=h, a=a, o=o, y=y)
+    return x_out, cache
+
+
+def layer_bwd(offsets, seg, ts, dx_out, cache, params, heads: int, rab=None, alpha: float = 1.0,
+              eps: float = 1e-5):
+    """Backward of layer_fwd: returns dict of dx and every parameter gradient (drab if rab)."""
+    dx_out = _f64(dx_out)
+    P = {k: _f64(v) for k, v in params.items()}
+    x, xt, h, a, o, y = (cache[n] for n in ("x", "xt", "h", "a", "o", "y"))
+    T, d = x.shape
+    dh = d // heads
+    g = {"w_out": y.T @ dx_out, "b_out": dx_out.sum(0)}
+    dy = dx_out @ P["w_out"].T
+    u = a[:, 3 * d:]
+    do, du, g["gamma"], g["beta"] = gln_bwd(o, u, seg, P["gamma"], dy, eps)
+    q, k, v = (a[:, i * d:(i + 1) * d].reshape(T, heads, dh) for i in range(3))
+    dq, dk, dv, drab = attn_bwd(offsets, seg, ts, q, k, v, do.reshape(T, heads, dh), rab, alpha)
+    da = np.concatenate([dq.reshape(T, d), dk.reshape(T, d), dv.reshape(T, d), du], axis=1)
+    s = 1.0 / (1.0 + np.exp(-h))
+    dhh = da * s * (1.0 + h * (1.0 - s))
+    g["w_in"] = xt.T @ dhh
+    g["b_in"] = dhh.sum(0)
+    dxt = dhh @ P["w_in"].T
+    dx, _, g["gamma_in"], g["beta_in"] = gln_bwd(x, None, seg, P["gamma_in"], dxt, eps)
+    g["x"] = dx + dx_out
+    if rab is not None:
+        g["rab"] = drab
+    return g

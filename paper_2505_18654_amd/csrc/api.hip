@@ -464,6 +464,53 @@ mtgr_status_t mtgr_group_layernorm_bwd(const mtgr_gln_problem_t* p, const void* 
     return ok();
 }
 
+static mtgr_status_t check_pointwise(int64_t rows, int32_t cols, mtgr_dtype_t dtype,
+                                     const void* const* mats, const int64_t* lds, const char* const* names,
+                                     int n, const float* bias) {
+    if (dtype != MTGR_DTYPE_BF16 && dtype != MTGR_DTYPE_FP32) return fail(MTGR_ERROR_UNSUPPORTED, "dtype %d", (int)dtype);
+    const int esz = dtype == MTGR_DTYPE_BF16 ? 2 : 4, per = 16 / esz;
+    if (rows < 0 || cols <= 0) return fail(MTGR_ERROR_INVALID_ARGUMENT, "rows = %lld, cols = %d", (long long)rows, cols);
+    if (cols % per != 0) return fail(MTGR_ERROR_INVALID_ARGUMENT, "cols = %d is not a multiple of %d", cols, per);
+    if (rows > 0) {
+        for (int i = 0; i < n; i++) {
+            if (mats[i] == nullptr) return fail(MTGR_ERROR_NULL_POINTER, "%s is NULL", names[i]);
+            if (!aligned16(mats[i])) return fail(MTGR_ERROR_INVALID_ARGUMENT, "%s is not 16-byte aligned", names[i]);
+            if (lds[i] < cols || (lds[i] * esz) % 16 != 0)
+                return fail(MTGR_ERROR_INVALID_ARGUMENT, "ld of %s = %lld (needs >= cols and 16-byte rows)", names[i],
+                            (long long)lds[i]);
+        }
+        if (bias != nullptr && ((uintptr_t)bias & 3u) != 0) return fail(MTGR_ERROR_INVALID_ARGUMENT, "bias is not 4-byte aligned");
+    }
+    return MTGR_SUCCESS;
+}
+
+mtgr_status_t mtgr_bias_silu_fwd(int64_t rows, int32_t cols, mtgr_dtype_t dtype, const void* h, int64_t ld_h,
+                                 const float* bias, void* out, int64_t ld_out, mtgr_stream_t stream) {
+    const void* mats[2] = {h, out};
+    const int64_t lds[2] = {ld_h, ld_out};
+    const char* names[2] = {"h", "out"};
+    mtgr_status_t st = check_pointwise(rows, cols, dtype, mats, lds, names, 2, bias);
+    if (st != MTGR_SUCCESS) return st;
+    hipError_t e = mtgr::launch_bias_silu(rows, cols, dtype == MTGR_DTYPE_BF16, false, h, ld_h, bias, nullptr, 0,
+                                          out, ld_out, (hipStream_t)stream);
+    if (e != hipSuccess) return device_fail(e, "bias silu forward");
+    return ok();
+}
+
+mtgr_status_t mtgr_bias_silu_bwd(int64_t rows, int32_t cols, mtgr_dtype_t dtype, const void* h, int64_t ld_h,
+                                 const float* bias, const void* dout, int64_t ld_dout, void* dh, int64_t ld_dh,
+                                 mtgr_stream_t stream) {
+    const void* mats[3] = {h, dout, dh};
+    const int64_t lds[3] = {ld_h, ld_dout, ld_dh};
+    const char* names[3] = {"h", "dout", "dh"};
+    mtgr_status_t st = check_pointwise(rows, cols, dtype, mats, lds, names, 3, bias);
+    if (st != MTGR_SUCCESS) return st;
+    hipError_t e = mtgr::launch_bias_silu(rows, cols, dtype == MTGR_DTYPE_BF16, true, h, ld_h, bias, dout, ld_dout,
+                                          dh, ld_dh, (hipStream_t)stream);
+    if (e != hipSuccess) return device_fail(e, "bias silu backward");
+    return ok();
+}
+
 mtgr_status_t mtgr_debug_validate_inputs(const mtgr_hstu_problem_t* p, const int32_t* offsets,
                                          const int8_t* seg, const int8_t* group_ids,
                                          int32_t num_groups, void* scratch, size_t scratch_bytes,

@@ -98,6 +98,12 @@ constexpr int ATTN_TILE_F32 = 64;     // rows per work item, fp32 kernels
 constexpr int SCHED_BUCKETS = 4096;   // length buckets of the heavy-first sort
 constexpr int XCDS = 8;               // accelerator complex dies of an MI355X
 
+// Bias + SiLU of the encoder layer's projection: out = silu(h + bias), or with `backward`
+// out = g * silu'(h + bias).  [rows, cols] with row strides; bias [cols] fp32 or NULL.
+hipError_t launch_bias_silu(long long rows, int cols, bool bf16, bool backward, const void* h, long long ld_h,
+                            const float* bias, const void* g, long long ld_g, void* out, long long ld_out,
+                            hipStream_t s);
+
 // Debug validation of a jagged batch: `first` (VALIDATE_CONDITIONS 64-bit slots of device
 // memory) receives per condition the smallest failing index, ~0 if none.
 constexpr int VALIDATE_CONDITIONS = 6;

@@ -1,0 +1,94 @@
+// Bias + SiLU of the encoder layer's projection (forward) and its derivative (backward).
+// Memory-bound elementwise work on [rows, cols] matrices with row strides; one 16-byte chunk
+// (8 bf16 or 4 fp32) per thread and step.
+#include "mtgr_internal.h"
+#include "mtgr_device.h"
+
+namespace mtgr {
+
+namespace {
+
+template <bool BF16>
+struct Chunk;
+
+template <>
+struct Chunk<true> {
+    static constexpr int N = 8;
+    __device__ static void load(const void* base, long long idx, float* out) {
+        const uint4 u = *(const uint4*)((const uint16_t*)base + idx);
+        const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+        for (int i = 0; i < 4; i++) {
+            out[2 * i] = __uint_as_float(w[i] << 16);
+            out[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+        }
+    }
+    __device__ static void store(void* base, long long idx, const float* v) {
+        *(uint4*)((uint16_t*)base + idx) = make_uint4(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]),
+                                                      pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7]));
+    }
+};
+
+template <>
+struct Chunk<false> {
+    static constexpr int N = 4;
+    __device__ static void load(const void* base, long long idx, float* out) {
+        const float4 f = *(const float4*)((const float*)base + idx);
+        out[0] = f.x;
+        out[1] = f.y;
+        out[2] = f.z;
+        out[3] = f.w;
+    }
+    __device__ static void store(void* base, long long idx, const float* v) {
+        *(float4*)((float*)base + idx) = make_float4(v[0], v[1], v[2], v[3]);
+    }
+};
+
+// z = h + bias; forward: out = silu(z) = z sigmoid(z); backward: out = g silu'(z) with
+// silu'(z) = sigmoid(z) (1 + z (1 - sigmoid(z))).
+template <bool BF16, bool BWD>
+__global__ __launch_bounds__(256) void bias_silu_kernel(long long rows, int cols, const void* h, long long ld_h,
+                                                        const float* bias, const void* g, long long ld_g,
+                                                        void* out, long long ld_out) {
+    using C = Chunk<BF16>;
+    constexpr int N = C::N;
+    const int nch = cols / N;
+    for (long long r = blockIdx.x; r < rows; r += gridDim.x) {
+        for (int ch = threadIdx.x; ch < nch; ch += blockDim.x) {
+            const int c = ch * N;
+            float z[N];
+            C::load(h, r * ld_h + c, z);
+            if (bias != nullptr) {
+#pragma unroll
+                for (int i = 0; i < N; i++) z[i] += bias[c + i];
+            }
+            float o[N];
+            if (BWD) C::load(g, r * ld_g + c, o);
+#pragma unroll
+            for (int i = 0; i < N; i++) {
+                const float sg = __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-1.4426950408889634f * z[i]));
+                o[i] = BWD ? o[i] * sg * (1.0f + z[i] * (1.0f - sg)) : z[i] * sg;
+            }
+            C::store(out, r * ld_out + c, o);
+        }
+    }
+}
+
+}  // namespace
+
+hipError_t launch_bias_silu(long long rows, int cols, bool bf16, bool backward, const void* h, long long ld_h,
+                            const float* bias, const void* g, long long ld_g, void* out, long long ld_out,
+                            hipStream_t s) {
+    if (rows <= 0 || cols <= 0) return hipSuccess;
+    const int grid = (int)(rows < 16384 ? rows : 16384);
+    if (bf16) {
+        if (backward) bias_silu_kernel<true, true><<<grid, 256, 0, s>>>(rows, cols, h, ld_h, bias, g, ld_g, out, ld_out);
+        else bias_silu_kernel<true, false><<<grid, 256, 0, s>>>(rows, cols, h, ld_h, bias, g, ld_g, out, ld_out);
+    } else {
+        if (backward) bias_silu_kernel<false, true><<<grid, 256, 0, s>>>(rows, cols, h, ld_h, bias, g, ld_g, out, ld_out);
+        else bias_silu_kernel<false, false><<<grid, 256, 0, s>>>(rows, cols, h, ld_h, bias, g, ld_g, out, ld_out);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace mtgr

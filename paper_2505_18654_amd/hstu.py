@@ -36,6 +36,7 @@ MTGR_VALIDATE_SCRATCH_BYTES = 64
 EXPORTED = (
     "mtgr_hstu_attn_workspace_size", "mtgr_hstu_attn_plan", "mtgr_hstu_attn_fwd", "mtgr_hstu_attn_bwd",
     "mtgr_group_layernorm_workspace_size", "mtgr_group_layernorm_fwd", "mtgr_group_layernorm_bwd",
+    "mtgr_bias_silu_fwd", "mtgr_bias_silu_bwd",
     "mtgr_debug_validate_inputs", "mtgr_status_string", "mtgr_last_error_message", "mtgr_version",
 )
 
@@ -90,10 +91,14 @@ def lib() -> ctypes.CDLL:
         L.mtgr_group_layernorm_fwd.argtypes = [G, vp, vp, vp, vp, vp, vp, vp, vp, vp]
         L.mtgr_group_layernorm_bwd.argtypes = [G, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
         L.mtgr_debug_validate_inputs.argtypes = [P, vp, vp, vp, i32, vp, sz, vp]
+        i64 = ctypes.c_int64
+        L.mtgr_bias_silu_fwd.argtypes = [i64, i32, ctypes.c_int, vp, i64, vp, vp, i64, vp]
+        L.mtgr_bias_silu_bwd.argtypes = [i64, i32, ctypes.c_int, vp, i64, vp, vp, i64, vp, i64, vp]
         for name in ("mtgr_hstu_attn_workspace_size", "mtgr_hstu_attn_plan", "mtgr_hstu_attn_fwd",
                      "mtgr_hstu_attn_bwd",
                      "mtgr_group_layernorm_workspace_size", "mtgr_group_layernorm_fwd",
-                     "mtgr_group_layernorm_bwd", "mtgr_debug_validate_inputs"):
+                     "mtgr_group_layernorm_bwd", "mtgr_debug_validate_inputs", "mtgr_bias_silu_fwd",
+                     "mtgr_bias_silu_bwd"):
             getattr(L, name).restype = ctypes.c_int
         L.mtgr_status_string.argtypes = [ctypes.c_int]
         L.mtgr_status_string.restype = ctypes.c_char_p
@@ -189,6 +194,16 @@ def mtgr_group_layernorm_bwd(problem, dy, x, u, group_ids, gamma, mean, rstd, dx
                                           _ptr(group_ids), _ptr(gamma), _ptr(mean), _ptr(rstd),
                                           _ptr(dx), _ptr(du), _ptr(dgamma), _ptr(dbeta),
                                           _ptr(workspace), int(workspace_bytes), _stream(stream)))
+
+
+def mtgr_bias_silu_fwd(rows, cols, dtype, h, ld_h, bias, out, ld_out, stream=None) -> None:
+    _check(lib().mtgr_bias_silu_fwd(int(rows), int(cols), int(dtype), _ptr(h), int(ld_h), _ptr(bias), _ptr(out),
+                                    int(ld_out), _stream(stream)))
+
+
+def mtgr_bias_silu_bwd(rows, cols, dtype, h, ld_h, bias, dout, ld_dout, dh, ld_dh, stream=None) -> None:
+    _check(lib().mtgr_bias_silu_bwd(int(rows), int(cols), int(dtype), _ptr(h), int(ld_h), _ptr(bias), _ptr(dout),
+                                    int(ld_dout), _ptr(dh), int(ld_dh), _stream(stream)))
 
 
 def mtgr_debug_validate_inputs(problem, offsets, seg, group_ids, num_groups, scratch, scratch_bytes,

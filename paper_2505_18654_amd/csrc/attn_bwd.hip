@@ -8,18 +8,20 @@
 //
 // No atomics on dQ/dK/dV (results are deterministic).  Two bf16 paths:
 //   stored dS (workspace of the backward size):
-//     dkdv kernel (column-parallel): per wave 32 keys, K and V in VGPRs; the visible 64-query
-//       tiles of Q and dO stream through two LDS buffers; per 32-query half: S = Q K^T,
-//       dP = dO V^T (lane = key column), then dV += P^T dO and dK += dS^T Q with dO and Q read
-//       transposed from their row-major tiles.  It writes dS (bf16, exactly the operand of its
-//       dK product) as 64 x 64 key-major blocks and forms drab (LDS histogram, one global
-//       atomic per bucket per workgroup).
+//     dkdv kernel (column-parallel): per wave 32 keys; the workgroup's 128 keys of K sit in LDS
+//       and V in VGPRs; the visible queries stream through LDS 32 at a time (Q, dO, codes,
+//       double-buffered).  Per unit: S = Q K^T, dP = dO V^T (lane = key column), then
+//       dV += P^T dO and dK += dS^T Q with dO and Q read transposed from their row-major
+//       tiles.  It writes dS (bf16, exactly the operand of its dK product, without 1 / n_b) as
+//       64 x 64 blocks in its register-fragment order (512 contiguous bytes per store) and
+//       forms drab (per-lane runs of equal buckets into an LDS histogram, one global atomic
+//       per bucket per workgroup).
 //     dq-from-dS kernel (row-parallel): dQ^T += K^T dS^T from K tiles and the stored blocks,
 //       16 MFMAs per 32 x 64 tile and no elementwise work.
 //   recompute (smaller workspace, or a dq-only call): the dq kernel (row-parallel, like the
 //     forward) keeps Q and dO in VGPRs, streams K and V tiles, recomputes S^T = K Q^T,
 //     dP^T = V dO^T and dS^T in registers, and forms dQ^T += K^T dS^T with K^T read by
-//     ds_read_b64_tr_b16.
+//     ds_read_b64_tr_b16; the dkdv kernel is the same as above without the dS store.
 #include <type_traits>
 
 #include "attn_bwd_common.h"

@@ -159,11 +159,14 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
                 }
             }
         }
-        lds_barrier();
         t = tn;
         cls = cls_n;
         cur ^= 1;
     }
+    // One barrier per tile suffices: the copy into a buffer is issued only after the barrier
+    // that every wave passes once done with the tile that buffer held.  The tiles' LDS is
+    // reused below.
+    __syncthreads();
 
     if (want_drab) {
         run.flush(sHist, lane);

@@ -121,10 +121,13 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_ds_bf16_kernel(AttnArgs a)
                 }
             }
         }
-        lds_barrier();
         t = tn;
         cur ^= 1;
     }
+    // One barrier per tile suffices: the copy into a buffer is issued only after the barrier
+    // that every wave passes once done with the tile that buffer held.  The tiles' LDS is
+    // reused below.
+    __syncthreads();
 
     uint16_t* sO = (w < 2 ? sK0 : sK1) + (w & 1) * 32 * DH;
 #pragma unroll

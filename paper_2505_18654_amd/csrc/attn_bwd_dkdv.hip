@@ -143,56 +143,60 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
             dpacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ga, vreg[kk], dpacc, 0, 0, 0);
         }
         uint32_t pk[2][4], dsk[2][4];
-        // Elements 4 q4 .. 4 q4 + 3 belong to queries 8 q4 + 4 hh + 0..3.  Work in groups of
-        // four, each LDS access kind issued for the whole group before its results are used:
-        // one round trip per group for the timestamps and one for the bias values, instead of
-        // a chain of dependent LDS reads (and histogram atomics) per element.
+        // Element rr belongs to query 8 (rr / 4) + 4 hh + rr % 4.  The elements go through
+        // straight-line code in groups of GRP (one branch per group for the mask of a PARTIAL
+        // unit, after the group) so that the compiler interleaves their dependent exp / rcp
+        // chains; with a branch per element each chain ran on its own.  All 16 form one group
+        // without a bias; with one, groups of 4 (their timestamps and then their bias values
+        // read from LDS first) keep the live registers within budget.
+        constexpr int GRP = RAB ? 4 : 16;
 #pragma unroll
-        for (int q4 = 0; q4 < 4; q4++) {
-            const int ql0 = 8 * q4 + 4 * hh;
-            int bk[4] = {0, 0, 0, 0};
-            float rb[4] = {0.f, 0.f, 0.f, 0.f};
+        for (int g0 = 0; g0 < 16; g0 += GRP) {
+            float pv[GRP], dv[GRP];
+            int bk[GRP];
             if (RAB) {
 #pragma unroll
-                for (int e = 0; e < 4; e++) bk[e] = rab_bucket(qts[ql0 + e], kts, a.nbuckets);
-#pragma unroll
-                for (int e = 0; e < 4; e++) rb[e] = sRab[bk[e]];
+                for (int e = 0; e < GRP; e++) {
+                    const int rr = g0 + e;
+                    bk[e] = rab_bucket(qts[8 * (rr >> 2) + 4 * hh + (rr & 3)], kts, a.nbuckets);
+                }
             }
-            float pv[4], dv[4];
 #pragma unroll
-            for (int e = 0; e < 4; e++) {
-                const int rr = 4 * q4 + e;
+            for (int e = 0; e < GRP; e++) {
+                const int rr = g0 + e;
                 // p and ds are P and dS without the per-user factor 1 / n_b (and, without a
                 // relative bias, P without alpha): the factors are applied once to dK, dV, dQ
                 // and drab.  silu'(x) = sg (1 + x (1 - sg)) and alpha s (1 - sg) = alpha (s - p).
-                float p, ds;
                 if (RAB) {
-                    const float x = sacc[rr] * alpha + rb[e];
+                    const float x = sacc[rr] * alpha + sRab[bk[e]];
                     float sg;
-                    p = silu_sig(x, sg);
-                    ds = dpacc[rr] * sg * (1.0f + x * (1.0f - sg));
+                    pv[e] = silu_sig(x, sg);
+                    dv[e] = dpacc[rr] * sg * (1.0f + x * (1.0f - sg));
                 } else {
                     const float sv = sacc[rr];
                     const float sg = __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(sv * c_exp));
-                    p = sv * sg;
-                    ds = (dpacc[rr] * sg) * __builtin_fmaf(alpha, sv - p, 1.0f);
+                    pv[e] = sv * sg;
+                    dv[e] = (dpacc[rr] * sg) * __builtin_fmaf(alpha, sv - pv[e], 1.0f);
                 }
-                if (cls == TILE_PARTIAL) {
-                    const int ql = ql0 + e;
-                    const bool vis = visible(qcode[ql], qts[ql], qb + ql, kcode, kts, kj);
-                    p = vis ? p : 0.f;
-                    ds = vis ? ds : 0.f;
-                }
-                pv[e] = p;
-                dv[e] = ds;
             }
-            pk[q4 >> 1][2 * (q4 & 1)] = pack_bf16x2(pv[0], pv[1]);
-            pk[q4 >> 1][2 * (q4 & 1) + 1] = pack_bf16x2(pv[2], pv[3]);
-            dsk[q4 >> 1][2 * (q4 & 1)] = pack_bf16x2(dv[0], dv[1]);
-            dsk[q4 >> 1][2 * (q4 & 1) + 1] = pack_bf16x2(dv[2], dv[3]);
+            if (cls == TILE_PARTIAL) {
+#pragma unroll
+                for (int e = 0; e < GRP; e++) {
+                    const int rr = g0 + e, ql = 8 * (rr >> 2) + 4 * hh + (rr & 3);
+                    const bool vis = visible(qcode[ql], qts[ql], qb + ql, kcode, kts, kj);
+                    pv[e] = vis ? pv[e] : 0.f;
+                    dv[e] = vis ? dv[e] : 0.f;
+                }
+            }
+#pragma unroll
+            for (int e = 0; e < GRP; e += 2) {
+                const int r = g0 + e;
+                pk[r >> 3][(r & 7) >> 1] = pack_bf16x2(pv[e], pv[e + 1]);
+                dsk[r >> 3][(r & 7) >> 1] = pack_bf16x2(dv[e], dv[e + 1]);
+            }
             if (want_drab) {
 #pragma unroll
-                for (int e = 0; e < 4; e++) run.add(sHist, lane, bk[e], dv[e]);
+                for (int e = 0; e < GRP; e++) run.add(sHist, lane, bk[e], dv[e]);
             }
         }
         if (store_rows) {

@@ -106,47 +106,55 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
                 dpacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, doreg[kk], dpacc, 0, 0, 0);
             }
             uint32_t dsk[2][4];
-            // Elements 4 q4 .. 4 q4 + 3 belong to keys 32 blk + 8 q4 + 4 hh + 0..3; groups of
-            // four issue their LDS reads (timestamps, bias values) before using them.
+            // Element rr belongs to key 32 blk + 8 (rr / 4) + 4 hh + rr % 4.  Straight-line code
+            // per group of GRP elements (one mask branch per group, after it) so that their
+            // exp / rcp chains interleave; 16 without a bias, 4 with one (timestamps and bias
+            // values read first) to stay within the register budget.
+            constexpr int GRP = RAB ? 4 : 16;
 #pragma unroll
-            for (int q4 = 0; q4 < 4; q4++) {
-                const int kl0 = 32 * blk + 8 * q4 + 4 * hh;
-                int bk[4] = {0, 0, 0, 0};
-                float rb[4] = {0.f, 0.f, 0.f, 0.f};
+            for (int g0 = 0; g0 < 16; g0 += GRP) {
+                float dv[GRP];
+                int bk[GRP];
                 if (RAB) {
 #pragma unroll
-                    for (int e = 0; e < 4; e++) bk[e] = rab_bucket(qts, kts[kl0 + e], a.nbuckets);
-#pragma unroll
-                    for (int e = 0; e < 4; e++) rb[e] = sRab[bk[e]];
+                    for (int e = 0; e < GRP; e++) {
+                        const int rr = g0 + e;
+                        bk[e] = rab_bucket(qts, kts[32 * blk + 8 * (rr >> 2) + 4 * hh + (rr & 3)], a.nbuckets);
+                    }
                 }
-                float dv[4];
 #pragma unroll
-                for (int e = 0; e < 4; e++) {
-                    const int rr = 4 * q4 + e;
-                    const int kl = kl0 + e;
+                for (int e = 0; e < GRP; e++) {
+                    const int rr = g0 + e;
                     // ds is dS without the per-user factor 1 / n_b, applied once to dQ and drab.
-                    float ds;
                     if (RAB) {
-                        const float x = sacc[rr] * alpha + rb[e];
+                        const float x = sacc[rr] * alpha + sRab[bk[e]];
                         float sg;
                         silu_sig(x, sg);
-                        ds = dpacc[rr] * sg * (1.0f + x * (1.0f - sg));
+                        dv[e] = dpacc[rr] * sg * (1.0f + x * (1.0f - sg));
                     } else {
                         const float sv = sacc[rr];
                         const float sg = __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(sv * c_exp));
-                        ds = (dpacc[rr] * sg) * __builtin_fmaf(alpha, __builtin_fmaf(-sv, sg, sv), 1.0f);
+                        dv[e] = (dpacc[rr] * sg) * __builtin_fmaf(alpha, __builtin_fmaf(-sv, sg, sv), 1.0f);
                     }
-                    if (cls == TILE_PARTIAL)
-                        ds = visible(qcode, qts, qi, kcode[kl], kts[kl], t * BN + kl) ? ds : 0.f;
-                    else if (!qvalid)
-                        ds = 0.f;
-                    dv[e] = ds;
                 }
-                dsk[q4 >> 1][2 * (q4 & 1)] = pack_bf16x2(dv[0], dv[1]);
-                dsk[q4 >> 1][2 * (q4 & 1) + 1] = pack_bf16x2(dv[2], dv[3]);
+                if (cls == TILE_PARTIAL) {
+#pragma unroll
+                    for (int e = 0; e < GRP; e++) {
+                        const int rr = g0 + e, kl = 32 * blk + 8 * (rr >> 2) + 4 * hh + (rr & 3);
+                        dv[e] = visible(qcode, qts, qi, kcode[kl], kts[kl], t * BN + kl) ? dv[e] : 0.f;
+                    }
+                } else if (!qvalid) {
+#pragma unroll
+                    for (int e = 0; e < GRP; e++) dv[e] = 0.f;
+                }
+#pragma unroll
+                for (int e = 0; e < GRP; e += 2) {
+                    const int r = g0 + e;
+                    dsk[r >> 3][(r & 7) >> 1] = pack_bf16x2(dv[e], dv[e + 1]);
+                }
                 if (want_drab) {
 #pragma unroll
-                    for (int e = 0; e < 4; e++) run.add(sHist, lane, bk[e], dv[e]);
+                    for (int e = 0; e < GRP; e++) run.add(sHist, lane, bk[e], dv[e]);
                 }
             }
 #pragma unroll

@@ -131,16 +131,27 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
         const int* qcode = sQcode[buf];
 
         // S (32 q x 32 keys) = Q K^T and dP = dO V^T: lane = key column, registers = queries.
+        // The LDS operands of k-step kk + PF_S are read while k-step kk's MFMAs issue; the
+        // scheduling fence after each step keeps the compiler from sinking the reads next to
+        // their use (it did, to save registers, and every MFMA then waited a full LDS round trip).
         floatx16 sacc, dpacc;
         zero(sacc);
         zero(dpacc);
+        constexpr int PF_S = 1;
+        bf16x8 qa[KSTEPS], ga[KSTEPS], kb[KSTEPS];
+        auto load_s = [&](int kk) {
+            qa[kk] = tile_read8<CPR>(sQ, col, 2 * kk + hh);
+            ga[kk] = tile_read8<CPR>(sG, col, 2 * kk + hh);
+            kb[kk] = tile_read8<CPR>(sK, 32 * w + col, 2 * kk + hh);
+        };
+#pragma unroll
+        for (int kk = 0; kk < PF_S && kk < KSTEPS; kk++) load_s(kk);
 #pragma unroll
         for (int kk = 0; kk < KSTEPS; kk++) {
-            const bf16x8 qa = tile_read8<CPR>(sQ, col, 2 * kk + hh);
-            const bf16x8 ga = tile_read8<CPR>(sG, col, 2 * kk + hh);
-            const bf16x8 kb = tile_read8<CPR>(sK, 32 * w + col, 2 * kk + hh);
-            sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa, kb, sacc, 0, 0, 0);
-            dpacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ga, vreg[kk], dpacc, 0, 0, 0);
+            if (kk + PF_S < KSTEPS) load_s(kk + PF_S);
+            sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa[kk], kb[kk], sacc, 0, 0, 0);
+            dpacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ga[kk], vreg[kk], dpacc, 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
         }
         uint32_t pk[2][4], dsk[2][4];
         // Element rr belongs to query 8 (rr / 4) + 4 hh + rr % 4.  The elements go through
@@ -212,18 +223,29 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
                     sub[(2 * kq + g) * 64 + lane] = make_uint2(dsk[kq][2 * g], dsk[kq][2 * g + 1]);
         }
         // dV (32 keys x dh) += P^T dO ; dK += dS^T Q.  A = P^T / dS^T from registers,
-        // B = dO / Q read transposed (lane = feature column, slots = queries).
+        // B = dO / Q read transposed (lane = feature column, slots = queries).  Step j =
+        // (kq, d) = (j / DBLK, j % DBLK); its operands are read PF_D steps ahead, as above.
+        constexpr int NJ = 2 * DBLK, PF_D = 2;
+        bf16x8 gbs[NJ], qbs[NJ];
+        auto load_d = [&](int j) {
+            gbs[j] = tile_read_tr<CPR>(sG, 16 * (j / DBLK), 32 * (j % DBLK), lane);
+            qbs[j] = tile_read_tr<CPR>(sQ, 16 * (j / DBLK), 32 * (j % DBLK), lane);
+        };
+        bf16x8 pa[2], da[2];
 #pragma unroll
         for (int kq = 0; kq < 2; kq++) {
-            const bf16x8 pa = as_bf16x8(make_uint4(pk[kq][0], pk[kq][1], pk[kq][2], pk[kq][3]));
-            const bf16x8 da = as_bf16x8(make_uint4(dsk[kq][0], dsk[kq][1], dsk[kq][2], dsk[kq][3]));
+            pa[kq] = as_bf16x8(make_uint4(pk[kq][0], pk[kq][1], pk[kq][2], pk[kq][3]));
+            da[kq] = as_bf16x8(make_uint4(dsk[kq][0], dsk[kq][1], dsk[kq][2], dsk[kq][3]));
+        }
 #pragma unroll
-            for (int d = 0; d < DBLK; d++) {
-                const bf16x8 gb = tile_read_tr<CPR>(sG, 16 * kq, 32 * d, lane);
-                const bf16x8 qbv = tile_read_tr<CPR>(sQ, 16 * kq, 32 * d, lane);
-                dvacc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pa, gb, dvacc[d], 0, 0, 0);
-                dkacc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(da, qbv, dkacc[d], 0, 0, 0);
-            }
+        for (int j = 0; j < PF_D && j < NJ; j++) load_d(j);
+#pragma unroll
+        for (int j = 0; j < NJ; j++) {
+            if (j + PF_D < NJ) load_d(j + PF_D);
+            const int kq = j / DBLK, d = j % DBLK;
+            dvacc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pa[kq], gbs[j], dvacc[d], 0, 0, 0);
+            dkacc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(da[kq], qbs[j], dkacc[d], 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
         }
         t = tn;
         half = hn;

@@ -94,7 +94,8 @@ typedef void* mtgr_stream_t;            /* hipStream_t */
  *   ld_*: token strides in ELEMENTS (>= H*dh, <= MTGR_MAX_LD); q, k, v may be views into one fused
  *     projection output.  Gradients share the layout of their primal:
  *     dq uses ld_q, dk ld_k, dv ld_v, and dout uses ld_o.
- *   flags: see MTGR_ATTN_PLANNED and MTGR_BWD_SKIP_*.
+ *   flags: MTGR_ATTN_PLANNED, MTGR_BWD_SKIP_DQ / _DKDV, MTGR_BWD_KEEP_DS / _DS_READY,
+ *     MTGR_FWD_CAND_ROWS (see their definitions above).
  * Alignment: every tensor pointer 16-byte aligned; every ld a multiple of 16 bytes. */
 typedef struct {
     int32_t num_users;
@@ -105,7 +106,7 @@ typedef struct {
     int32_t dtype;                      /* mtgr_dtype_t */
     float alpha;
     int32_t num_rab_buckets;
-    uint32_t flags;                     /* MTGR_ATTN_PLANNED | MTGR_BWD_SKIP_* (0 = none) */
+    uint32_t flags;                     /* MTGR_ATTN_PLANNED, MTGR_BWD_*, MTGR_FWD_* bits (0 = none) */
     int64_t ld_q, ld_k, ld_v, ld_o;
 } mtgr_hstu_problem_t;
 

@@ -121,29 +121,47 @@ __global__ __launch_bounds__(1024) void build_schedule_kernel(const int* __restr
     __threadfence_block();
     __syncthreads();
     // Group g = rank * heads + h goes to XCD g % 8 at queue position
-    // sum of tile counts of the earlier groups with the same residue.
+    // sum of tile counts of the earlier groups with the same residue.  One pass over 1024
+    // groups at a time: a scan with stride 8 inside each wave, then per residue over the
+    // 16 waves, with a running carry per residue.
+    __shared__ int wsum[16][XCDS];
+    __shared__ int carry[XCDS];
+    if (tid < XCDS) carry[tid] = 0;
+    const int lane = tid & 63, wv = tid >> 6, x = tid % XCDS;
     const long long groups = (long long)num_users * heads;
-    for (int x = 0; x < XCDS; x++) {
-        const long long count = groups > x ? (groups - x + XCDS - 1) / XCDS : 0;
-        int carry = 0;
-        for (long long base = 0; base < count; base += 1024) {
-            const long long kk = base + tid;
-            int nq = 0, b = -1, h = 0;
-            if (kk < count) {
-                const long long g = kk * XCDS + x;
-                b = sorted_users[g / heads];
-                h = (int)(g % heads);
-                const int n = offsets[b + 1] - offsets[b];
-                nq = (n + bm - 1) / bm;
-            }
-            int total;
-            const int pos = carry + block_exclusive_scan(nq, scratch, &total);
-            for (int t = 0; t < nq; t++) {
-                const long long slot = (long long)(pos + t) * XCDS + x;
-                if (slot < slots) items[slot] = make_int2(b, (t << 8) | h);
-            }
-            carry += total;
+    for (long long base = 0; base < groups; base += 1024) {
+        const long long g = base + tid;
+        int nq = 0, b = -1, h = 0;
+        if (g < groups) {
+            b = sorted_users[g / heads];
+            h = (int)(g % heads);
+            const int n = offsets[b + 1] - offsets[b];
+            nq = (n + bm - 1) / bm;
         }
+        int incl = nq;
+#pragma unroll
+        for (int off = XCDS; off < 64; off <<= 1) {
+            const int o = __shfl_up(incl, off, 64);
+            if (lane >= off) incl += o;
+        }
+        if (lane >= 64 - XCDS) wsum[wv][x] = incl;   // this wave's total of residue x
+        __syncthreads();
+        if (tid < XCDS) {
+            int run = carry[tid];
+            for (int i = 0; i < 16; i++) {
+                const int t = wsum[i][tid];
+                wsum[i][tid] = run;
+                run += t;
+            }
+            carry[tid] = run;
+        }
+        __syncthreads();
+        const int pos = wsum[wv][x] + incl - nq;
+        for (int t = 0; t < nq; t++) {
+            const long long slot = (long long)(pos + t) * XCDS + x;
+            if (slot < slots) items[slot] = make_int2(b, (t << 8) | h);
+        }
+        __syncthreads();   // wsum is rewritten by the next pass
     }
 }
 

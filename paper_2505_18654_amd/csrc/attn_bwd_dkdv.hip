@@ -154,60 +154,126 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
             __builtin_amdgcn_sched_barrier(0);
         }
         uint32_t pk[2][4], dsk[2][4];
-        // Element rr belongs to query 8 (rr / 4) + 4 hh + rr % 4.  The elements go through
-        // straight-line code in groups of GRP (one branch per group for the mask of a PARTIAL
-        // unit, after the group) so that the compiler interleaves their dependent exp / rcp
-        // chains; with a branch per element each chain ran on its own.  All 16 form one group
-        // without a bias; with one, groups of 4 (their timestamps and then their bias values
-        // read from LDS first) keep the live registers within budget.
-        constexpr int GRP = RAB ? 4 : 16;
+        // dV (32 keys x dh) += P^T dO ; dK += dS^T Q.  A = P^T / dS^T from registers,
+        // B = dO / Q read transposed (lane = feature column, slots = queries).  Step j =
+        // (kq, d) = (j / DBLK, j % DBLK); its operands are read PF_D steps ahead, as above.
+        constexpr int NJ = 2 * DBLK, PF_D = 2;
+        bf16x8 gbs[NJ], qbs[NJ];
+        auto load_d = [&](int j) {
+            gbs[j] = tile_read_tr<CPR>(sG, 16 * (j / DBLK), 32 * (j % DBLK), lane);
+            qbs[j] = tile_read_tr<CPR>(sQ, 16 * (j / DBLK), 32 * (j % DBLK), lane);
+        };
+        bf16x8 pa[2], da[2];
+        auto operands = [&](int kq) {
+            pa[kq] = as_bf16x8(make_uint4(pk[kq][0], pk[kq][1], pk[kq][2], pk[kq][3]));
+            da[kq] = as_bf16x8(make_uint4(dsk[kq][0], dsk[kq][1], dsk[kq][2], dsk[kq][3]));
+        };
+        auto product = [&](int j) {
+            const int kq = j / DBLK, d = j % DBLK;
+            dvacc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pa[kq], gbs[j], dvacc[d], 0, 0, 0);
+            dkacc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(da[kq], qbs[j], dkacc[d], 0, 0, 0);
+        };
+        // Element rr belongs to query 8 (rr / 4) + 4 hh + rr % 4.  p and ds are P and dS
+        // without the per-user factor 1 / n_b (and, without a relative bias, P without alpha):
+        // the factors are applied once to dK, dV, dQ and drab.  silu'(x) = sg (1 + x (1 - sg))
+        // and alpha s (1 - sg) = alpha (s - p).
+        auto mask = [&](int rr, float& p, float& ds) {
+            const int ql = 8 * (rr >> 2) + 4 * hh + (rr & 3);
+            const bool vis = visible(qcode[ql], qts[ql], qb + ql, kcode, kts, kj);
+            p = vis ? p : 0.f;
+            ds = vis ? ds : 0.f;
+        };
+        if constexpr (!RAB) {
+            // Elements 0..7 (queries 0..15) first; then elements 8..15 interleave with the
+            // dV / dK products of queries 0..15, so that one wave overlaps its own VALU and
+            // MFMA work; then the products of queries 16..31.  The mask of a PARTIAL unit is
+            // one branch per half, after its straight-line element math.
+            // s (1 - sg) is one explicit fma, so that every instantiation (with and without
+            // the dS store) rounds alike and their dK / dV agree bit for bit.
+            auto element = [&](int rr, float& p, float& ds) {
+                const float sv = sacc[rr];
+                const float sg = __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(sv * c_exp));
+                p = sv * sg;
+                ds = (dpacc[rr] * sg) * __builtin_fmaf(alpha, __builtin_fmaf(-sv, sg, sv), 1.0f);
+            };
+            float pv[16], dv[16];
 #pragma unroll
-        for (int g0 = 0; g0 < 16; g0 += GRP) {
-            float pv[GRP], dv[GRP];
-            int bk[GRP];
-            if (RAB) {
+            for (int rr = 0; rr < 8; rr++) element(rr, pv[rr], dv[rr]);
+            if (cls == TILE_PARTIAL) {
 #pragma unroll
-                for (int e = 0; e < GRP; e++) {
-                    const int rr = g0 + e;
-                    bk[e] = rab_bucket(qts[8 * (rr >> 2) + 4 * hh + (rr & 3)], kts, a.nbuckets);
-                }
+                for (int rr = 0; rr < 8; rr++) mask(rr, pv[rr], dv[rr]);
             }
 #pragma unroll
-            for (int e = 0; e < GRP; e++) {
-                const int rr = g0 + e;
-                // p and ds are P and dS without the per-user factor 1 / n_b (and, without a
-                // relative bias, P without alpha): the factors are applied once to dK, dV, dQ
-                // and drab.  silu'(x) = sg (1 + x (1 - sg)) and alpha s (1 - sg) = alpha (s - p).
-                if (RAB) {
-                    const float x = sacc[rr] * alpha + sRab[bk[e]];
-                    float sg;
-                    pv[e] = silu_sig(x, sg);
-                    dv[e] = dpacc[rr] * sg * (1.0f + x * (1.0f - sg));
-                } else {
-                    const float sv = sacc[rr];
-                    const float sg = __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(sv * c_exp));
-                    pv[e] = sv * sg;
-                    dv[e] = (dpacc[rr] * sg) * __builtin_fmaf(alpha, sv - pv[e], 1.0f);
-                }
+            for (int r = 0; r < 8; r += 2) {
+                pk[0][r >> 1] = pack_bf16x2(pv[r], pv[r + 1]);
+                dsk[0][r >> 1] = pack_bf16x2(dv[r], dv[r + 1]);
+            }
+            operands(0);
+            // Operands one step ahead here (two spilled); 8 / DBLK elements per step.
+            constexpr int EPS = 8 / DBLK;
+            load_d(0);
+#pragma unroll
+            for (int j = 0; j < DBLK; j++) {
+                load_d(j + 1);
+                product(j);
+#pragma unroll
+                for (int e = 8 + EPS * j; e < 8 + EPS * (j + 1); e++) element(e, pv[e], dv[e]);
+                // Pin the products here: their results are read only by later products, and
+                // the compiler otherwise sinks them all behind the element math.
+                asm volatile("" : "+v"(dvacc[j]), "+v"(dkacc[j]));
+                __builtin_amdgcn_sched_barrier(0);
             }
             if (cls == TILE_PARTIAL) {
 #pragma unroll
-                for (int e = 0; e < GRP; e++) {
-                    const int rr = g0 + e, ql = 8 * (rr >> 2) + 4 * hh + (rr & 3);
-                    const bool vis = visible(qcode[ql], qts[ql], qb + ql, kcode, kts, kj);
-                    pv[e] = vis ? pv[e] : 0.f;
-                    dv[e] = vis ? dv[e] : 0.f;
+                for (int rr = 8; rr < 16; rr++) mask(rr, pv[rr], dv[rr]);
+            }
+#pragma unroll
+            for (int r = 8; r < 16; r += 2) {
+                pk[1][(r - 8) >> 1] = pack_bf16x2(pv[r], pv[r + 1]);
+                dsk[1][(r - 8) >> 1] = pack_bf16x2(dv[r], dv[r + 1]);
+            }
+        } else {
+            // With a relative bias: groups of 4 elements (their timestamps and then their bias
+            // values read from LDS first) keep the live registers within budget.
+#pragma unroll
+            for (int g0 = 0; g0 < 16; g0 += 4) {
+                float pv[4], dv[4];
+                int bk[4];
+#pragma unroll
+                for (int e = 0; e < 4; e++) {
+                    const int rr = g0 + e;
+                    bk[e] = rab_bucket(qts[8 * (rr >> 2) + 4 * hh + (rr & 3)], kts, a.nbuckets);
+                }
+#pragma unroll
+                for (int e = 0; e < 4; e++) {
+                    const float x = sacc[g0 + e] * alpha + sRab[bk[e]];
+                    float sg;
+                    pv[e] = silu_sig(x, sg);
+                    dv[e] = dpacc[g0 + e] * sg * (1.0f + x * (1.0f - sg));
+                }
+                if (cls == TILE_PARTIAL) {
+#pragma unroll
+                    for (int e = 0; e < 4; e++) mask(g0 + e, pv[e], dv[e]);
+                }
+#pragma unroll
+                for (int e = 0; e < 4; e += 2) {
+                    const int r = g0 + e;
+                    pk[r >> 3][(r & 7) >> 1] = pack_bf16x2(pv[e], pv[e + 1]);
+                    dsk[r >> 3][(r & 7) >> 1] = pack_bf16x2(dv[e], dv[e + 1]);
+                }
+                if (want_drab) {
+#pragma unroll
+                    for (int e = 0; e < 4; e++) run.add(sHist, lane, bk[e], dv[e]);
                 }
             }
+            operands(0);
 #pragma unroll
-            for (int e = 0; e < GRP; e += 2) {
-                const int r = g0 + e;
-                pk[r >> 3][(r & 7) >> 1] = pack_bf16x2(pv[e], pv[e + 1]);
-                dsk[r >> 3][(r & 7) >> 1] = pack_bf16x2(dv[e], dv[e + 1]);
-            }
-            if (want_drab) {
+            for (int j = 0; j < PF_D && j < NJ; j++) load_d(j);
 #pragma unroll
-                for (int e = 0; e < GRP; e++) run.add(sHist, lane, bk[e], dv[e]);
+            for (int j = 0; j < DBLK; j++) {
+                if (j + PF_D < NJ) load_d(j + PF_D);
+                product(j);
+                __builtin_amdgcn_sched_barrier(0);
             }
         }
         if (store_rows) {
@@ -222,29 +288,14 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
                 for (int g = 0; g < 2; g++)
                     sub[(2 * kq + g) * 64 + lane] = make_uint2(dsk[kq][2 * g], dsk[kq][2 * g + 1]);
         }
-        // dV (32 keys x dh) += P^T dO ; dK += dS^T Q.  A = P^T / dS^T from registers,
-        // B = dO / Q read transposed (lane = feature column, slots = queries).  Step j =
-        // (kq, d) = (j / DBLK, j % DBLK); its operands are read PF_D steps ahead, as above.
-        constexpr int NJ = 2 * DBLK, PF_D = 2;
-        bf16x8 gbs[NJ], qbs[NJ];
-        auto load_d = [&](int j) {
-            gbs[j] = tile_read_tr<CPR>(sG, 16 * (j / DBLK), 32 * (j % DBLK), lane);
-            qbs[j] = tile_read_tr<CPR>(sQ, 16 * (j / DBLK), 32 * (j % DBLK), lane);
-        };
-        bf16x8 pa[2], da[2];
+        // Operands 0 .. DBLK (one step ahead, without a bias) or up to DBLK + 1 (two steps
+        // ahead) have been read.
+        operands(1);
+        if constexpr (!RAB && DBLK + 1 < NJ) load_d(DBLK + 1);
 #pragma unroll
-        for (int kq = 0; kq < 2; kq++) {
-            pa[kq] = as_bf16x8(make_uint4(pk[kq][0], pk[kq][1], pk[kq][2], pk[kq][3]));
-            da[kq] = as_bf16x8(make_uint4(dsk[kq][0], dsk[kq][1], dsk[kq][2], dsk[kq][3]));
-        }
-#pragma unroll
-        for (int j = 0; j < PF_D && j < NJ; j++) load_d(j);
-#pragma unroll
-        for (int j = 0; j < NJ; j++) {
+        for (int j = DBLK; j < NJ; j++) {
             if (j + PF_D < NJ) load_d(j + PF_D);
-            const int kq = j / DBLK, d = j % DBLK;
-            dvacc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pa[kq], gbs[j], dvacc[d], 0, 0, 0);
-            dkacc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(da[kq], qbs[j], dkacc[d], 0, 0, 0);
+            product(j);
             __builtin_amdgcn_sched_barrier(0);
         }
         t = tn;

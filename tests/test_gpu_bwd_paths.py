@@ -122,3 +122,41 @@ def test_stored_path_flag_errors():
     with pytest.raises(hstu.MtgrError) as e:
         ops.attn_bwd(q, k, v, do, jag, workspace=ws_fwd, parts="dq_from_ds")
     assert e.value.status == hstu.MTGR_ERROR_WORKSPACE_TOO_SMALL
+
+
+@pytest.mark.parametrize("alpha", [0.0883883, -0.7, 3.0, 1e-25, 0.0])
+def test_alpha_values(alpha):
+    """Score scales of either sign, a tiny one and zero (every other test uses alpha = 1):
+    both backward forms against the oracle on users with every mask case."""
+    U, S, R, C = SEG_USER, SEG_HIST, SEG_RT, SEG_CAND
+    rng = np.random.default_rng(23)
+    segs, tss = [], []
+    for n_s, n_r, n_c in ((150, 40, 20), (60, 3, 2), (200, 70, 45)):
+        segs.append([U] * 4 + [S] * n_s + [R] * n_r + [C] * n_c)
+        tss.append([0] * 4 + sorted(rng.integers(-10**6, 0, n_s).tolist()) +
+                   sorted(rng.choice(86400, n_r, replace=False).tolist()) + rng.integers(0, 86400, n_c).tolist())
+    L = custom_layout(segs, tss, heads=2, head_dim=128, dtype="bf16", rab_buckets=0)
+    inp = make_inputs(L, all_exact=True)
+    jag = jagged(inp)
+    q, k, v, do = inp["q"], inp["k"], inp["v"], inp["do"]
+    say(f"[bwd paths] alpha={alpha}")
+    p = ops.attn_problem(jag, q, k, v, do, None, alpha)
+    outs = {"stored": ops.attn_bwd(q, k, v, do, jag, alpha=alpha,
+                                   workspace=ops.workspace_for(p, q.device, backward=True)),
+            "recompute": ops.attn_bwd(q, k, v, do, jag, alpha=alpha,
+                                      workspace=ops.workspace_for(p, q.device, backward=False))}
+    torch.cuda.synchronize()
+    vals = make_values(L)
+    ref = oracle.attn_bwd(L.offsets, L.seg, L.ts, vals["q"], vals["k"], vals["v"], to_np(do), None,
+                          alpha=alpha)
+    users = list(range(L.num_users))
+    errs = {}
+    for name, (dq, dk, dv, _) in outs.items():
+        for t, x, r in (("dq", dq, ref[0]), ("dk", dk, ref[1]), ("dv", dv, ref[2])):
+            g = to_np(x)
+            if alpha == 0.0:
+                assert np.all(g == 0), (name, t)
+                continue
+            errs[(name, t)] = per_user_err(L, users, g, r, STORAGE_ULP["bf16"])
+    say(f"[bwd paths] alpha={alpha} " + " ".join(f"{n}.{t}={e:.2e}" for (n, t), e in errs.items()))
+    assert all(e <= TOL["bf16"] for e in errs.values()), errs

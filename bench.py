@@ -151,6 +151,10 @@ def main():
                     help="time one whole encoder layer (Group-LN, projection GEMM, bias + SiLU, "
                          "attention, gate + Group-LN, output GEMM; forward and backward) instead "
                          "of the attention path, and print its own JSON line")
+    ap.add_argument("--embedding", action="store_true",
+                    help="time the dynamic embedding table instead (de-duplication, lookup with "
+                         "insertion, gather and sparse SGD of the workload's sparse IDs) and print "
+                         "its own JSON line")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB three times (scale of the "
                          "FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -179,6 +183,8 @@ def main():
     spec = layout.spec
     if args.layer:
         return bench_layer(args, layout)
+    if args.embedding:
+        return bench_embedding(args, layout)
     H, dh = spec.heads, spec.head_dim
     d = H * dh
     T = layout.total_tokens
@@ -366,6 +372,70 @@ def bench_layer(args, layout):
                        "pass": "fwd" if fwd_only else "fwd+bwd", "layer": True},
             "tflops": (f_attn + f_gemm) / (ms * 1e-3) / 1e12,
             "flop_split": {"attention": f_attn, "gemm": f_gemm}}
+    print(json.dumps(line), flush=True)
+
+
+def bench_embedding(args, layout):
+    """Sparse-ID side of a training step on the workload's batch: every token carries
+    EMB_FEATURES sparse IDs drawn Zipf(1.05) over 10^8 IDs (seeded, synthetic); a step is
+    dedup + lookup with insertion + gather + SGD of those IDs on a bf16 table of dim 64."""
+    import torch
+    from paper_2505_18654_amd.embedding import DynamicEmbedding
+    EMB_FEATURES, DIM, ROWS = 8, 64, 1 << 24
+    T = layout.total_tokens
+    n = T * EMB_FEATURES
+    rng = np.random.default_rng(17)
+    batches = []
+    for i in range(4):   # distinct batches, cycled
+        base = rng.zipf(1.05, n) % 100_000_000
+        ids = (base.astype(np.uint64) * np.uint64(0x9E3779B97F4A7C15)).view(np.int64)
+        batches.append(torch.from_numpy(ids).cuda())
+    table = DynamicEmbedding(ROWS, DIM, dtype=torch.bfloat16)
+    grad = torch.randn(n, DIM, device="cuda").bfloat16()
+    now = [0]
+
+    def step(i):
+        now[0] += 1
+        out, b = table.lookup(batches[i % len(batches)], now=now[0])
+        table.sgd(b, grad, 1e-3)
+        return b
+
+    for i in range(max(args.warmup, len(batches))):
+        b = step(i)
+    torch.cuda.synchronize()
+    nu = int(b.num_unique.item())
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record()
+    for i in range(args.steps):
+        step(i)
+    e1.record()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ms = e0.elapsed_time(e1) / args.steps
+    st = table.stats()
+    # gather alone, for its HBM roofline: reads and writes n rows of DIM bf16
+    _, b = table.lookup(batches[0], now=now[0] + 1, gather=False)
+    out = torch.empty(n, DIM, dtype=torch.bfloat16, device="cuda")
+    torch.cuda.synchronize()
+    g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    g0.record()
+    for _ in range(10):
+        table.gather(b, out)
+    g1.record()
+    torch.cuda.synchronize()
+    g_ms = g0.elapsed_time(g1) / 10
+    g_bytes = n * DIM * 2 * 2 + n * 8
+    line = {"metric": "dynamic embedding table step (dedup + lookup/insert + gather + SGD) IDs/s, 1 MI355X",
+            "value": n * args.steps / elapsed, "unit": "ids/s", "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "dtype": "bf16",
+            "data": "synthetic",
+            "config": {"workload": args.workload, "ids_per_step": n, "unique_per_step": nu,
+                       "features_per_token": EMB_FEATURES, "dim": DIM, "row_capacity": ROWS,
+                       "key_capacity": table.key_capacity, "live_keys": st["num_keys"], "embedding": True},
+            "roofline": {"bound": "hbm", "kernel": "gather_kernel", "achieved": g_bytes / (g_ms * 1e-3) / 1e9,
+                         "peak": 8000.0, "unit": "GB/s",
+                         "frac": g_bytes / (g_ms * 1e-3) / 1e9 / 8000.0, "traffic": None}}
     print(json.dumps(line), flush=True)
 
 

@@ -23,7 +23,7 @@
  *     which concurrent threads won their atomic operations: they are valid but not
  *     reproducible.  What is reproducible: the set of unique IDs, ids[n] ==
  *     unique[inverse[n]], the ID -> embedding mapping and every gathered value; the sgd
- *     update is a float atomic sum (order varies in the last bits).
+ *     update sums each ID's gradients in an order that varies (last bits only).
  */
 #ifndef MTGR_EMBEDDING_H
 #define MTGR_EMBEDDING_H
@@ -114,17 +114,20 @@ mtgr_status_t mtgr_embedding_gather(const mtgr_embedding_table_t* t, int64_t n,
                                     const int32_t* inverse, const int32_t* rows, void* out,
                                     int64_t ld_out, mtgr_stream_t stream);
 
-/* Workspace bytes of mtgr_embedding_sgd: an fp32 [n_max, dim] gradient accumulator. */
-mtgr_status_t mtgr_embedding_sgd_workspace_size(int64_t n_max, int32_t dim, size_t* bytes);
+/* Workspace bytes of mtgr_embedding_sgd for n IDs and up to n_max unique IDs. */
+mtgr_status_t mtgr_embedding_sgd_workspace_size(int64_t n, int64_t n_max, int32_t dim, size_t* bytes);
 
 /* Sparse SGD step of the embedding rows of a batch:
  *   g[u, :] = sum over i with inverse[i] == u of grad_out[i, :]          (fp32)
  *   values[rows[u], :] -= lr * g[u, :]      for u < *num_unique with rows[u] >= 0
- * grad_out [n, dim] of the table's dtype, row stride ld_grad; rows and num_unique as
- * produced by mtgr_embedding_lookup for the same batch. */
+ * grad_out [n, dim] of the table's dtype, row stride ld_grad; inverse, occurrences and
+ * num_unique as produced by mtgr_embedding_dedup and rows by mtgr_embedding_lookup for the same
+ * batch.  The positions are grouped by ID first (a counting sort driven by occurrences), so
+ * each ID's gradient rows are summed in registers; only groups that straddle a 64-position
+ * chunk are combined with float atomics (their order, and the last bits, vary). */
 mtgr_status_t mtgr_embedding_sgd(const mtgr_embedding_table_t* t, int64_t n, const int32_t* inverse,
-                                 const void* grad_out, int64_t ld_grad, int64_t n_max,
-                                 const int32_t* rows, const int64_t* num_unique, float lr,
+                                 const int32_t* occurrences, const void* grad_out, int64_t ld_grad,
+                                 int64_t n_max, const int32_t* rows, const int64_t* num_unique, float lr,
                                  void* workspace, size_t workspace_bytes, mtgr_stream_t stream);
 
 /* Eviction by time: every live key whose row has last_ts < threshold is deleted (its slot

@@ -1,10 +1,12 @@
 // C ABI of the library: argument validation (pure host code, before any HIP call),
-// workspace layout and kernel launches.  See include/mtgr_hstu.h for the contract.
+// workspace layout and kernel launches.  See include/mtgr_hstu.h and include/mtgr_embedding.h
+// for the contract.
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <string>
 
+#include "../../include/mtgr_embedding.h"
 #include "../../include/mtgr_hstu.h"
 #include "mtgr_internal.h"
 
@@ -566,5 +568,225 @@ const char* mtgr_status_string(mtgr_status_t status) {
 const char* mtgr_last_error_message(void) { return g_last_error.c_str(); }
 
 int32_t mtgr_version(void) { return MTGR_HSTU_VERSION; }
+
+
+}  // extern "C"
+
+// ------------------------------------------------------------------------ embedding table
+namespace {
+
+constexpr long long EMB_MAX_BATCH = 1ll << 30;   // IDs per dedup call (int32 positions)
+
+mtgr_status_t check_table(const mtgr_embedding_table_t* t, mtgr::EmbArgs* a) {
+    if (!t) return fail(MTGR_ERROR_NULL_POINTER, "table is NULL");
+    if (t->dtype != MTGR_DTYPE_BF16 && t->dtype != MTGR_DTYPE_FP32)
+        return fail(MTGR_ERROR_UNSUPPORTED, "dtype %d is not supported", t->dtype);
+    if (t->key_capacity < 2 || t->key_capacity > (1ll << 40) || (t->key_capacity & (t->key_capacity - 1)))
+        return fail(MTGR_ERROR_INVALID_ARGUMENT, "key_capacity %lld is not a power of two in 2 .. 2^40",
+                    (long long)t->key_capacity);
+    if (t->row_capacity < 1 || t->row_capacity > 0x7fffffffll)
+        return fail(MTGR_ERROR_INVALID_ARGUMENT, "row_capacity %lld outside 1 .. 2^31 - 1",
+                    (long long)t->row_capacity);
+    if (t->key_capacity < t->row_capacity + 1)
+        return fail(MTGR_ERROR_INVALID_ARGUMENT, "key_capacity %lld below row_capacity + 1",
+                    (long long)t->key_capacity);
+    if (t->dim < 8 || t->dim > 4096 || t->dim % 8)
+        return fail(MTGR_ERROR_INVALID_ARGUMENT, "dim %d is not a multiple of 8 in 8 .. 4096", t->dim);
+    REQUIRE_PTR(t->keys, "keys");
+    REQUIRE_PTR(t->key_rows, "key_rows");
+    REQUIRE_PTR(t->values, "values");
+    REQUIRE_PTR(t->counts, "counts");
+    REQUIRE_PTR(t->last_ts, "last_ts");
+    REQUIRE_PTR(t->free_rows, "free_rows");
+    REQUIRE_PTR(t->state, "state");
+    a->key_capacity = t->key_capacity;
+    a->row_capacity = (int)t->row_capacity;
+    a->dim = t->dim;
+    a->esize = t->dtype == MTGR_DTYPE_BF16 ? 2 : 4;
+    a->keys = t->keys;
+    a->key_rows = t->key_rows;
+    a->values = t->values;
+    a->counts = t->counts;
+    a->last_ts = t->last_ts;
+    a->free_rows = t->free_rows;
+    a->state = t->state;
+    return MTGR_SUCCESS;
+}
+
+mtgr_status_t check_count(long long n, long long max, const char* name) {
+    if (n < 0 || n > max) return fail(MTGR_ERROR_INVALID_ARGUMENT, "%s %lld outside 0 .. %lld", name, n, max);
+    return MTGR_SUCCESS;
+}
+
+}  // namespace
+
+extern "C" {
+
+mtgr_status_t mtgr_embedding_init(const mtgr_embedding_table_t* t, mtgr_stream_t stream) {
+    mtgr::EmbArgs a;
+    mtgr_status_t st = check_table(t, &a);
+    if (st != MTGR_SUCCESS) return st;
+    hipError_t e = mtgr::launch_emb_init(a, (hipStream_t)stream);
+    if (e != hipSuccess) return device_fail(e, "embedding init");
+    return ok();
+}
+
+mtgr_status_t mtgr_embedding_dedup_workspace_size(int64_t n, size_t* bytes) {
+    if (!bytes) return fail(MTGR_ERROR_NULL_POINTER, "bytes is NULL");
+    mtgr_status_t st = check_count(n, EMB_MAX_BATCH, "n");
+    if (st != MTGR_SUCCESS) return st;
+    *bytes = mtgr::dedup_workspace_bytes(n);
+    return ok();
+}
+
+mtgr_status_t mtgr_embedding_dedup(int64_t n, const uint64_t* ids, uint64_t* unique, int32_t* occurrences,
+                                   int32_t* inverse, int64_t* num_unique, void* workspace,
+                                   size_t workspace_bytes, mtgr_stream_t stream) {
+    mtgr_status_t st = check_count(n, EMB_MAX_BATCH, "n");
+    if (st != MTGR_SUCCESS) return st;
+    REQUIRE_PTR(num_unique, "num_unique");
+    REQUIRE_PTR(workspace, "workspace");
+    if (n > 0) {
+        REQUIRE_PTR(ids, "ids");
+        REQUIRE_PTR(unique, "unique");
+        REQUIRE_PTR(inverse, "inverse");
+        if (occurrences && !aligned16(occurrences))
+            return fail(MTGR_ERROR_INVALID_ARGUMENT, "occurrences is not 16-byte aligned");
+    }
+    const size_t need = mtgr::dedup_workspace_bytes(n);
+    if (workspace_bytes < need)
+        return fail(MTGR_ERROR_WORKSPACE_TOO_SMALL, "workspace %zu bytes, need %zu", workspace_bytes, need);
+    hipError_t e = mtgr::launch_emb_dedup(n, ids, unique, occurrences, inverse, (long long*)num_unique, workspace,
+                                          (hipStream_t)stream);
+    if (e != hipSuccess) return device_fail(e, "embedding dedup");
+    return ok();
+}
+
+mtgr_status_t mtgr_embedding_lookup_workspace_size(int64_t n_max, size_t* bytes) {
+    if (!bytes) return fail(MTGR_ERROR_NULL_POINTER, "bytes is NULL");
+    mtgr_status_t st = check_count(n_max, EMB_MAX_BATCH, "n_max");
+    if (st != MTGR_SUCCESS) return st;
+    *bytes = mtgr::lookup_workspace_bytes(n_max);
+    return ok();
+}
+
+mtgr_status_t mtgr_embedding_lookup(const mtgr_embedding_table_t* t, int64_t n_max, const uint64_t* unique,
+                                    const int32_t* occurrences, const int64_t* num_unique, int32_t now,
+                                    int32_t insert, int32_t* rows, void* workspace, size_t workspace_bytes,
+                                    mtgr_stream_t stream) {
+    mtgr::EmbArgs a;
+    mtgr_status_t st = check_table(t, &a);
+    if (st != MTGR_SUCCESS) return st;
+    st = check_count(n_max, EMB_MAX_BATCH, "n_max");
+    if (st != MTGR_SUCCESS) return st;
+    if (n_max == 0) return ok();
+    REQUIRE_PTR(unique, "unique");
+    REQUIRE_PTR(num_unique, "num_unique");
+    REQUIRE_PTR(rows, "rows");
+    REQUIRE_PTR(workspace, "workspace");
+    if (occurrences && !aligned16(occurrences))
+        return fail(MTGR_ERROR_INVALID_ARGUMENT, "occurrences is not 16-byte aligned");
+    const size_t need = mtgr::lookup_workspace_bytes(n_max);
+    if (workspace_bytes < need)
+        return fail(MTGR_ERROR_WORKSPACE_TOO_SMALL, "workspace %zu bytes, need %zu", workspace_bytes, need);
+    hipError_t e = mtgr::launch_emb_lookup(a, n_max, unique, occurrences, (const long long*)num_unique, now,
+                                           insert ? 1 : 0, rows, workspace, (hipStream_t)stream);
+    if (e != hipSuccess) return device_fail(e, "embedding lookup");
+    return ok();
+}
+
+mtgr_status_t mtgr_embedding_gather(const mtgr_embedding_table_t* t, int64_t n, const int32_t* inverse,
+                                    const int32_t* rows, void* out, int64_t ld_out, mtgr_stream_t stream) {
+    mtgr::EmbArgs a;
+    mtgr_status_t st = check_table(t, &a);
+    if (st != MTGR_SUCCESS) return st;
+    st = check_count(n, 0x7fffffffll, "n");
+    if (st != MTGR_SUCCESS) return st;
+    if (ld_out < t->dim || ld_out % 8)
+        return fail(MTGR_ERROR_INVALID_ARGUMENT, "ld_out %lld is below dim or not a multiple of 8",
+                    (long long)ld_out);
+    if (n == 0) return ok();
+    REQUIRE_PTR(inverse, "inverse");
+    REQUIRE_PTR(rows, "rows");
+    REQUIRE_PTR(out, "out");
+    hipError_t e = mtgr::launch_emb_gather(a, n, inverse, rows, out, ld_out, (hipStream_t)stream);
+    if (e != hipSuccess) return device_fail(e, "embedding gather");
+    return ok();
+}
+
+mtgr_status_t mtgr_embedding_sgd_workspace_size(int64_t n, int64_t n_max, int32_t dim, size_t* bytes) {
+    if (!bytes) return fail(MTGR_ERROR_NULL_POINTER, "bytes is NULL");
+    mtgr_status_t st = check_count(n, EMB_MAX_BATCH, "n");
+    if (st != MTGR_SUCCESS) return st;
+    st = check_count(n_max, EMB_MAX_BATCH, "n_max");
+    if (st != MTGR_SUCCESS) return st;
+    if (dim < 8 || dim > 4096 || dim % 8)
+        return fail(MTGR_ERROR_INVALID_ARGUMENT, "dim %d is not a multiple of 8 in 8 .. 4096", dim);
+    *bytes = mtgr::sgd_workspace_bytes(n, n_max, dim);
+    return ok();
+}
+
+mtgr_status_t mtgr_embedding_sgd(const mtgr_embedding_table_t* t, int64_t n, const int32_t* inverse,
+                                 const int32_t* occurrences, const void* grad_out, int64_t ld_grad, int64_t n_max,
+                                 const int32_t* rows, const int64_t* num_unique, float lr, void* workspace,
+                                 size_t workspace_bytes, mtgr_stream_t stream) {
+    mtgr::EmbArgs a;
+    mtgr_status_t st = check_table(t, &a);
+    if (st != MTGR_SUCCESS) return st;
+    st = check_count(n, EMB_MAX_BATCH, "n");
+    if (st != MTGR_SUCCESS) return st;
+    st = check_count(n_max, EMB_MAX_BATCH, "n_max");
+    if (st != MTGR_SUCCESS) return st;
+    if (!std::isfinite(lr)) return fail(MTGR_ERROR_INVALID_ARGUMENT, "lr is not finite");
+    if (ld_grad < t->dim || ld_grad % 8)
+        return fail(MTGR_ERROR_INVALID_ARGUMENT, "ld_grad %lld is below dim or not a multiple of 8",
+                    (long long)ld_grad);
+    if (n_max == 0) return ok();
+    if (n > 0) {
+        REQUIRE_PTR(inverse, "inverse");
+        REQUIRE_PTR(occurrences, "occurrences");
+        REQUIRE_PTR(grad_out, "grad_out");
+    }
+    REQUIRE_PTR(rows, "rows");
+    REQUIRE_PTR(num_unique, "num_unique");
+    REQUIRE_PTR(workspace, "workspace");
+    const size_t need = mtgr::sgd_workspace_bytes(n, n_max, t->dim);
+    if (workspace_bytes < need)
+        return fail(MTGR_ERROR_WORKSPACE_TOO_SMALL, "workspace %zu bytes, need %zu", workspace_bytes, need);
+    hipError_t e = mtgr::launch_emb_sgd(a, n, inverse, occurrences, grad_out, ld_grad, n_max, rows,
+                                        (const long long*)num_unique, lr, workspace, (hipStream_t)stream);
+    if (e != hipSuccess) return device_fail(e, "embedding sgd");
+    return ok();
+}
+
+mtgr_status_t mtgr_embedding_evict(const mtgr_embedding_table_t* t, int32_t threshold, int64_t* num_evicted,
+                                   mtgr_stream_t stream) {
+    mtgr::EmbArgs a;
+    mtgr_status_t st = check_table(t, &a);
+    if (st != MTGR_SUCCESS) return st;
+    REQUIRE_PTR(num_evicted, "num_evicted");
+    hipError_t e = mtgr::launch_emb_evict(a, threshold, (long long*)num_evicted, (hipStream_t)stream);
+    if (e != hipSuccess) return device_fail(e, "embedding evict");
+    return ok();
+}
+
+mtgr_status_t mtgr_embedding_rehash(const mtgr_embedding_table_t* from, const mtgr_embedding_table_t* to,
+                                    mtgr_stream_t stream) {
+    mtgr::EmbArgs a, b;
+    mtgr_status_t st = check_table(from, &a);
+    if (st != MTGR_SUCCESS) return st;
+    st = check_table(to, &b);
+    if (st != MTGR_SUCCESS) return st;
+    if (from->values != to->values || from->counts != to->counts || from->last_ts != to->last_ts ||
+        from->free_rows != to->free_rows || from->state != to->state)
+        return fail(MTGR_ERROR_INVALID_ARGUMENT, "from and to must share the value store and state");
+    if (from->row_capacity != to->row_capacity || from->dim != to->dim || from->dtype != to->dtype)
+        return fail(MTGR_ERROR_INVALID_ARGUMENT, "from and to differ in row_capacity, dim or dtype");
+    if (from->keys == to->keys || from->key_rows == to->key_rows)
+        return fail(MTGR_ERROR_INVALID_ARGUMENT, "to needs a key store of its own");
+    hipError_t e = mtgr::launch_emb_rehash(a, b, (hipStream_t)stream);
+    if (e != hipSuccess) return device_fail(e, "embedding rehash");
+    return ok();
+}
 
 }  // extern "C"

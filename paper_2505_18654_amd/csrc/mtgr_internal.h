@@ -111,4 +111,37 @@ hipError_t launch_validate(const int* offsets, int num_users, long long total, i
                            const int8_t* seg, const int8_t* group_ids, int groups,
                            unsigned long long* first, hipStream_t s);
 
+// Dynamic embedding table (see include/mtgr_embedding.h): the table descriptor as the
+// kernels take it.
+struct EmbArgs {
+    long long key_capacity;   // power of two
+    int row_capacity;
+    int dim;
+    int esize;                // bytes per value element: 2 (bf16) or 4 (fp32)
+    uint64_t* keys;
+    int* key_rows;
+    void* values;
+    uint32_t* counts;
+    int* last_ts;
+    int* free_rows;
+    int* state;
+};
+size_t dedup_set_capacity(long long n);
+size_t dedup_workspace_bytes(long long n);
+size_t lookup_workspace_bytes(long long n_max);
+hipError_t launch_emb_init(const EmbArgs& t, hipStream_t s);
+hipError_t launch_emb_dedup(long long n, const uint64_t* ids, uint64_t* unique, int* occ, int* inverse,
+                            long long* num_unique, void* ws, hipStream_t s);
+hipError_t launch_emb_lookup(const EmbArgs& t, long long n_max, const uint64_t* unique, const int* occ,
+                             const long long* num_unique, int now, int insert, int* rows, void* ws,
+                             hipStream_t s);
+hipError_t launch_emb_gather(const EmbArgs& t, long long n, const int* inverse, const int* rows, void* out,
+                             long long ld_out, hipStream_t s);
+size_t sgd_workspace_bytes(long long n, long long n_max, int dim);
+hipError_t launch_emb_sgd(const EmbArgs& t, long long n, const int* inverse, const int* occ, const void* grad,
+                          long long ld_grad, long long n_max, const int* rows, const long long* num_unique,
+                          float lr, void* ws, hipStream_t s);
+hipError_t launch_emb_evict(const EmbArgs& t, int threshold, long long* num_evicted, hipStream_t s);
+hipError_t launch_emb_rehash(const EmbArgs& from, const EmbArgs& to, hipStream_t s);
+
 }  // namespace mtgr

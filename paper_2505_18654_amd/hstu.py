@@ -32,12 +32,20 @@ MTGR_BWD_KEEP_DS = 8
 MTGR_BWD_DS_READY = 16
 MTGR_FWD_CAND_ROWS = 32
 MTGR_VALIDATE_SCRATCH_BYTES = 64
+MTGR_EMB_KEY_EMPTY = 0xFFFFFFFFFFFFFFFF
+MTGR_EMB_KEY_DELETED = 0xFFFFFFFFFFFFFFFE
+MTGR_EMB_STATE_WORDS = 8
+MTGR_EMB_STATE_NEXT_ROW, MTGR_EMB_STATE_FREE_TOP, MTGR_EMB_STATE_NUM_KEYS, MTGR_EMB_STATE_OVERFLOW = 0, 1, 2, 3
 
 EXPORTED = (
     "mtgr_hstu_attn_workspace_size", "mtgr_hstu_attn_plan", "mtgr_hstu_attn_fwd", "mtgr_hstu_attn_bwd",
     "mtgr_group_layernorm_workspace_size", "mtgr_group_layernorm_fwd", "mtgr_group_layernorm_bwd",
     "mtgr_bias_silu_fwd", "mtgr_bias_silu_bwd",
     "mtgr_debug_validate_inputs", "mtgr_status_string", "mtgr_last_error_message", "mtgr_version",
+    "mtgr_embedding_init", "mtgr_embedding_dedup_workspace_size", "mtgr_embedding_dedup",
+    "mtgr_embedding_lookup_workspace_size", "mtgr_embedding_lookup", "mtgr_embedding_gather",
+    "mtgr_embedding_sgd_workspace_size", "mtgr_embedding_sgd", "mtgr_embedding_evict",
+    "mtgr_embedding_rehash",
 )
 
 
@@ -70,6 +78,15 @@ class GlnProblem(ctypes.Structure):
     ]
 
 
+class EmbeddingTable(ctypes.Structure):
+    _fields_ = [
+        ("key_capacity", ctypes.c_int64), ("row_capacity", ctypes.c_int64), ("dim", ctypes.c_int32),
+        ("dtype", ctypes.c_int32), ("keys", ctypes.c_void_p), ("key_rows", ctypes.c_void_p),
+        ("values", ctypes.c_void_p), ("counts", ctypes.c_void_p), ("last_ts", ctypes.c_void_p),
+        ("free_rows", ctypes.c_void_p), ("state", ctypes.c_void_p),
+    ]
+
+
 _lib = None
 
 
@@ -94,12 +111,20 @@ def lib() -> ctypes.CDLL:
         i64 = ctypes.c_int64
         L.mtgr_bias_silu_fwd.argtypes = [i64, i32, ctypes.c_int, vp, i64, vp, vp, i64, vp]
         L.mtgr_bias_silu_bwd.argtypes = [i64, i32, ctypes.c_int, vp, i64, vp, vp, i64, vp, i64, vp]
-        for name in ("mtgr_hstu_attn_workspace_size", "mtgr_hstu_attn_plan", "mtgr_hstu_attn_fwd",
-                     "mtgr_hstu_attn_bwd",
-                     "mtgr_group_layernorm_workspace_size", "mtgr_group_layernorm_fwd",
-                     "mtgr_group_layernorm_bwd", "mtgr_debug_validate_inputs", "mtgr_bias_silu_fwd",
-                     "mtgr_bias_silu_bwd"):
-            getattr(L, name).restype = ctypes.c_int
+        E = ctypes.POINTER(EmbeddingTable)
+        L.mtgr_embedding_init.argtypes = [E, vp]
+        L.mtgr_embedding_dedup_workspace_size.argtypes = [i64, ctypes.POINTER(sz)]
+        L.mtgr_embedding_dedup.argtypes = [i64, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.mtgr_embedding_lookup_workspace_size.argtypes = [i64, ctypes.POINTER(sz)]
+        L.mtgr_embedding_lookup.argtypes = [E, i64, vp, vp, vp, i32, i32, vp, vp, sz, vp]
+        L.mtgr_embedding_gather.argtypes = [E, i64, vp, vp, vp, i64, vp]
+        L.mtgr_embedding_sgd_workspace_size.argtypes = [i64, i64, i32, ctypes.POINTER(sz)]
+        L.mtgr_embedding_sgd.argtypes = [E, i64, vp, vp, vp, i64, i64, vp, vp, ctypes.c_float, vp, sz, vp]
+        L.mtgr_embedding_evict.argtypes = [E, i32, vp, vp]
+        L.mtgr_embedding_rehash.argtypes = [E, E, vp]
+        for name in EXPORTED:
+            if name not in ("mtgr_status_string", "mtgr_last_error_message", "mtgr_version"):
+                getattr(L, name).restype = ctypes.c_int
         L.mtgr_status_string.argtypes = [ctypes.c_int]
         L.mtgr_status_string.restype = ctypes.c_char_p
         L.mtgr_last_error_message.argtypes = []
@@ -228,3 +253,60 @@ def gln_problem(num_tokens: int, dim: int, groups: int, dtype: int = MTGR_DTYPE_
                 eps: float = 1e-5, ld_x: Optional[int] = None, ld_u: Optional[int] = None,
                 ld_y: Optional[int] = None) -> GlnProblem:
     return GlnProblem(num_tokens, dim, groups, dtype, eps, ld_x or dim, ld_u or dim, ld_y or dim)
+
+
+# ------------------------------------------------------------------ embedding table
+
+def mtgr_embedding_init(table: EmbeddingTable, stream=None) -> None:
+    _check(lib().mtgr_embedding_init(ctypes.byref(table), _stream(stream)))
+
+
+def mtgr_embedding_dedup_workspace_size(n: int) -> int:
+    out = ctypes.c_size_t(0)
+    _check(lib().mtgr_embedding_dedup_workspace_size(n, ctypes.byref(out)))
+    return out.value
+
+
+def mtgr_embedding_dedup(n, ids, unique, occurrences, inverse, num_unique, workspace, workspace_bytes,
+                         stream=None) -> None:
+    _check(lib().mtgr_embedding_dedup(n, _ptr(ids), _ptr(unique), _ptr(occurrences), _ptr(inverse),
+                                      _ptr(num_unique), _ptr(workspace), workspace_bytes, _stream(stream)))
+
+
+def mtgr_embedding_lookup_workspace_size(n_max: int) -> int:
+    out = ctypes.c_size_t(0)
+    _check(lib().mtgr_embedding_lookup_workspace_size(n_max, ctypes.byref(out)))
+    return out.value
+
+
+def mtgr_embedding_lookup(table, n_max, unique, occurrences, num_unique, now, insert, rows, workspace,
+                          workspace_bytes, stream=None) -> None:
+    _check(lib().mtgr_embedding_lookup(ctypes.byref(table), n_max, _ptr(unique), _ptr(occurrences),
+                                       _ptr(num_unique), now, int(bool(insert)), _ptr(rows), _ptr(workspace),
+                                       workspace_bytes, _stream(stream)))
+
+
+def mtgr_embedding_gather(table, n, inverse, rows, out, ld_out, stream=None) -> None:
+    _check(lib().mtgr_embedding_gather(ctypes.byref(table), n, _ptr(inverse), _ptr(rows), _ptr(out), ld_out,
+                                       _stream(stream)))
+
+
+def mtgr_embedding_sgd_workspace_size(n: int, n_max: int, dim: int) -> int:
+    out = ctypes.c_size_t(0)
+    _check(lib().mtgr_embedding_sgd_workspace_size(n, n_max, dim, ctypes.byref(out)))
+    return out.value
+
+
+def mtgr_embedding_sgd(table, n, inverse, occurrences, grad_out, ld_grad, n_max, rows, num_unique, lr,
+                       workspace, workspace_bytes, stream=None) -> None:
+    _check(lib().mtgr_embedding_sgd(ctypes.byref(table), n, _ptr(inverse), _ptr(occurrences), _ptr(grad_out),
+                                    ld_grad, n_max, _ptr(rows), _ptr(num_unique), lr, _ptr(workspace),
+                                    workspace_bytes, _stream(stream)))
+
+
+def mtgr_embedding_evict(table, threshold, num_evicted, stream=None) -> None:
+    _check(lib().mtgr_embedding_evict(ctypes.byref(table), threshold, _ptr(num_evicted), _stream(stream)))
+
+
+def mtgr_embedding_rehash(src, dst, stream=None) -> None:
+    _check(lib().mtgr_embedding_rehash(ctypes.byref(src), ctypes.byref(dst), _stream(stream)))

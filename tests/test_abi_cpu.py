@@ -9,14 +9,15 @@ import pytest
 from paper_2505_18654_amd import hstu
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "mtgr_hstu.h")
+HEADERS = [os.path.join(ROOT, "include", h) for h in sorted(os.listdir(os.path.join(ROOT, "include")))
+           if h.endswith(".h")]
 
 BF16, FP32 = hstu.MTGR_DTYPE_BF16, hstu.MTGR_DTYPE_FP32
 FAKE = 0x7f0000000000           # 256-byte aligned non-NULL address, never dereferenced
 
 
 def declared_functions():
-    text = open(HEADER).read()
+    text = "".join(open(h).read() for h in HEADERS)
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"\b(mtgr_[a-z_]+)\s*\(", text)))
 
@@ -24,6 +25,7 @@ def declared_functions():
 def test_library_exports_every_declared_function():
     names = declared_functions()
     assert "mtgr_hstu_attn_fwd" in names and "mtgr_group_layernorm_bwd" in names
+    assert "mtgr_embedding_lookup" in names
     L = hstu.lib()
     for n in names:
         assert hasattr(L, n), n
@@ -282,3 +284,64 @@ def test_cand_rows_flag_is_forward_only():
         bwd_call(p)
     assert e.value.status == hstu.MTGR_ERROR_INVALID_ARGUMENT
     assert "forward only" in hstu.mtgr_last_error_message()
+
+
+# ------------------------------------------------------------------ embedding table
+
+def emb_table(**kw):
+    base = dict(key_capacity=1024, row_capacity=500, dim=64, dtype=BF16, keys=FAKE, key_rows=FAKE,
+                values=FAKE, counts=FAKE, last_ts=FAKE, free_rows=FAKE, state=FAKE)
+    base.update(kw)
+    return hstu.EmbeddingTable(**base)
+
+
+def test_embedding_struct_layout():
+    assert ctypes.sizeof(hstu.EmbeddingTable) == 80
+    assert hstu.EmbeddingTable.keys.offset == 24
+
+
+@pytest.mark.parametrize("mutate,status", [
+    (dict(key_capacity=1000), hstu.MTGR_ERROR_INVALID_ARGUMENT),     # not a power of two
+    (dict(key_capacity=256), hstu.MTGR_ERROR_INVALID_ARGUMENT),      # below row_capacity + 1
+    (dict(row_capacity=0), hstu.MTGR_ERROR_INVALID_ARGUMENT),
+    (dict(row_capacity=2 ** 31), hstu.MTGR_ERROR_INVALID_ARGUMENT),
+    (dict(dim=12), hstu.MTGR_ERROR_INVALID_ARGUMENT),
+    (dict(dim=8192), hstu.MTGR_ERROR_INVALID_ARGUMENT),
+    (dict(dtype=5), hstu.MTGR_ERROR_UNSUPPORTED),
+    (dict(values=0), hstu.MTGR_ERROR_NULL_POINTER),
+    (dict(state=FAKE + 4), hstu.MTGR_ERROR_INVALID_ARGUMENT),        # misaligned
+])
+def test_embedding_table_checks(mutate, status):
+    with pytest.raises(hstu.MtgrError) as e:
+        hstu.mtgr_embedding_init(emb_table(**mutate), stream=0)
+    assert e.value.status == status
+
+
+def test_embedding_call_checks():
+    t = emb_table()
+    with pytest.raises(hstu.MtgrError) as e:
+        hstu.mtgr_embedding_dedup_workspace_size(2 ** 31)
+    assert e.value.status == hstu.MTGR_ERROR_INVALID_ARGUMENT
+    need = hstu.mtgr_embedding_dedup_workspace_size(1000)
+    assert need >= 1000 * 4 + 2048 * 16
+    with pytest.raises(hstu.MtgrError) as e:
+        hstu.mtgr_embedding_dedup(1000, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, need - 1, stream=0)
+    assert e.value.status == hstu.MTGR_ERROR_WORKSPACE_TOO_SMALL
+    with pytest.raises(hstu.MtgrError) as e:
+        hstu.mtgr_embedding_gather(t, 10, FAKE, FAKE, FAKE, 60, stream=0)   # ld_out < dim
+    assert e.value.status == hstu.MTGR_ERROR_INVALID_ARGUMENT
+    with pytest.raises(hstu.MtgrError) as e:
+        hstu.mtgr_embedding_sgd(t, 10, FAKE, FAKE, FAKE, 64, 10, FAKE, FAKE, float("nan"), FAKE, 1 << 20, stream=0)
+    assert e.value.status == hstu.MTGR_ERROR_INVALID_ARGUMENT
+    wsb = hstu.mtgr_embedding_lookup_workspace_size(100)
+    with pytest.raises(hstu.MtgrError) as e:
+        hstu.mtgr_embedding_lookup(t, 100, FAKE, None, FAKE, 0, 1, FAKE, FAKE, wsb - 1, stream=0)
+    assert e.value.status == hstu.MTGR_ERROR_WORKSPACE_TOO_SMALL
+    other = emb_table(keys=FAKE + 4096, key_rows=FAKE + 8192, key_capacity=2048)
+    with pytest.raises(hstu.MtgrError) as e:
+        hstu.mtgr_embedding_rehash(t, emb_table(key_capacity=2048, values=FAKE + 256), stream=0)
+    assert e.value.status == hstu.MTGR_ERROR_INVALID_ARGUMENT      # different value store
+    with pytest.raises(hstu.MtgrError) as e:
+        hstu.mtgr_embedding_rehash(t, emb_table(key_capacity=2048), stream=0)
+    assert e.value.status == hstu.MTGR_ERROR_INVALID_ARGUMENT      # same key store
+    assert other.key_capacity == 2048

@@ -57,7 +57,7 @@ enum {
  *   free_rows [row_capacity] int32       stack of rows released by eviction
  *   state     [MTGR_EMB_STATE_WORDS] int32
  * key_capacity is a power of two >= 2 and at least row_capacity + 1 (so that a probe always
- * meets a non-live slot); row_capacity in 1 .. 2^31 - 1; dim a multiple of 8 in 8 .. 4096. */
+ * meets a non-live slot); row_capacity in 1 .. 2^31 - 1; dim a multiple of 8 in 8 .. 1024. */
 typedef struct {
     int64_t key_capacity;
     int64_t row_capacity;

@@ -590,8 +590,8 @@ mtgr_status_t check_table(const mtgr_embedding_table_t* t, mtgr::EmbArgs* a) {
     if (t->key_capacity < t->row_capacity + 1)
         return fail(MTGR_ERROR_INVALID_ARGUMENT, "key_capacity %lld below row_capacity + 1",
                     (long long)t->key_capacity);
-    if (t->dim < 8 || t->dim > 4096 || t->dim % 8)
-        return fail(MTGR_ERROR_INVALID_ARGUMENT, "dim %d is not a multiple of 8 in 8 .. 4096", t->dim);
+    if (t->dim < 8 || t->dim > 1024 || t->dim % 8)
+        return fail(MTGR_ERROR_INVALID_ARGUMENT, "dim %d is not a multiple of 8 in 8 .. 1024", t->dim);
     REQUIRE_PTR(t->keys, "keys");
     REQUIRE_PTR(t->key_rows, "key_rows");
     REQUIRE_PTR(t->values, "values");
@@ -720,8 +720,8 @@ mtgr_status_t mtgr_embedding_sgd_workspace_size(int64_t n, int64_t n_max, int32_
     if (st != MTGR_SUCCESS) return st;
     st = check_count(n_max, EMB_MAX_BATCH, "n_max");
     if (st != MTGR_SUCCESS) return st;
-    if (dim < 8 || dim > 4096 || dim % 8)
-        return fail(MTGR_ERROR_INVALID_ARGUMENT, "dim %d is not a multiple of 8 in 8 .. 4096", dim);
+    if (dim < 8 || dim > 1024 || dim % 8)
+        return fail(MTGR_ERROR_INVALID_ARGUMENT, "dim %d is not a multiple of 8 in 8 .. 1024", dim);
     *bytes = mtgr::sgd_workspace_bytes(n, n_max, dim);
     return ok();
 }

@@ -58,9 +58,9 @@ __global__ void zero_i64_kernel(long long* p) { *p = 0; }
 // global set (capacity tmask + 1 >= 2 n) and adds its local count there with one atomic.
 // Skewed batches repeat a few hot IDs thousands of times; counting them in LDS first keeps the
 // global atomics on a hot ID to one per workgroup.  pos[i] = the global slot of ids[i].
-constexpr int DEDUP_PER_THREAD = 8;
-constexpr int DEDUP_CHUNK = THREADS * DEDUP_PER_THREAD;   // 2048 IDs
-constexpr int DEDUP_LCAP = 2 * DEDUP_CHUNK;               // LDS set: 4096 entries, 64 KB
+constexpr int DEDUP_PER_THREAD = 4;
+constexpr int DEDUP_CHUNK = THREADS * DEDUP_PER_THREAD;   // 1024 IDs
+constexpr int DEDUP_LCAP = 2 * DEDUP_CHUNK;               // LDS set: 2048 entries, 32 KB
 
 __global__ __launch_bounds__(THREADS) void dedup_insert_kernel(long long n, const uint64_t* __restrict__ ids,
                                                                uint64_t* tkeys, int* tocc, int* __restrict__ pos,
@@ -430,39 +430,49 @@ __global__ __launch_bounds__(THREADS) void group_scatter_kernel(long long n, con
 }
 
 // Sum of each ID's gradient rows.  The grouped positions are cut into chunks of GROUP_CHUNK;
-// one thread per (chunk, 16-byte column block) walks its chunk, summing the current ID's rows
-// in registers.  An ID whose whole range lies inside the chunk is stored; the pieces of an ID
-// that straddles chunks are added with float atomics into the zeroed accumulator.
-constexpr int GROUP_CHUNK = 64;
+// a workgroup of THREADS threads takes CPB = THREADS / cpr consecutive chunks, one thread per
+// (chunk, 16-byte column block).  A thread walks its chunk and sums runs of one ID in
+// registers: runs strictly inside the chunk are complete IDs and are stored; the first and last
+// run go to LDS, where one thread per column then merges equal IDs across the workgroup's chunks
+// and stores each merged run, or adds it with a float atomic when the ID continues beyond the
+// workgroup.  A hot ID with thousands of positions thus costs one atomic per workgroup and
+// column element instead of one per chunk.
+constexpr int GROUP_CHUNK = 32;
 
 template <int ESIZE>
-__global__ void group_sum_kernel(EmbArgs t, long long n, const int* __restrict__ list, const int* __restrict__ lu,
-                                 const int* __restrict__ start, const int* __restrict__ occ,
-                                 const void* __restrict__ grad, long long ld_grad, float* acc) {
+__global__ __launch_bounds__(THREADS) void group_sum_kernel(EmbArgs t, long long n, const int* __restrict__ list,
+                                                            const int* __restrict__ lu,
+                                                            const int* __restrict__ start,
+                                                            const int* __restrict__ occ,
+                                                            const void* __restrict__ grad, long long ld_grad,
+                                                            float* acc) {
     constexpr int epc = 16 / ESIZE, UNR = 8;
     static_assert(GROUP_CHUNK % UNR == 0, "whole unrolled steps");
-    const int cpr = t.dim / epc;
-    const long long nchunk = (n + GROUP_CHUNK - 1) / GROUP_CHUNK;
-    for (long long tid = thread_id(); tid < nchunk * cpr; tid += grid_threads()) {
-        const long long c = tid / cpr;
-        const int j = (int)(tid - c * cpr);
-        const long long p0 = c * GROUP_CHUNK, p1 = min(n, p0 + GROUP_CHUNK);
-        float f[epc];
+    __shared__ float first_part[THREADS][epc];
+    __shared__ float last_part[THREADS][epc];
+    __shared__ int first_u[THREADS];
+    __shared__ int last_u[THREADS];
+    const int cpr = t.dim / epc;                       // column blocks per row (<= THREADS here)
+    const int cpb = THREADS / cpr;                     // chunks per workgroup
+    const long long P0 = (long long)blockIdx.x * cpb * GROUP_CHUNK, P1 = min(n, P0 + (long long)cpb * GROUP_CHUNK);
+    const int c = threadIdx.x / cpr, j = threadIdx.x - c * cpr;
+    const long long p0 = P0 + (long long)c * GROUP_CHUNK, p1 = min(P1, p0 + GROUP_CHUNK);
+    auto store_or_add = [&](int u, const float* f, long long lo, long long hi) {
+        float* dst = acc + (long long)u * t.dim + j * epc;
+        const long long s0 = start[u], s1 = s0 + occ[u];
+        if (s0 >= lo && s1 <= hi) {
 #pragma unroll
-        for (int e = 0; e < epc; e++) f[e] = 0.f;
-        int cur = -1;
-        auto flush = [&]() {
-            float* dst = acc + (long long)cur * t.dim + j * epc;
-            const long long s0 = start[cur], s1 = s0 + occ[cur];
-            if (s0 >= p0 && s1 <= p1) {
+            for (int e = 0; e < epc; e++) dst[e] = f[e];
+        } else {
 #pragma unroll
-                for (int e = 0; e < epc; e++) dst[e] = f[e];
-            } else {
+            for (int e = 0; e < epc; e++) atomicAdd(dst + e, f[e]);
+        }
+    };
+    float f[epc];
 #pragma unroll
-                for (int e = 0; e < epc; e++) atomicAdd(dst + e, f[e]);
-            }
-        };
-        // UNR positions per step, their list entries and gradient chunks loaded together.
+    for (int e = 0; e < epc; e++) f[e] = 0.f;
+    int cur = -1, runs = 0;
+    if (c < cpb) {
         for (long long pb = p0; pb < p1; pb += UNR) {
             int ii[UNR], uu[UNR];
 #pragma unroll
@@ -484,8 +494,17 @@ __global__ void group_sum_kernel(EmbArgs t, long long n, const int* __restrict__
             for (int k = 0; k < UNR; k++) {
                 if (uu[k] < 0) continue;
                 if (uu[k] != cur) {
-                    if (cur >= 0) flush();
+                    if (cur >= 0) {
+                        if (runs == 1) {   // the first run of the chunk: to LDS
+                            first_u[threadIdx.x] = cur;
+#pragma unroll
+                            for (int e = 0; e < epc; e++) first_part[threadIdx.x][e] = f[e];
+                        } else {           // a run strictly inside the chunk: a whole ID
+                            store_or_add(cur, f, p0, p1);
+                        }
+                    }
                     cur = uu[k];
+                    runs++;
 #pragma unroll
                     for (int e = 0; e < epc; e++) f[e] = 0.f;
                 }
@@ -493,7 +512,37 @@ __global__ void group_sum_kernel(EmbArgs t, long long n, const int* __restrict__
                 for (int e = 0; e < epc; e++) f[e] += g[k][e];
             }
         }
-        if (cur >= 0) flush();
+    }
+    // the last run (the first as well when the chunk holds one ID; none for an empty chunk)
+    if (runs == 1) first_u[threadIdx.x] = -1;
+    if (runs == 0) first_u[threadIdx.x] = -1;
+    last_u[threadIdx.x] = cur;
+#pragma unroll
+    for (int e = 0; e < epc; e++) last_part[threadIdx.x][e] = f[e];
+    __syncthreads();
+    if (threadIdx.x < cpr) {
+        int run_u = -1;
+        float r[epc];
+#pragma unroll
+        for (int e = 0; e < epc; e++) r[e] = 0.f;
+        for (int cc = 0; cc < cpb; cc++) {
+            const int pair = cc * cpr + j;
+#pragma unroll
+            for (int half = 0; half < 2; half++) {
+                const int u = half == 0 ? first_u[pair] : last_u[pair];
+                if (u < 0) continue;
+                const float* part = half == 0 ? first_part[pair] : last_part[pair];
+                if (u != run_u) {
+                    if (run_u >= 0) store_or_add(run_u, r, P0, P1);
+                    run_u = u;
+#pragma unroll
+                    for (int e = 0; e < epc; e++) r[e] = 0.f;
+                }
+#pragma unroll
+                for (int e = 0; e < epc; e++) r[e] += part[e];
+            }
+        }
+        if (run_u >= 0) store_or_add(run_u, r, P0, P1);
     }
 }
 
@@ -686,14 +735,13 @@ hipError_t launch_emb_sgd(const EmbArgs& t, long long n, const int* inverse, con
         iscan_apply_kernel<<<(int)nblk, THREADS, 0, s>>>(occ, num_unique, n_max, bsum, start);
         group_scatter_kernel<<<(int)((n + DEDUP_CHUNK - 1) / DEDUP_CHUNK), THREADS, 0, s>>>(n, inverse, start, cursor,
                                                                                           list, lu);
-        const int epc = 16 / t.esize;
+        const int cpr = t.dim * t.esize / 16, cpb = THREADS / cpr;
         const long long nchunk = (n + GROUP_CHUNK - 1) / GROUP_CHUNK;
+        const int blocks = (int)((nchunk + cpb - 1) / cpb);
         if (t.esize == 2)
-            group_sum_kernel<2><<<grid_for(nchunk * (t.dim / epc)), THREADS, 0, s>>>(t, n, list, lu, start, occ,
-                                                                                     grad, ld_grad, acc);
+            group_sum_kernel<2><<<blocks, THREADS, 0, s>>>(t, n, list, lu, start, occ, grad, ld_grad, acc);
         else
-            group_sum_kernel<4><<<grid_for(nchunk * (t.dim / epc)), THREADS, 0, s>>>(t, n, list, lu, start, occ,
-                                                                                     grad, ld_grad, acc);
+            group_sum_kernel<4><<<blocks, THREADS, 0, s>>>(t, n, list, lu, start, occ, grad, ld_grad, acc);
     }
     const int epc = 16 / t.esize;
     if (t.esize == 2)

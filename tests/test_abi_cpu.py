@@ -306,7 +306,7 @@ def test_embedding_struct_layout():
     (dict(row_capacity=0), hstu.MTGR_ERROR_INVALID_ARGUMENT),
     (dict(row_capacity=2 ** 31), hstu.MTGR_ERROR_INVALID_ARGUMENT),
     (dict(dim=12), hstu.MTGR_ERROR_INVALID_ARGUMENT),
-    (dict(dim=8192), hstu.MTGR_ERROR_INVALID_ARGUMENT),
+    (dict(dim=2048), hstu.MTGR_ERROR_INVALID_ARGUMENT),
     (dict(dtype=5), hstu.MTGR_ERROR_UNSUPPORTED),
     (dict(values=0), hstu.MTGR_ERROR_NULL_POINTER),
     (dict(state=FAKE + 4), hstu.MTGR_ERROR_INVALID_ARGUMENT),        # misaligned

@@ -130,10 +130,11 @@ mtgr_status_t mtgr_embedding_sgd(const mtgr_embedding_table_t* t, int64_t n, con
                                  int64_t n_max, const int32_t* rows, const int64_t* num_unique, float lr,
                                  void* workspace, size_t workspace_bytes, mtgr_stream_t stream);
 
-/* Eviction by time: every live key whose row has last_ts < threshold is deleted (its slot
- * becomes DELETED, its row goes onto the free-row stack).  *num_evicted (device int64)
- * receives the number of deleted keys. */
-mtgr_status_t mtgr_embedding_evict(const mtgr_embedding_table_t* t, int32_t threshold,
+/* Eviction by time and frequency: every live key whose row has last_ts < threshold or
+ * counts < min_count is deleted (its slot becomes DELETED, its row goes onto the free-row
+ * stack).  min_count = 0 evicts by time only.  *num_evicted (device int64) receives the number
+ * of deleted keys. */
+mtgr_status_t mtgr_embedding_evict(const mtgr_embedding_table_t* t, int32_t threshold, uint32_t min_count,
                                    int64_t* num_evicted, mtgr_stream_t stream);
 
 /* Rebuilds the key store of `from` into the key store of `to` (its keys / key_rows, of

@@ -13,7 +13,9 @@ What the device table computes, written as plainly as possible:
                            every found / inserted ID gets count += occ and last_ts = now;
   gather(ids)           -> the rows of the IDs (zeros for absent IDs);
   sgd(ids, grad, lr)    -> row(id) -= lr * (sum of grad rows at the positions holding id);
-  evict(threshold)      -> every ID whose last_ts < threshold is removed; returns how many.
+  evict(threshold, min_count)
+                        -> every ID whose last_ts < threshold or whose count < min_count is
+                           removed; returns how many.
 """
 from __future__ import annotations
 
@@ -95,8 +97,8 @@ class DictTable:
             if r is not None:
                 r.value = r.value - lr * g
 
-    def evict(self, threshold: int) -> int:
-        gone = [k for k, r in self.rows.items() if r.last_ts < threshold]
+    def evict(self, threshold: int, min_count: int = 0) -> int:
+        gone = [k for k, r in self.rows.items() if r.last_ts < threshold or r.count < min_count]
         for k in gone:
             del self.rows[k]
         return len(gone)

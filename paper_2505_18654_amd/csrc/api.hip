@@ -759,13 +759,13 @@ mtgr_status_t mtgr_embedding_sgd(const mtgr_embedding_table_t* t, int64_t n, con
     return ok();
 }
 
-mtgr_status_t mtgr_embedding_evict(const mtgr_embedding_table_t* t, int32_t threshold, int64_t* num_evicted,
-                                   mtgr_stream_t stream) {
+mtgr_status_t mtgr_embedding_evict(const mtgr_embedding_table_t* t, int32_t threshold, uint32_t min_count,
+                                   int64_t* num_evicted, mtgr_stream_t stream) {
     mtgr::EmbArgs a;
     mtgr_status_t st = check_table(t, &a);
     if (st != MTGR_SUCCESS) return st;
     REQUIRE_PTR(num_evicted, "num_evicted");
-    hipError_t e = mtgr::launch_emb_evict(a, threshold, (long long*)num_evicted, (hipStream_t)stream);
+    hipError_t e = mtgr::launch_emb_evict(a, threshold, min_count, (long long*)num_evicted, (hipStream_t)stream);
     if (e != hipSuccess) return device_fail(e, "embedding evict");
     return ok();
 }

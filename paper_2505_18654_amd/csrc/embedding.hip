@@ -579,12 +579,12 @@ __global__ void sgd_apply_kernel(EmbArgs t, long long n_max, const int* __restri
 }
 
 // ------------------------------------------------------------------------ evict / rehash
-__global__ void evict_kernel(EmbArgs t, int threshold, long long* num_evicted) {
+__global__ void evict_kernel(EmbArgs t, int threshold, uint32_t min_count, long long* num_evicted) {
     for (long long p = thread_id(); p < t.key_capacity; p += grid_threads()) {
         const uint64_t k = t.keys[p];
         if (k >= KEY_DELETED) continue;
         const int row = t.key_rows[p];
-        if (row < 0 || t.last_ts[row] >= threshold) continue;
+        if (row < 0 || (t.last_ts[row] >= threshold && t.counts[row] >= min_count)) continue;
         t.keys[p] = KEY_DELETED;
         t.key_rows[p] = -1;
         const int i = atomicAdd(t.state + MTGR_EMB_STATE_FREE_TOP, 1);
@@ -751,9 +751,10 @@ hipError_t launch_emb_sgd(const EmbArgs& t, long long n, const int* inverse, con
     return hipGetLastError();
 }
 
-hipError_t launch_emb_evict(const EmbArgs& t, int threshold, long long* num_evicted, hipStream_t s) {
+hipError_t launch_emb_evict(const EmbArgs& t, int threshold, uint32_t min_count, long long* num_evicted,
+                            hipStream_t s) {
     zero_i64_kernel<<<1, 1, 0, s>>>(num_evicted);
-    evict_kernel<<<grid_for(t.key_capacity), THREADS, 0, s>>>(t, threshold, num_evicted);
+    evict_kernel<<<grid_for(t.key_capacity), THREADS, 0, s>>>(t, threshold, min_count, num_evicted);
     return hipGetLastError();
 }
 

@@ -141,7 +141,8 @@ size_t sgd_workspace_bytes(long long n, long long n_max, int dim);
 hipError_t launch_emb_sgd(const EmbArgs& t, long long n, const int* inverse, const int* occ, const void* grad,
                           long long ld_grad, long long n_max, const int* rows, const long long* num_unique,
                           float lr, void* ws, hipStream_t s);
-hipError_t launch_emb_evict(const EmbArgs& t, int threshold, long long* num_evicted, hipStream_t s);
+hipError_t launch_emb_evict(const EmbArgs& t, int threshold, uint32_t min_count, long long* num_evicted,
+                            hipStream_t s);
 hipError_t launch_emb_rehash(const EmbArgs& from, const EmbArgs& to, hipStream_t s);
 
 }  // namespace mtgr

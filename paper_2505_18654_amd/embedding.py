@@ -10,6 +10,7 @@ library's HIP kernels.  IDs are int64 tensors holding the bit patterns of uint64
     ...
     table.sgd(batch, grad_out, lr=0.05)          # sparse update of the batch's rows
     table.evict(threshold=t - window)            # drop IDs not seen since the threshold
+    table.evict(threshold=0, min_count=3)        # drop IDs seen fewer than 3 times
 """
 from __future__ import annotations
 
@@ -116,11 +117,11 @@ class DynamicEmbedding:
         hstu.mtgr_embedding_sgd(self.table, batch.n, batch.inverse, batch.occurrences, grad_out,
                                 grad_out.stride(0), batch.n_max, batch.rows, batch.num_unique, float(lr), ws, wsb)
 
-    def evict(self, threshold: int) -> int:
-        """Deletes every ID whose last lookup was before `threshold`; returns how many
-        (synchronises to read the count)."""
+    def evict(self, threshold: int, min_count: int = 0) -> int:
+        """Deletes every ID whose last lookup was before `threshold` or whose occurrence count
+        is below `min_count`; returns how many (synchronises to read the count)."""
         num = torch.empty(1, dtype=torch.int64, device=self.device)
-        hstu.mtgr_embedding_evict(self.table, int(threshold), num)
+        hstu.mtgr_embedding_evict(self.table, int(threshold), int(min_count), num)
         return int(num.item())
 
     def grow(self, key_capacity: int) -> None:

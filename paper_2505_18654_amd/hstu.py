@@ -120,7 +120,7 @@ def lib() -> ctypes.CDLL:
         L.mtgr_embedding_gather.argtypes = [E, i64, vp, vp, vp, i64, vp]
         L.mtgr_embedding_sgd_workspace_size.argtypes = [i64, i64, i32, ctypes.POINTER(sz)]
         L.mtgr_embedding_sgd.argtypes = [E, i64, vp, vp, vp, i64, i64, vp, vp, ctypes.c_float, vp, sz, vp]
-        L.mtgr_embedding_evict.argtypes = [E, i32, vp, vp]
+        L.mtgr_embedding_evict.argtypes = [E, i32, ctypes.c_uint32, vp, vp]
         L.mtgr_embedding_rehash.argtypes = [E, E, vp]
         for name in EXPORTED:
             if name not in ("mtgr_status_string", "mtgr_last_error_message", "mtgr_version"):
@@ -304,8 +304,9 @@ def mtgr_embedding_sgd(table, n, inverse, occurrences, grad_out, ld_grad, n_max,
                                     workspace_bytes, _stream(stream)))
 
 
-def mtgr_embedding_evict(table, threshold, num_evicted, stream=None) -> None:
-    _check(lib().mtgr_embedding_evict(ctypes.byref(table), threshold, _ptr(num_evicted), _stream(stream)))
+def mtgr_embedding_evict(table, threshold, min_count, num_evicted, stream=None) -> None:
+    _check(lib().mtgr_embedding_evict(ctypes.byref(table), threshold, min_count, _ptr(num_evicted),
+                                      _stream(stream)))
 
 
 def mtgr_embedding_rehash(src, dst, stream=None) -> None:

@@ -120,6 +120,7 @@ def test_evict_by_time_and_lookup_without_insert():
         ref.lookup(u, occ, now=step, insert=True)
     for thr in (2, 5):
         assert t.evict(thr) == ref.evict(thr)
+    assert t.evict(0, min_count=4) == ref.evict(0, min_count=4)   # by frequency
     live = np.array(sorted(ref.rows), np.uint64)
     probe = np.concatenate([live, np.array([1, 2, 3], np.uint64)])   # three IDs never inserted
     _, b = t.lookup(to_dev(probe), now=50, insert=False, gather=False)

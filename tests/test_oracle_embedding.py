@@ -101,3 +101,17 @@ def test_row_capacity():
     t.evict(1)
     t.lookup([3, 4, 5], [1, 1, 1], now=1, insert=True)
     assert len(t.rows) == 3
+
+
+def test_evict_by_count_brute_force():
+    rng = np.random.default_rng(4)
+    t = DictTable(1000, 2)
+    total = collections.Counter()
+    for step in range(4):
+        ids = zipf_ids(rng, 300, 150)
+        u, occ, _ = t.dedup(ids)
+        t.lookup(u, occ, now=step, insert=True)
+        total.update(int(x) for x in ids)
+    keep = {k for k, c in total.items() if c >= 5}
+    assert t.evict(0, min_count=5) == len(total) - len(keep)
+    assert set(t.rows) == keep

@@ -150,11 +150,18 @@ __global__ __launch_bounds__(WAVES * 64) void gln_fwd_kernel(GlnArgs a) {
 // (LDS atomics among the workgroup's waves, or the workgroup's own workspace slot when
 // 2 G d floats do not fit in LDS); the accumulator is then stored to the workgroup's slot
 // and gln_param_reduce_kernel sums the slots in a fixed order.  No device-wide atomics.
+// Rows of more than 2 chunks per lane (d > 1024 bf16, > 512 fp32) need more than the 256
+// registers of two waves per SIMD: there the workgroup runs half as many waves, each taking the
+// token runs of two.
+template <int NCH>
+constexpr int bwd_real_waves() { return NCH >= 4 ? BWD_WAVES / 2 : BWD_WAVES; }
+
 template <bool BF16, int NCH, bool GATE, bool LDS_ACC>
-__global__ __launch_bounds__(BWD_WAVES * 64) void gln_bwd_kernel(GlnArgs a, float* __restrict__ part,
-                                                                 int tpw) {
+__global__ __launch_bounds__(bwd_real_waves<NCH>() * 64) void gln_bwd_kernel(GlnArgs a, float* __restrict__ part,
+                                                                              int tpw) {
     using V = Vec<BF16>;
     constexpr int N = V::N;
+    constexpr int RW = bwd_real_waves<NCH>(), WPW = BWD_WAVES / RW;
     extern __shared__ float sAcc[];
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int d = a.d;
@@ -162,10 +169,10 @@ __global__ __launch_bounds__(BWD_WAVES * 64) void gln_bwd_kernel(GlnArgs a, floa
     const int accn = 2 * a.G * d;
     float* slot = part + (long long)blockIdx.x * accn;
     float* acc = LDS_ACC ? sAcc : slot;
-    for (int i = threadIdx.x; i < accn; i += BWD_WAVES * 64) acc[i] = 0.f;
+    for (int i = threadIdx.x; i < accn; i += RW * 64) acc[i] = 0.f;
     __syncthreads();
-    const long long t0 = ((long long)blockIdx.x * BWD_WAVES + w) * tpw;
-    const long long t1 = min(t0 + tpw, a.T);
+    const long long t0 = ((long long)blockIdx.x * BWD_WAVES + (long long)w * WPW) * tpw;
+    const long long t1 = min(t0 + (long long)WPW * tpw, a.T);
     const float inv_d = 1.0f / (float)d;
     float gam[NCH][N], pg[NCH][N], pb[NCH][N];
     int gcur = -1;
@@ -201,8 +208,12 @@ __global__ __launch_bounds__(BWD_WAVES * 64) void gln_bwd_kernel(GlnArgs a, floa
         mnext = a.mean[t];
         rnext = a.rstd[t];
     };
-    if (t0 < t1) load_rows(t0);
+    // The next token's rows are loaded while the current one is processed, except for the
+    // widest rows (8 chunks per lane), where the second copy would not fit in registers.
+    constexpr bool PREFETCH = NCH <= 4;
+    if (PREFETCH && t0 < t1) load_rows(t0);
     for (long long t = t0; t < t1; t++) {
+        if (!PREFETCH) load_rows(t);
         float xx[NCH][N], uu[NCH][N], dy[NCH][N];
 #pragma unroll
         for (int c = 0; c < NCH; c++)
@@ -214,7 +225,7 @@ __global__ __launch_bounds__(BWD_WAVES * 64) void gln_bwd_kernel(GlnArgs a, floa
             }
         const int g = gnext;
         const float mean = mnext, rstd = rnext;
-        if (t + 1 < t1) load_rows(t + 1);
+        if (PREFETCH && t + 1 < t1) load_rows(t + 1);
         if (g != gcur) {
             flush();
             gcur = g;
@@ -272,7 +283,7 @@ __global__ __launch_bounds__(BWD_WAVES * 64) void gln_bwd_kernel(GlnArgs a, floa
     flush();
     __syncthreads();
     if (LDS_ACC)
-        for (int i = threadIdx.x; i < accn; i += BWD_WAVES * 64) slot[i] = sAcc[i];
+        for (int i = threadIdx.x; i < accn; i += RW * 64) slot[i] = sAcc[i];
 }
 
 // dgamma/dbeta = sum over workgroup slots (fixed order).  Block = 64 columns x 4 row sets.
@@ -311,12 +322,13 @@ static hipError_t gln_launch(const GlnArgs& a, bool bwd, hipStream_t s) {
     const bool lds = accn * (int)sizeof(float) <= GLN_LDS_ACC_BYTES;
     const size_t shm = lds ? accn * sizeof(float) : 0;
     float* part = a.workspace;
+    constexpr int threads = bwd_real_waves<NCH>() * 64;
     if (lds) {
-        if (gate) gln_bwd_kernel<BF16, NCH, true, true><<<nslots, BWD_WAVES * 64, shm, s>>>(a, part, tpw);
-        else gln_bwd_kernel<BF16, NCH, false, true><<<nslots, BWD_WAVES * 64, shm, s>>>(a, part, tpw);
+        if (gate) gln_bwd_kernel<BF16, NCH, true, true><<<nslots, threads, shm, s>>>(a, part, tpw);
+        else gln_bwd_kernel<BF16, NCH, false, true><<<nslots, threads, shm, s>>>(a, part, tpw);
     } else {
-        if (gate) gln_bwd_kernel<BF16, NCH, true, false><<<nslots, BWD_WAVES * 64, 0, s>>>(a, part, tpw);
-        else gln_bwd_kernel<BF16, NCH, false, false><<<nslots, BWD_WAVES * 64, 0, s>>>(a, part, tpw);
+        if (gate) gln_bwd_kernel<BF16, NCH, true, false><<<nslots, threads, 0, s>>>(a, part, tpw);
+        else gln_bwd_kernel<BF16, NCH, false, false><<<nslots, threads, 0, s>>>(a, part, tpw);
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

@@ -21,6 +21,15 @@ struct Vec;   // 16-byte chunk of the storage type
 template <>
 struct Vec<true> {
     static constexpr int N = 8;
+    __device__ static uint4 raw(const void* base, long long idx) { return *(const uint4*)((const uint16_t*)base + idx); }
+    __device__ static void unpack(const uint4 u, float* out) {
+        const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+        for (int i = 0; i < 4; i++) {
+            out[2 * i] = __uint_as_float(w[i] << 16);
+            out[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+        }
+    }
     __device__ static void load(const void* base, long long idx, float* out) {
         const uint4 u = *(const uint4*)((const uint16_t*)base + idx);
         const uint32_t w[4] = {u.x, u.y, u.z, u.w};
@@ -43,6 +52,11 @@ struct Vec<true> {
 template <>
 struct Vec<false> {
     static constexpr int N = 4;
+    __device__ static uint4 raw(const void* base, long long idx) { return *(const uint4*)((const float*)base + idx); }
+    __device__ static void unpack(const uint4 u, float* out) {
+        out[0] = __uint_as_float(u.x); out[1] = __uint_as_float(u.y);
+        out[2] = __uint_as_float(u.z); out[3] = __uint_as_float(u.w);
+    }
     __device__ static void load(const void* base, long long idx, float* out) {
         const float4 f = *(const float4*)((const float*)base + idx);
         out[0] = f.x; out[1] = f.y; out[2] = f.z; out[3] = f.w;
@@ -190,42 +204,56 @@ __global__ __launch_bounds__(bwd_real_waves<NCH>() * 64) void gln_bwd_kernel(Gln
             }
         }
     };
-    // raw rows and statistics of the token being processed and of the next one
-    float xr[NCH][N] = {}, ur[NCH][N] = {}, yr[NCH][N] = {};
-    int gnext = 0;
-    float mnext = 0.f, rnext = 0.f;
-    auto load_rows = [&](long long t) {
+    // Rows and statistics of the tokens ahead, kept as the raw 16-byte chunks as loaded.  Up to
+    // two chunks per lane the next two tokens are in flight while the current one is
+    // processed (three rows are read per token, and one token per wave in flight leaves HBM
+    // idle), the next one up to four chunks, none at eight (no registers left).
+    struct Rows {
+        uint4 x[NCH], y[NCH], u[NCH];
+        int g;
+        float m, r;
+    };
+    auto fetch = [&](long long t, Rows& r) {
 #pragma unroll
         for (int c = 0; c < NCH; c++) {
             const int ch = lane + 64 * c;
             if (ch < nch) {
-                V::load(a.x, t * a.ld_x + ch * N, xr[c]);
-                V::load(a.dy, t * a.ld_y + ch * N, yr[c]);
-                if (GATE) V::load(a.u, t * a.ld_u + ch * N, ur[c]);
+                r.x[c] = V::raw(a.x, t * a.ld_x + ch * N);
+                r.y[c] = V::raw(a.dy, t * a.ld_y + ch * N);
+                if (GATE) r.u[c] = V::raw(a.u, t * a.ld_u + ch * N);
             }
         }
-        gnext = a.gid[t];
-        mnext = a.mean[t];
-        rnext = a.rstd[t];
+        r.g = a.gid[t];
+        r.m = a.mean[t];
+        r.r = a.rstd[t];
     };
-    // The next token's rows are loaded while the current one is processed, except for the
-    // widest rows (8 chunks per lane), where the second copy would not fit in registers.
-    constexpr bool PREFETCH = NCH <= 4;
-    if (PREFETCH && t0 < t1) load_rows(t0);
+    constexpr int PFD = NCH <= 2 ? 2 : NCH <= 4 ? 1 : 0;
+    Rows ring[PFD > 0 ? PFD : 1] = {};
+#pragma unroll
+    for (int k = 0; k < PFD; k++)
+        if (t0 + k < t1) fetch(t0 + k, ring[k]);
     for (long long t = t0; t < t1; t++) {
-        if (!PREFETCH) load_rows(t);
+        Rows cur;
+        if constexpr (PFD == 0) {
+            cur = Rows{};
+            fetch(t, cur);
+        } else {
+            cur = ring[0];
+#pragma unroll
+            for (int k = 0; k + 1 < PFD; k++) ring[k] = ring[k + 1];
+            if (t + PFD < t1) fetch(t + PFD, ring[PFD - 1]);
+        }
         float xx[NCH][N], uu[NCH][N], dy[NCH][N];
 #pragma unroll
-        for (int c = 0; c < NCH; c++)
+        for (int c = 0; c < NCH; c++) {
+            V::unpack(cur.x[c], xx[c]);
+            V::unpack(cur.y[c], dy[c]);
 #pragma unroll
-            for (int i = 0; i < N; i++) {
-                xx[c][i] = xr[c][i];
-                dy[c][i] = yr[c][i];
-                uu[c][i] = GATE ? ur[c][i] : 1.f;
-            }
-        const int g = gnext;
-        const float mean = mnext, rstd = rnext;
-        if (PREFETCH && t + 1 < t1) load_rows(t + 1);
+            for (int i = 0; i < N; i++) uu[c][i] = 1.f;
+            if (GATE) V::unpack(cur.u[c], uu[c]);
+        }
+        const int g = cur.g;
+        const float mean = cur.m, rstd = cur.r;
         if (g != gcur) {
             flush();
             gcur = g;

@@ -62,13 +62,22 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_ds_bf16_kernel(AttnArgs a)
         return tile_class(sq64, sk, overlap);
     };
     TileWalker<decltype(written_of)> written(written_of, ntk);
-    // 8 KB block copied as is: instruction i of wave w moves bytes [1024 (4 i + w), +1024).
+    // 8 KB block: instruction i of wave w fills bytes [1024 (4 i + w), +1024) of the LDS copy.
+    // The 16-byte unit u = 128 sub-block + 32 row + v of the block (row = 2 kq + g, v = 16-byte
+    // half of a fragment row) sits at u ^ dsw(u), which permutes units only inside aligned groups
+    // of 16.  Stored as is, the 32 lanes of one transposing read below (4 rows x 8 chunks of one
+    // fragment column range) hit 4 bank pairs, 8 lanes each; swizzled, 32 distinct ones.
+    auto dsw = [](int u) {
+        const int row = (u >> 5) & 3;
+        return ((row & 1) << 1) | ((row >> 1) << 2) | (((u >> 4) & 1) << 3);
+    };
     auto block_dma = [&](uint16_t* dst, const uint16_t* src) {
 #pragma unroll
         for (int i = 0; i < 2; i++) {
             const int part = __builtin_amdgcn_readfirstlane(i * 4 + w);
+            const int u = part * 64 + lane;
             lds_dma16(__builtin_amdgcn_readfirstlane(lds_address(dst) + (uint32_t)part * 1024u),
-                      uniform_ptr(src + part * 512), (uint32_t)lane * 16u);
+                      uniform_ptr(src + part * 512), (uint32_t)((u ^ dsw(u)) & 63) * 16u);
         }
     };
     auto issue = [&](int t, int buf) {
@@ -83,16 +92,20 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_ds_bf16_kernel(AttnArgs a)
     // 16 (G % 2) + 4 q .. + 3, i.e. chunk (kq = G % 2, g = q / 2, lane' = key % 32 + 32 (q % 2)).
     // k-step ks, half p of its 8 slots adds key offset 8 (2 ks + p): sub-block (2 ks + p) / 4,
     // chunk offset 8 ((2 ks + p) % 4).
+    // In the swizzled copy the lane's unit moves by dsw (its row and v bit 4 fix it: the same for
+    // every k-step), and the k-step's offset of 4 units is applied by XOR (the two touch the
+    // same unit bits).
     const int gq = lane >> 4, sq_ = (lane & 15) >> 2, qq = lane & 3;
     const uint32_t ds_lane = (uint32_t)(w & 1) * 4096u +
-                             (uint32_t)(((2 * (gq & 1) + (qq >> 1)) * 64 + 32 * (qq & 1) + 4 * (gq >> 1) + sq_) * 8);
+                             ((uint32_t)(((2 * (gq & 1) + (qq >> 1)) * 64 + 32 * (qq & 1) + 4 * (gq >> 1) + sq_) * 8) ^
+                              (uint32_t)((((qq >> 1) << 1) | ((gq & 1) << 2) | ((qq & 1) << 3)) * 16));
     auto ds_operand = [&](const uint16_t* blk, int ks) {
-        const char* base = (const char*)blk + ds_lane;
+        const char* base = (const char*)blk;
         const int c0 = 2 * ks, c1 = 2 * ks + 1;
         const short4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (lds_short4*)(base + (c0 >> 2) * 2048 + 64 * (c0 & 3)));
+            (lds_short4*)(base + (c0 >> 2) * 2048 + (ds_lane ^ (64u * (c0 & 3)))));
         const short4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (lds_short4*)(base + (c1 >> 2) * 2048 + 64 * (c1 & 3)));
+            (lds_short4*)(base + (c1 >> 2) * 2048 + (ds_lane ^ (64u * (c1 & 3)))));
         const short __attribute__((ext_vector_type(8))) v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
         return __builtin_bit_cast(bf16x8, v);
     };

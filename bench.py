@@ -160,8 +160,9 @@ def main():
                          "FETCH_SIZE / WRITE_SIZE counters) and exit")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py: this build measures one GPU; --gpus {args.gpus} is not supported "
-              "(the hot path shards by user across GPUs with no forward exchange; see DESIGN.md)",
+        print(f"bench.py: measures one GPU only; --gpus {args.gpus} is not supported "
+              "(users are independent, so the path would shard by user across GPUs with no "
+              "exchange in the forward pass and one small all-reduce of the parameter gradients)",
               file=sys.stderr)
         sys.exit(2)
 

@@ -287,19 +287,15 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
                 lds_barrier();
                 t2 = walk.next(t1 + 1, &cls2);
                 if (t2 < ntk) issue_k(t2, P);
-                // half 1 of t_i; next S = half 0 of t_{i+1}
-                if (!RAB && partial) premask(sB, C1{}, sVts[P], sVcode[P], qrel);
-                if (RAB && partial)
-                    half_step(T{}, T{}, T{}, CP{}, C1{}, CQ{}, C0{}, sB, sA, pkA, pkB, qrel);
-                else
-                    half_step(T{}, T{}, F{}, CP{}, C1{}, CQ{}, C0{}, sB, sA, pkA, pkB, qrel);
-            } else {
-                if (!RAB && partial) premask(sB, C1{}, sVts[P], sVcode[P], qrel);
-                if (RAB && partial)
-                    half_step(T{}, F{}, T{}, CP{}, C1{}, CP{}, C0{}, sB, sA, pkA, pkB, qrel);
-                else
-                    half_step(T{}, F{}, F{}, CP{}, C1{}, CP{}, C0{}, sB, sA, pkA, pkB, qrel);
             }
+            // half 1 of t_i; next S = half 0 of t_{i+1}.  After the last tile that S is formed
+            // from the idle K buffer (no copy is in flight into it) and never used: one code
+            // path for every tile keeps the O accumulators in one set of registers.
+            if (!RAB && partial) premask(sB, C1{}, sVts[P], sVcode[P], qrel);
+            if (RAB && partial)
+                half_step(T{}, T{}, T{}, CP{}, C1{}, CQ{}, C0{}, sB, sA, pkA, pkB, qrel);
+            else
+                half_step(T{}, T{}, F{}, CP{}, C1{}, CQ{}, C0{}, sB, sA, pkA, pkB, qrel);
             // PV of keys 48 .. 63
             const bf16x8 pb = as_bf16x8(make_uint4(pkB[0], pkB[1], pkB[2], pkB[3]));
 #pragma unroll

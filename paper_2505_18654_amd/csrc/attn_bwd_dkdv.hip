@@ -22,10 +22,9 @@ template <int DH, bool RAB, bool STORE>
 __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) {
     constexpr int CPR = DH / 8, KSTEPS = DH / 16, DBLK = DH / 32, UNIT = 32 * DH;
     __shared__ __align__(16) uint16_t sK[BM * DH];
-    __shared__ __align__(16) uint16_t sQ0[UNIT];
-    __shared__ __align__(16) uint16_t sQ1[UNIT];
-    __shared__ __align__(16) uint16_t sG0[UNIT];
-    __shared__ __align__(16) uint16_t sG1[UNIT];
+    // Query unit buffers: Q then dO of one unit in one array, so that a dO operand sits a constant
+    // distance from the Q operand read with the same lane offset (one address for both reads).
+    __shared__ __align__(16) uint16_t sQG[2][2 * UNIT];
     __shared__ int sQts[2][32];
     __shared__ int sQcode[2][32];
     __shared__ float sRab[MTGR_RAB_LDS];
@@ -94,8 +93,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
     // when it starts past the user's end, so every copied unit holds a valid row).
     auto issue = [&](int t, int half, int buf) {
         const int r0 = t * BN + 32 * half;
-        tile_dma<DH, 32>(buf ? sQ1 : sQ0, Qb, a.ld_q, r0, nb, h * DH, tid);
-        tile_dma<DH, 32>(buf ? sG1 : sG0, Gb, a.ld_o, r0, nb, h * DH, tid);
+        tile_dma<DH, 32>(sQG[buf], Qb, a.ld_q, r0, nb, h * DH, tid);
+        tile_dma<DH, 32>(sQG[buf] + UNIT, Gb, a.ld_o, r0, nb, h * DH, tid);
         codes_dma<32>(sQts[buf], sQcode[buf], a.ts + ob, a.tok_code + ob, r0, nb, tid);
     };
 
@@ -125,8 +124,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
             hn = 0;
         }
         if (tn < ntq) issue(tn, hn, buf ^ 1);
-        const uint16_t* sQ = buf ? sQ1 : sQ0;
-        const uint16_t* sG = buf ? sG1 : sG0;
+        const uint16_t* sQ = sQG[buf];
+        const uint16_t* sG = sQ + UNIT;
         const int* qts = sQts[buf];
         const int* qcode = sQcode[buf];
 

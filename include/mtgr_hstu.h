@@ -87,7 +87,12 @@ typedef void* mtgr_stream_t;            /* hipStream_t */
 
 /* Shape of one attention call.
  *   num_users B >= 0, total_tokens T >= 0 (T < 2^31), max_seqlen >= every user's length.
- *   num_heads H in 1..255; head_dim dh: bf16 {32, 64, 128}, fp32 {16, 32, 64, 128}.
+ *   num_heads H in 1..255; head_dim dh in {16, 32, 64, 128} for both dtypes.  bf16 at
+ *     dh = 32..128 runs on the bf16 matrix cores; bf16 at dh = 16 runs on vector-ALU kernels
+ *     with bf16 storage and fp32 arithmetic (a pair then holds 64 flop of products against
+ *     the SiLU's transcendental work, so the matrix cores would not pay), as does fp32.
+ *   A problem whose work list would reach 2^24 workgroups returns MTGR_ERROR_UNSUPPORTED
+ *     (one launch holds at most 2^32 - 1 work-items).
  *   alpha: multiplier of q.k inside the SiLU (Eq. 5 has none: pass 1.0).
  *   num_rab_buckets: 0 = no relative bias, else 1..64 (rab is [H][num_rab_buckets] fp32;
  *     a gap whose log-time bucket is >= num_rab_buckets uses the last bucket).
@@ -111,7 +116,8 @@ typedef struct {
 } mtgr_hstu_problem_t;
 
 /* Shape of one gate + Group-LN call.
- *   num_tokens T >= 0, dim d (bf16: multiple of 8 and <= 4096; fp32: multiple of 4 and <= 2048),
+ *   num_tokens T in 0 .. 2^28 - 1, dim d (bf16: multiple of 8 and <= 4096; fp32: multiple of 4
+ *   and <= 2048),
  *   num_groups G in 1..127, eps > 0.
  *   ld_*: token strides in elements (>= d).  Gradients share the layout of their
  *   primal: dx uses ld_x, du ld_u, dy ld_y. */
@@ -131,7 +137,8 @@ typedef struct {
  *     H * sum_b ceil(n_b / 64)^2 blocks of 8 KB, from T, B and max_seqlen).  With it the
  *     bf16 backward stores dS from its dk/dv kernel and forms dq from it (fewer operations;
  *     the same dS operand, so dq differs from the recomputing form only in the order of its
- *     float sums).  The first bytes have the backward = 0 layout, so one plan serves. */
+ *     float sums).  The first bytes have the backward = 0 layout, so one plan serves.
+ *     For fp32 and for bf16 at head_dim 16 (vector-ALU kernels) both sizes are equal. */
 mtgr_status_t mtgr_hstu_attn_workspace_size(const mtgr_hstu_problem_t* p, int backward,
                                             size_t* bytes);
 

@@ -40,6 +40,11 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 constexpr int MAX_SEQLEN = (mtgr::SCHED_BUCKETS - 1) * 64;
 
+// The vector-ALU kernels serve fp32 and bf16 at head_dim 16; the MFMA kernels the rest.
+bool vec_path(const mtgr_hstu_problem_t* p) {
+    return p->dtype == MTGR_DTYPE_FP32 || p->head_dim == 16;
+}
+
 struct AttnLayout {
     int tile;            // rows per work item
     int ntile;           // 64-token summary tiles per user
@@ -50,7 +55,7 @@ struct AttnLayout {
 
 AttnLayout attn_layout(const mtgr_hstu_problem_t* p) {
     AttnLayout L{};
-    L.tile = p->dtype == MTGR_DTYPE_BF16 ? mtgr::ATTN_TILE_BF16 : mtgr::ATTN_TILE_F32;
+    L.tile = vec_path(p) ? mtgr::ATTN_TILE_F32 : mtgr::ATTN_TILE_BF16;
     L.ntile = (p->max_seqlen + 63) / 64;
     L.slots = mtgr::schedule_slots(p->total_tokens, p->num_users, p->max_seqlen, p->num_heads, L.tile);
     L.off_summ = 0;
@@ -63,7 +68,7 @@ AttnLayout attn_layout(const mtgr_hstu_problem_t* p) {
     L.off_ds = L.total;
     const size_t blocks = (size_t)p->num_heads * (size_t)L.ntile *
                           (size_t)((p->total_tokens + 63) / 64 + p->num_users);
-    L.total_bwd = p->dtype == MTGR_DTYPE_BF16 ? L.off_ds + blocks * mtgr::DS_BLOCK_BYTES : L.total;
+    L.total_bwd = vec_path(p) ? L.total : L.off_ds + blocks * mtgr::DS_BLOCK_BYTES;
     return L;
 }
 
@@ -86,8 +91,7 @@ mtgr_status_t check_problem(const mtgr_hstu_problem_t* p) {
         return fail(MTGR_ERROR_INVALID_ARGUMENT, "num_heads %d outside 1..%d", p->num_heads,
                     MTGR_MAX_HEADS);
     const int dh = p->head_dim;
-    const bool dh_ok = p->dtype == MTGR_DTYPE_BF16 ? (dh == 32 || dh == 64 || dh == 128)
-                                                    : (dh == 16 || dh == 32 || dh == 64 || dh == 128);
+    const bool dh_ok = dh == 16 || dh == 32 || dh == 64 || dh == 128;
     if (!dh_ok)
         return fail(MTGR_ERROR_UNSUPPORTED, "head_dim %d not supported for %s", dh,
                     p->dtype == MTGR_DTYPE_BF16 ? "bf16" : "fp32");
@@ -113,9 +117,11 @@ mtgr_status_t check_problem(const mtgr_hstu_problem_t* p) {
             return fail(MTGR_ERROR_UNSUPPORTED, "%s %lld above %lld elements", names[i], lds[i],
                         (long long)MTGR_MAX_LD);
     }
+    // Every attention kernel launches one 256-thread workgroup per work-list slot, and a grid
+    // holds at most 2^32 - 1 work-items.
     if (mtgr::schedule_slots(p->total_tokens, p->num_users, p->max_seqlen, p->num_heads,
-                             mtgr::ATTN_TILE_F32) >= (1ll << 31))
-        return fail(MTGR_ERROR_UNSUPPORTED, "problem too large for one launch");
+                             vec_path(p) ? mtgr::ATTN_TILE_F32 : mtgr::ATTN_TILE_BF16) >= (1ll << 24))
+        return fail(MTGR_ERROR_UNSUPPORTED, "problem too large for one launch (2^24 work items or more)");
     return MTGR_SUCCESS;
 }
 
@@ -245,7 +251,7 @@ mtgr_status_t mtgr_hstu_attn_fwd(const mtgr_hstu_problem_t* p, const int32_t* of
     a.cand_rows = (p->flags & MTGR_FWD_CAND_ROWS) ? 1 : 0;
     hipError_t e = p->dtype == MTGR_DTYPE_BF16
                        ? mtgr::launch_attn_fwd_bf16(a, p->head_dim, (int)L.slots, s)
-                       : mtgr::launch_attn_fwd_f32(a, p->head_dim, (int)L.slots, s);
+                       : mtgr::launch_attn_fwd_f32(a, p->head_dim, (int)L.slots, s);   // bf16 dh 16: vector kernel
     if (e != hipSuccess) return device_fail(e, "attention forward");
     return ok();
 }
@@ -290,8 +296,9 @@ mtgr_status_t mtgr_hstu_attn_bwd(const mtgr_hstu_problem_t* p, const int32_t* of
         REQUIRE_PTR(dv, "dv");
     }
     const AttnLayout L = attn_layout(p);
-    // Stored-dS path: bf16 and a backward-size workspace.
-    const bool ds_path = p->dtype == MTGR_DTYPE_BF16 && L.total_bwd > L.total && workspace_bytes >= L.total_bwd;
+    // Stored-dS path: the MFMA kernels and a backward-size workspace.
+    const bool vec = vec_path(p);
+    const bool ds_path = !vec && L.total_bwd > L.total && workspace_bytes >= L.total_bwd;
     if ((keep_ds || ds_ready) && !ds_path)
         return fail(MTGR_ERROR_WORKSPACE_TOO_SMALL,
                     "MTGR_BWD_KEEP_DS / _DS_READY need a bf16 problem and %zu workspace bytes", L.total_bwd);
@@ -304,9 +311,10 @@ mtgr_status_t mtgr_hstu_attn_bwd(const mtgr_hstu_problem_t* p, const int32_t* of
     plan.store_ds = want_dkdv && ds_path && (want_dq || keep_ds);
     plan.dq_from_ds = want_dq && (ds_ready || (want_dkdv && ds_path));
     plan.dq_recompute = want_dq && !plan.dq_from_ds;
-    // drab comes from the dk/dv kernel when it runs (bf16), else from the recomputing dq kernel
-    float* drab_out = p->dtype == MTGR_DTYPE_BF16 ? ((want_dkdv || plan.dq_recompute) ? drab : nullptr)
-                                                  : (want_dq ? drab : nullptr);
+    // drab comes from the dk/dv kernel when it runs (MFMA kernels), else from the recomputing
+    // dq kernel; the vector-ALU kernels form it in their dq kernel
+    float* drab_out = !vec ? ((want_dkdv || plan.dq_recompute) ? drab : nullptr)
+                           : (want_dq ? drab : nullptr);
     if (drab_out) {
         hipError_t e = mtgr::launch_fill_f32(drab_out, (long long)p->num_heads * p->num_rab_buckets, 0.f, s);
         if (e != hipSuccess) return device_fail(e, "drab fill");
@@ -321,9 +329,9 @@ mtgr_status_t mtgr_hstu_attn_bwd(const mtgr_hstu_problem_t* p, const int32_t* of
     a.dk = dk;
     a.dv = dv;
     a.drab = drab_out;
-    hipError_t e = p->dtype == MTGR_DTYPE_BF16
-                       ? mtgr::launch_attn_bwd_bf16(a, p->head_dim, (int)L.slots, plan, s)
-                       : mtgr::launch_attn_bwd_f32(a, p->head_dim, (int)L.slots, want_dq, want_dkdv, s);
+    hipError_t e = !vec ? mtgr::launch_attn_bwd_bf16(a, p->head_dim, (int)L.slots, plan, s)
+                        : mtgr::launch_attn_bwd_vec(a, p->dtype == MTGR_DTYPE_BF16, p->head_dim, (int)L.slots,
+                                                    want_dq, want_dkdv, s);
     if (e != hipSuccess) return device_fail(e, "attention backward");
     return ok();
 }
@@ -337,6 +345,10 @@ mtgr_status_t check_gln(const mtgr_gln_problem_t* p) {
     if (p->dtype != MTGR_DTYPE_BF16 && p->dtype != MTGR_DTYPE_FP32)
         return fail(MTGR_ERROR_UNSUPPORTED, "dtype %d is not supported", p->dtype);
     if (p->num_tokens < 0) return fail(MTGR_ERROR_INVALID_ARGUMENT, "num_tokens < 0");
+    // The forward launches 16 work-items per token (a wave per four tokens); a grid holds at
+    // most 2^32 - 1 work-items.
+    if (p->num_tokens >= (1ll << 28))
+        return fail(MTGR_ERROR_UNSUPPORTED, "num_tokens %lld above 2^28 - 1", (long long)p->num_tokens);
     const int vec = p->dtype == MTGR_DTYPE_BF16 ? 8 : 4;
     const int dmax = p->dtype == MTGR_DTYPE_BF16 ? 4096 : 2048;
     if (p->dim <= 0 || p->dim % vec != 0)

@@ -33,10 +33,11 @@ using bwd::BM;
 using bwd::BN;
 }  // namespace
 
-// ------------------------------------------------------------------ fp32 parity kernels
-// dq kernel: 64 query rows, 4 threads per row (dh/4 features each); keys staged 32 at a time.
-template <int DH, bool RAB>
-__global__ __launch_bounds__(256) void attn_bwd_dq_f32_kernel(AttnArgs a) {
+// ------------------------------------------------------------------ vector-ALU kernels
+// fp32 storage (the parity mode) or bf16 storage at head_dim 16 (see the forward's vector
+// kernel); arithmetic in fp32.  dq kernel: 64 query rows, 4 threads per row (dh/4 features each); keys staged 32 at a time.
+template <int DH, bool RAB, class E>
+__global__ __launch_bounds__(256) void attn_bwd_dq_vec_kernel(AttnArgs a) {
     constexpr int BMF = 64, SUB = 32, Q4 = DH / 4, KP = DH + 1;
     __shared__ float sK[SUB * KP];
     __shared__ float sV[SUB * KP];
@@ -57,15 +58,15 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_f32_kernel(AttnArgs a) {
     const TileSummary sq = load_summary(summ, qt);
     const int qi = q0 + (tid >> 2), part = tid & 3;
     const bool qvalid = qi < nb;
-    const float* Q = (const float*)a.q;
-    const float* K = (const float*)a.k;
-    const float* V = (const float*)a.v;
-    const float* DO = (const float*)a.dout;
+    const E* Q = (const E*)a.q;
+    const E* K = (const E*)a.k;
+    const E* V = (const E*)a.v;
+    const E* DO = (const E*)a.dout;
     float qv[Q4], gv[Q4], acc[Q4];
 #pragma unroll
     for (int c = 0; c < Q4; c++) {
-        qv[c] = qvalid ? Q[(long long)(ob + qi) * a.ld_q + h * DH + part * Q4 + c] : 0.f;
-        gv[c] = qvalid ? DO[(long long)(ob + qi) * a.ld_o + h * DH + part * Q4 + c] : 0.f;
+        qv[c] = qvalid ? ld_elem(Q, (long long)(ob + qi) * a.ld_q + h * DH + part * Q4 + c) : 0.f;
+        gv[c] = qvalid ? ld_elem(DO, (long long)(ob + qi) * a.ld_o + h * DH + part * Q4 + c) : 0.f;
         acc[c] = 0.f;
     }
     int qcode = 0, qts = 0;
@@ -85,8 +86,8 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_f32_kernel(AttnArgs a) {
             __syncthreads();
             for (int i = tid; i < SUB * DH; i += 256) {
                 const int row = i / DH, c = i % DH, key = kb + row;
-                sK[row * KP + c] = key < nb ? K[(long long)(ob + key) * a.ld_k + h * DH + c] : 0.f;
-                sV[row * KP + c] = key < nb ? V[(long long)(ob + key) * a.ld_v + h * DH + c] : 0.f;
+                sK[row * KP + c] = key < nb ? ld_elem(K, (long long)(ob + key) * a.ld_k + h * DH + c) : 0.f;
+                sV[row * KP + c] = key < nb ? ld_elem(V, (long long)(ob + key) * a.ld_v + h * DH + c) : 0.f;
             }
             if (tid < SUB) {
                 const int key = kb + tid;
@@ -124,16 +125,16 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_f32_kernel(AttnArgs a) {
     __syncthreads();
     if (want_drab && tid < a.nbuckets && sHist[tid] != 0.f) atomicAdd(&a.drab[h * a.nbuckets + tid], sHist[tid]);
     if (qvalid) {
-        float* DQ = (float*)a.dq;
+        E* DQ = (E*)a.dq;
 #pragma unroll
         for (int c = 0; c < Q4; c++)
-            DQ[(long long)(ob + qi) * a.ld_q + h * DH + part * Q4 + c] = a.alpha * acc[c];
+            st_elem(DQ, (long long)(ob + qi) * a.ld_q + h * DH + part * Q4 + c, a.alpha * acc[c]);
     }
 }
 
 // dkdv kernel: 64 key rows, 4 threads per key; queries staged 32 at a time.
-template <int DH, bool RAB>
-__global__ __launch_bounds__(256) void attn_bwd_dkdv_f32_kernel(AttnArgs a) {
+template <int DH, bool RAB, class E>
+__global__ __launch_bounds__(256) void attn_bwd_dkdv_vec_kernel(AttnArgs a) {
     constexpr int BMF = 64, SUB = 32, Q4 = DH / 4, KP = DH + 1;
     __shared__ float sQ[SUB * KP];
     __shared__ float sG[SUB * KP];
@@ -152,15 +153,15 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_f32_kernel(AttnArgs a) {
     const TileSummary sk = load_summary(summ, kt);
     const int kj = k0 + (tid >> 2), part = tid & 3;
     const bool kvalid = kj < nb;
-    const float* Q = (const float*)a.q;
-    const float* K = (const float*)a.k;
-    const float* V = (const float*)a.v;
-    const float* DO = (const float*)a.dout;
+    const E* Q = (const E*)a.q;
+    const E* K = (const E*)a.k;
+    const E* V = (const E*)a.v;
+    const E* DO = (const E*)a.dout;
     float kv[Q4], vv[Q4], dk[Q4], dv[Q4];
 #pragma unroll
     for (int c = 0; c < Q4; c++) {
-        kv[c] = kvalid ? K[(long long)(ob + kj) * a.ld_k + h * DH + part * Q4 + c] : 0.f;
-        vv[c] = kvalid ? V[(long long)(ob + kj) * a.ld_v + h * DH + part * Q4 + c] : 0.f;
+        kv[c] = kvalid ? ld_elem(K, (long long)(ob + kj) * a.ld_k + h * DH + part * Q4 + c) : 0.f;
+        vv[c] = kvalid ? ld_elem(V, (long long)(ob + kj) * a.ld_v + h * DH + part * Q4 + c) : 0.f;
         dk[c] = 0.f;
         dv[c] = 0.f;
     }
@@ -178,8 +179,8 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_f32_kernel(AttnArgs a) {
             __syncthreads();
             for (int i = tid; i < SUB * DH; i += 256) {
                 const int row = i / DH, c = i % DH, qr = qb + row;
-                sQ[row * KP + c] = qr < nb ? Q[(long long)(ob + qr) * a.ld_q + h * DH + c] : 0.f;
-                sG[row * KP + c] = qr < nb ? DO[(long long)(ob + qr) * a.ld_o + h * DH + c] : 0.f;
+                sQ[row * KP + c] = qr < nb ? ld_elem(Q, (long long)(ob + qr) * a.ld_q + h * DH + c) : 0.f;
+                sG[row * KP + c] = qr < nb ? ld_elem(DO, (long long)(ob + qr) * a.ld_o + h * DH + c) : 0.f;
             }
             if (tid < SUB) {
                 const int qr = qb + tid;
@@ -214,12 +215,12 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_f32_kernel(AttnArgs a) {
         }
     }
     if (kvalid) {
-        float* DK = (float*)a.dk;
-        float* DV = (float*)a.dv;
+        E* DK = (E*)a.dk;
+        E* DV = (E*)a.dv;
 #pragma unroll
         for (int c = 0; c < Q4; c++) {
-            DK[(long long)(ob + kj) * a.ld_k + h * DH + part * Q4 + c] = a.alpha * dk[c];
-            DV[(long long)(ob + kj) * a.ld_v + h * DH + part * Q4 + c] = dv[c];
+            st_elem(DK, (long long)(ob + kj) * a.ld_k + h * DH + part * Q4 + c, a.alpha * dk[c]);
+            st_elem(DV, (long long)(ob + kj) * a.ld_v + h * DH + part * Q4 + c, dv[c]);
         }
     }
 }
@@ -247,15 +248,15 @@ static hipError_t bwd_bf16_dh(const AttnArgs& a, int slots, const BwdPlan& plan,
     return hipSuccess;
 }
 
-template <int DH, bool RAB_IN>
-static hipError_t bwd_f32_dh(const AttnArgs& a, int slots, bool dq, bool dkdv, hipStream_t s) {
+template <int DH, bool RAB_IN, class E>
+static hipError_t bwd_vec_dh(const AttnArgs& a, int slots, bool dq, bool dkdv, hipStream_t s) {
     if (dq) {
-        attn_bwd_dq_f32_kernel<DH, RAB_IN><<<slots, 256, 0, s>>>(a);
+        attn_bwd_dq_vec_kernel<DH, RAB_IN, E><<<slots, 256, 0, s>>>(a);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
     if (dkdv) {
-        attn_bwd_dkdv_f32_kernel<DH, RAB_IN><<<slots, 256, 0, s>>>(a);
+        attn_bwd_dkdv_vec_kernel<DH, RAB_IN, E><<<slots, 256, 0, s>>>(a);
         return hipGetLastError();
     }
     return hipSuccess;
@@ -272,14 +273,19 @@ hipError_t launch_attn_bwd_bf16(const AttnArgs& a, int head_dim, int slots, cons
     }
 }
 
-hipError_t launch_attn_bwd_f32(const AttnArgs& a, int head_dim, int slots, bool dq, bool dkdv,
+hipError_t launch_attn_bwd_vec(const AttnArgs& a, bool bf16, int head_dim, int slots, bool dq, bool dkdv,
                                hipStream_t s) {
     const bool rab = a.rab != nullptr;
+    if (bf16) {
+        if (head_dim != 16) return hipErrorInvalidValue;
+        return rab ? bwd_vec_dh<16, true, uint16_t>(a, slots, dq, dkdv, s)
+                   : bwd_vec_dh<16, false, uint16_t>(a, slots, dq, dkdv, s);
+    }
     switch (head_dim) {
-        case 16: return rab ? bwd_f32_dh<16, true>(a, slots, dq, dkdv, s) : bwd_f32_dh<16, false>(a, slots, dq, dkdv, s);
-        case 32: return rab ? bwd_f32_dh<32, true>(a, slots, dq, dkdv, s) : bwd_f32_dh<32, false>(a, slots, dq, dkdv, s);
-        case 64: return rab ? bwd_f32_dh<64, true>(a, slots, dq, dkdv, s) : bwd_f32_dh<64, false>(a, slots, dq, dkdv, s);
-        case 128: return rab ? bwd_f32_dh<128, true>(a, slots, dq, dkdv, s) : bwd_f32_dh<128, false>(a, slots, dq, dkdv, s);
+        case 16: return rab ? bwd_vec_dh<16, true, float>(a, slots, dq, dkdv, s) : bwd_vec_dh<16, false, float>(a, slots, dq, dkdv, s);
+        case 32: return rab ? bwd_vec_dh<32, true, float>(a, slots, dq, dkdv, s) : bwd_vec_dh<32, false, float>(a, slots, dq, dkdv, s);
+        case 64: return rab ? bwd_vec_dh<64, true, float>(a, slots, dq, dkdv, s) : bwd_vec_dh<64, false, float>(a, slots, dq, dkdv, s);
+        case 128: return rab ? bwd_vec_dh<128, true, float>(a, slots, dq, dkdv, s) : bwd_vec_dh<128, false, float>(a, slots, dq, dkdv, s);
         default: return hipErrorInvalidValue;
     }
 }

@@ -342,10 +342,12 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
     }
 }
 
-// fp32 parity kernel: 64 query rows per workgroup, 4 threads per row each owning dh/4
-// features; keys staged 32 at a time in LDS; plain FMA loops.
-template <int DH, bool RAB>
-__global__ __launch_bounds__(256) void attn_fwd_f32_kernel(AttnArgs a) {
+// Vector-ALU kernel (fp32 storage, the parity mode; or bf16 storage at head_dim 16, where a
+// pair holds 64 flop of products against the SiLU's transcendental work, so matrix cores would
+// not pay): 64 query rows per workgroup, 4 threads per row each owning dh/4 features; keys
+// staged 32 at a time in LDS as fp32; plain FMA loops in fp32.
+template <int DH, bool RAB, class E>
+__global__ __launch_bounds__(256) void attn_fwd_vec_kernel(AttnArgs a) {
     constexpr int BMF = 64, SUB = 32, Q4 = DH / 4, KP = DH + 1;
     __shared__ float sK[SUB * KP];
     __shared__ float sV[SUB * KP];
@@ -367,13 +369,13 @@ __global__ __launch_bounds__(256) void attn_fwd_f32_kernel(AttnArgs a) {
     const int qi = q0 + (tid >> 2), part = tid & 3;
     const bool qvalid = qi < nb;
     int qcode = 0, qts = 0;
-    const float* Q = (const float*)a.q;
-    const float* K = (const float*)a.k;
-    const float* V = (const float*)a.v;
+    const E* Q = (const E*)a.q;
+    const E* K = (const E*)a.k;
+    const E* V = (const E*)a.v;
     float qv[Q4], ov[Q4];
 #pragma unroll
     for (int c = 0; c < Q4; c++) {
-        qv[c] = qvalid ? Q[(long long)(ob + qi) * a.ld_q + h * DH + part * Q4 + c] : 0.f;
+        qv[c] = qvalid ? ld_elem(Q, (long long)(ob + qi) * a.ld_q + h * DH + part * Q4 + c) : 0.f;
         ov[c] = 0.f;
     }
     if (qvalid) {
@@ -391,8 +393,8 @@ __global__ __launch_bounds__(256) void attn_fwd_f32_kernel(AttnArgs a) {
             __syncthreads();
             for (int i = tid; i < SUB * DH; i += 256) {
                 const int row = i / DH, c = i % DH, key = kb + row;
-                sK[row * KP + c] = key < nb ? K[(long long)(ob + key) * a.ld_k + h * DH + c] : 0.f;
-                sV[row * KP + c] = key < nb ? V[(long long)(ob + key) * a.ld_v + h * DH + c] : 0.f;
+                sK[row * KP + c] = key < nb ? ld_elem(K, (long long)(ob + key) * a.ld_k + h * DH + c) : 0.f;
+                sV[row * KP + c] = key < nb ? ld_elem(V, (long long)(ob + key) * a.ld_v + h * DH + c) : 0.f;
             }
             if (tid < SUB) {
                 const int key = kb + tid;
@@ -418,9 +420,9 @@ __global__ __launch_bounds__(256) void attn_fwd_f32_kernel(AttnArgs a) {
         }
     }
     if (qvalid && (!a.cand_rows || a.seg[ob + qi] == SEG_CAND)) {
-        float* O = (float*)a.out;
+        E* O = (E*)a.out;
 #pragma unroll
-        for (int c = 0; c < Q4; c++) O[(long long)(ob + qi) * a.ld_o + h * DH + part * Q4 + c] = ov[c];
+        for (int c = 0; c < Q4; c++) st_elem(O, (long long)(ob + qi) * a.ld_o + h * DH + part * Q4 + c, ov[c]);
     }
 }
 
@@ -433,17 +435,18 @@ static hipError_t fwd_bf16_dh(const AttnArgs& a, int slots, hipStream_t s) {
     return hipGetLastError();
 }
 
-template <int DH>
-static hipError_t fwd_f32_dh(const AttnArgs& a, int slots, hipStream_t s) {
+template <int DH, class E>
+static hipError_t fwd_vec_dh(const AttnArgs& a, int slots, hipStream_t s) {
     if (a.rab)
-        attn_fwd_f32_kernel<DH, true><<<slots, 256, 0, s>>>(a);
+        attn_fwd_vec_kernel<DH, true, E><<<slots, 256, 0, s>>>(a);
     else
-        attn_fwd_f32_kernel<DH, false><<<slots, 256, 0, s>>>(a);
+        attn_fwd_vec_kernel<DH, false, E><<<slots, 256, 0, s>>>(a);
     return hipGetLastError();
 }
 
 hipError_t launch_attn_fwd_bf16(const AttnArgs& a, int head_dim, int slots, hipStream_t s) {
     switch (head_dim) {
+        case 16: return fwd_vec_dh<16, uint16_t>(a, slots, s);
         case 32: return fwd_bf16_dh<32>(a, slots, s);
         case 64: return fwd_bf16_dh<64>(a, slots, s);
         case 128: return fwd_bf16_dh<128>(a, slots, s);
@@ -453,10 +456,10 @@ hipError_t launch_attn_fwd_bf16(const AttnArgs& a, int head_dim, int slots, hipS
 
 hipError_t launch_attn_fwd_f32(const AttnArgs& a, int head_dim, int slots, hipStream_t s) {
     switch (head_dim) {
-        case 16: return fwd_f32_dh<16>(a, slots, s);
-        case 32: return fwd_f32_dh<32>(a, slots, s);
-        case 64: return fwd_f32_dh<64>(a, slots, s);
-        case 128: return fwd_f32_dh<128>(a, slots, s);
+        case 16: return fwd_vec_dh<16, float>(a, slots, s);
+        case 32: return fwd_vec_dh<32, float>(a, slots, s);
+        case 64: return fwd_vec_dh<64, float>(a, slots, s);
+        case 128: return fwd_vec_dh<128, float>(a, slots, s);
         default: return hipErrorInvalidValue;
     }
 }

@@ -163,6 +163,10 @@ __device__ __forceinline__ float bf16_to_f32(uint16_t h) {
     return __uint_as_float(((uint32_t)h) << 16);
 }
 
+// Element access of the vector-ALU kernels, which store either fp32 or bf16 and compute in fp32.
+__device__ __forceinline__ float ld_elem(const float* p, long long i) { return p[i]; }
+__device__ __forceinline__ float ld_elem(const uint16_t* p, long long i) { return bf16_to_f32(p[i]); }
+
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef float float2_t __attribute__((ext_vector_type(2)));
 
@@ -173,6 +177,9 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 }
 
 __device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) { return pack_bf16x2(f, 0.f) & 0xffffu; }
+
+__device__ __forceinline__ void st_elem(float* p, long long i, float v) { p[i] = v; }
+__device__ __forceinline__ void st_elem(uint16_t* p, long long i, float v) { p[i] = (uint16_t)f32_to_bf16_bits(v); }
 
 // v + (v of another lane of the same 16-lane row), the partner chosen by a DPP control.
 template <int CTRL>

@@ -60,7 +60,8 @@ hipError_t launch_attn_bwd_bf16(const AttnArgs& a, int head_dim, int slots, cons
                                 hipStream_t s);
 hipError_t launch_ds_offsets(const int* offsets, int num_users, int heads, long long* ds_off,
                              hipStream_t s);
-hipError_t launch_attn_bwd_f32(const AttnArgs& a, int head_dim, int slots, bool dq, bool dkdv,
+// Vector-ALU backward: fp32 storage at any supported head_dim, or bf16 storage at head_dim 16.
+hipError_t launch_attn_bwd_vec(const AttnArgs& a, bool bf16, int head_dim, int slots, bool dq, bool dkdv,
                                hipStream_t s);
 
 struct GlnArgs {
@@ -94,7 +95,7 @@ hipError_t launch_gln_fwd(const GlnArgs& a, bool bf16, hipStream_t s);
 hipError_t launch_gln_bwd(const GlnArgs& a, bool bf16, hipStream_t s);
 
 constexpr int ATTN_TILE_BF16 = 128;   // query / key rows per work item, bf16 kernels
-constexpr int ATTN_TILE_F32 = 64;     // rows per work item, fp32 kernels
+constexpr int ATTN_TILE_F32 = 64;     // rows per work item, vector-ALU kernels (fp32, bf16 at dh 16)
 constexpr int SCHED_BUCKETS = 4096;   // length buckets of the heavy-first sort
 constexpr int XCDS = 8;               // accelerator complex dies of an MI355X
 

@@ -91,3 +91,42 @@ def dense_gln(x, u, gid, gamma, beta, eps=1e-5):
     zn = torch.nn.functional.layer_norm(z, (z.shape[1],), eps=eps)
     g = torch.as_tensor(np.asarray(gid), dtype=torch.long)
     return zn * gamma[g] + beta[g]
+
+
+def operand_rounding_bounds(offsets, seg, ts, q, k, v, dout, rab=None, alpha=1.0):
+    """Per-element bound of the error that rounding the MFMA operands P and dS to bf16 (half
+    an ulp, 2^-9 relative, round to nearest) adds to the attention outputs, for inputs whose
+    products cancel (e.g. activations with a non-zero mean): each output element is a sum of
+    terms, and rounding each P or dS factor perturbs the sum by at most 2^-9 times the sum
+    of the terms' magnitudes,
+        o_i: 2^-9 sum_j |p_ij| |v_j|        dv_j: 2^-9 sum_i |p_ij| |dout_i|
+        dq_i: 2^-9 alpha sum_j |dS_ij| |k_j|   dk_j: 2^-9 alpha sum_i |dS_ij| |q_i|
+    (p, dS with their 1/n_b, as in Eq. 5 and its chain rule).  numpy fp64 [T, H, dh] in,
+    dict of [T, H, dh] bounds out; dense per user (small batches only)."""
+    offsets = np.asarray(offsets)
+    q, k, v, dout = (np.asarray(x, np.float64) for x in (q, k, v, dout))
+    out = {name: np.zeros_like(q) for name in ("o", "dq", "dk", "dv")}
+    u = 2.0 ** -9
+    for b in range(len(offsets) - 1):
+        s0, s1 = int(offsets[b]), int(offsets[b + 1])
+        n = s1 - s0
+        if n == 0:
+            continue
+        sg_t = torch.from_numpy(np.asarray(seg[s0:s1], np.int64))[None]
+        ts_t = torch.from_numpy(np.asarray(ts[s0:s1]))[None]
+        M = rule_mask(sg_t, ts_t, torch.ones(1, n, dtype=torch.bool))[0].numpy()
+        for h in range(q.shape[1]):
+            Q, K, V, G = q[s0:s1, h], k[s0:s1, h], v[s0:s1, h], dout[s0:s1, h]
+            S = alpha * (Q @ K.T)
+            if rab is not None:
+                gap = np.abs(np.asarray(ts[s0:s1], np.int64)[:, None] - np.asarray(ts[s0:s1], np.int64)[None, :])
+                bk = bucket_torch(torch.from_numpy(gap)).clamp(max=rab.shape[1] - 1).numpy()
+                S = S + np.asarray(rab)[h][bk]
+            sg = 1.0 / (1.0 + np.exp(-S))
+            P = np.where(M, S * sg, 0.0) / n
+            dS = np.where(M, (G @ V.T) * sg * (1.0 + S * (1.0 - sg)), 0.0) / n
+            out["o"][s0:s1, h] = u * np.abs(P) @ np.abs(V)
+            out["dv"][s0:s1, h] = u * np.abs(P).T @ np.abs(G)
+            out["dq"][s0:s1, h] = u * abs(alpha) * np.abs(dS) @ np.abs(K)
+            out["dk"][s0:s1, h] = u * abs(alpha) * np.abs(dS).T @ np.abs(Q)
+    return out

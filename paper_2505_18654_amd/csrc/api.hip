@@ -201,6 +201,34 @@ mtgr_status_t schedule(const mtgr_hstu_problem_t* p, const AttnLayout& L, const 
     return MTGR_SUCCESS;
 }
 
+// Forward after check_attn_common passed on (workspace, its size).
+mtgr_status_t attn_fwd_checked(const mtgr_hstu_problem_t* p, const int32_t* offsets, const int8_t* seg,
+                               const int32_t* ts, const void* q, const void* k, const void* v,
+                               const float* rab, void* out, void* workspace, hipStream_t s) {
+    if (p->num_users == 0 || p->total_tokens == 0) return ok();
+    REQUIRE_PTR(q, "q");
+    REQUIRE_PTR(k, "k");
+    REQUIRE_PTR(v, "v");
+    REQUIRE_PTR(out, "out");
+    const AttnLayout L = attn_layout(p);
+    if (!(p->flags & MTGR_ATTN_PLANNED)) {
+        mtgr_status_t st = schedule(p, L, offsets, seg, ts, workspace, s);
+        if (st != MTGR_SUCCESS) return st;
+    }
+    mtgr::AttnArgs a = make_args(p, L, offsets, seg, ts, workspace);
+    a.q = q;
+    a.k = k;
+    a.v = v;
+    a.rab = rab;
+    a.out = out;
+    a.cand_rows = (p->flags & MTGR_FWD_CAND_ROWS) ? 1 : 0;
+    // bf16 at head_dim 16 goes to the vector kernel inside launch_attn_fwd_bf16
+    hipError_t e = p->dtype == MTGR_DTYPE_BF16 ? mtgr::launch_attn_fwd_bf16(a, p->head_dim, (int)L.slots, s)
+                                               : mtgr::launch_attn_fwd_f32(a, p->head_dim, (int)L.slots, s);
+    if (e != hipSuccess) return device_fail(e, "attention forward");
+    return ok();
+}
+
 }  // namespace
 
 extern "C" {
@@ -231,29 +259,7 @@ mtgr_status_t mtgr_hstu_attn_fwd(const mtgr_hstu_problem_t* p, const int32_t* of
                                  size_t workspace_bytes, mtgr_stream_t stream) {
     mtgr_status_t st = check_attn_common(p, offsets, seg, ts, rab, workspace, workspace_bytes);
     if (st != MTGR_SUCCESS) return st;
-    if (p->num_users == 0 || p->total_tokens == 0) return ok();
-    REQUIRE_PTR(q, "q");
-    REQUIRE_PTR(k, "k");
-    REQUIRE_PTR(v, "v");
-    REQUIRE_PTR(out, "out");
-    hipStream_t s = (hipStream_t)stream;
-    const AttnLayout L = attn_layout(p);
-    if (!(p->flags & MTGR_ATTN_PLANNED)) {
-        st = schedule(p, L, offsets, seg, ts, workspace, s);
-        if (st != MTGR_SUCCESS) return st;
-    }
-    mtgr::AttnArgs a = make_args(p, L, offsets, seg, ts, workspace);
-    a.q = q;
-    a.k = k;
-    a.v = v;
-    a.rab = rab;
-    a.out = out;
-    a.cand_rows = (p->flags & MTGR_FWD_CAND_ROWS) ? 1 : 0;
-    hipError_t e = p->dtype == MTGR_DTYPE_BF16
-                       ? mtgr::launch_attn_fwd_bf16(a, p->head_dim, (int)L.slots, s)
-                       : mtgr::launch_attn_fwd_f32(a, p->head_dim, (int)L.slots, s);   // bf16 dh 16: vector kernel
-    if (e != hipSuccess) return device_fail(e, "attention forward");
-    return ok();
+    return attn_fwd_checked(p, offsets, seg, ts, q, k, v, rab, out, workspace, (hipStream_t)stream);
 }
 
 mtgr_status_t mtgr_hstu_attn_bwd(const mtgr_hstu_problem_t* p, const int32_t* offsets,

@@ -175,6 +175,31 @@ mtgr_status_t mtgr_hstu_attn_fwd(const mtgr_hstu_problem_t* p, const int32_t* of
                                  const void* k, const void* v, const float* rab, void* out,
                                  void* workspace, size_t workspace_bytes, mtgr_stream_t stream);
 
+/* Bytes of the per-GPU device array that holds the plan of mtgr_hstu_attn_fwd_noalloc. */
+#define MTGR_NOALLOC_SCRATCH_BYTES (16u * 1024u * 1024u)
+
+/* For callers that cannot allocate device memory: code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc.  mtgr_hstu_attn_fwd without a workspace: the plan (tile
+ * summaries, work list, token codes) is built on every call into a file-scope device array of
+ * the library, MTGR_NOALLOC_SCRATCH_BYTES on each GPU it runs on, kept until the process ends.
+ * Same arguments and results as mtgr_hstu_attn_fwd otherwise (same kernels and plan, so the
+ * output is bit for bit that of mtgr_hstu_attn_fwd).
+ *   - Calls nothing that allocates (no hipMalloc / hipFree).  Its first call on a device looks
+ *     up that device's array address (hipGetSymbolAddress), with that device current.
+ *   - stream must belong to the current device (MTGR_ERROR_INVALID_ARGUMENT otherwise).
+ *   - Every call on one GPU shares that GPU's array, which keeps the last call's plan: calls
+ *     that overlap on one GPU (different streams, or host threads) race and give undefined
+ *     output; order them on one stream.
+ *   - A problem whose plan (mtgr_hstu_attn_workspace_size(p, 0)) exceeds
+ *     MTGR_NOALLOC_SCRATCH_BYTES returns MTGR_ERROR_UNSUPPORTED before any launch (the five
+ *     workloads of the benchmark need at most 7.4 MB: 1024 users, 1.5M tokens, 6 heads).
+ *   - MTGR_ATTN_PLANNED is rejected (MTGR_ERROR_INVALID_ARGUMENT): there is no plan kept for
+ *     the caller between calls. */
+mtgr_status_t mtgr_hstu_attn_fwd_noalloc(const mtgr_hstu_problem_t* p, const int32_t* offsets,
+                                         const int8_t* seg, const int32_t* ts, const void* q,
+                                         const void* k, const void* v, const float* rab, void* out,
+                                         mtgr_stream_t stream);
+
 /* Backward of Eq. 5: given dout = dL/dout, writes dq, dk, dv (same dtype and
  * layout as q, k, v) and, when drab != NULL, drab = dL/drab ([H][num_rab_buckets]
  * fp32; requires rab != NULL).  With s = alpha q.k + rab, sg = sigmoid(s):

@@ -4,6 +4,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <mutex>
 #include <string>
 
 #include "../../include/mtgr_embedding.h"
@@ -201,6 +202,36 @@ mtgr_status_t schedule(const mtgr_hstu_problem_t* p, const AttnLayout& L, const 
     return MTGR_SUCCESS;
 }
 
+// Plan storage of mtgr_hstu_attn_fwd_noalloc: a file-scope device array, one per GPU the library
+// runs on, held until the process ends.  In host code `scratch` names a host-side stand-in, so
+// host code only ever uses the device address hipGetSymbolAddress returns for it.
+__device__ __align__(256) unsigned char scratch[MTGR_NOALLOC_SCRATCH_BYTES];
+
+constexpr int MAX_DEVICES = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[MAX_DEVICES] = {};
+
+// Device address of `scratch` on the current device: looked up once per device (with that device
+// current, at its first call) and kept.
+mtgr_status_t scratch_of_current_device(void** ptr) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return device_fail(e, "hipGetDevice");
+    if (dev < 0 || dev >= MAX_DEVICES)
+        return fail(MTGR_ERROR_UNSUPPORTED, "device %d above the %d devices with a scratch address", dev,
+                    MAX_DEVICES);
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return device_fail(e, "hipGetSymbolAddress(scratch)");
+        if (!p) return fail(MTGR_ERROR_DEVICE, "hipGetSymbolAddress(scratch) returned NULL");
+        g_scratch_ptr[dev] = p;
+    }
+    *ptr = g_scratch_ptr[dev];
+    return MTGR_SUCCESS;
+}
+
 // Forward after check_attn_common passed on (workspace, its size).
 mtgr_status_t attn_fwd_checked(const mtgr_hstu_problem_t* p, const int32_t* offsets, const int8_t* seg,
                                const int32_t* ts, const void* q, const void* k, const void* v,
@@ -260,6 +291,37 @@ mtgr_status_t mtgr_hstu_attn_fwd(const mtgr_hstu_problem_t* p, const int32_t* of
     mtgr_status_t st = check_attn_common(p, offsets, seg, ts, rab, workspace, workspace_bytes);
     if (st != MTGR_SUCCESS) return st;
     return attn_fwd_checked(p, offsets, seg, ts, q, k, v, rab, out, workspace, (hipStream_t)stream);
+}
+
+mtgr_status_t mtgr_hstu_attn_fwd_noalloc(const mtgr_hstu_problem_t* p, const int32_t* offsets,
+                                         const int8_t* seg, const int32_t* ts, const void* q, const void* k,
+                                         const void* v, const float* rab, void* out, mtgr_stream_t stream) {
+    mtgr_status_t st = check_problem(p);
+    if (st != MTGR_SUCCESS) return st;
+    if (p->flags & MTGR_ATTN_PLANNED)
+        return fail(MTGR_ERROR_INVALID_ARGUMENT,
+                    "MTGR_ATTN_PLANNED: the no-alloc forward rebuilds its plan in the shared scratch on every call");
+    if (p->num_users == 0 || p->total_tokens == 0) return ok();
+    const AttnLayout L = attn_layout(p);
+    if (L.total > (size_t)MTGR_NOALLOC_SCRATCH_BYTES)
+        return fail(MTGR_ERROR_UNSUPPORTED, "the plan needs %zu bytes, above the %u-byte scratch", L.total,
+                    (unsigned)MTGR_NOALLOC_SCRATCH_BYTES);
+    hipStream_t s = (hipStream_t)stream;
+    int cur = -1, sdev = -1;
+    hipError_t e = hipGetDevice(&cur);
+    if (e != hipSuccess) return device_fail(e, "hipGetDevice");
+    if (s) {
+        e = hipStreamGetDevice(s, &sdev);
+        if (e != hipSuccess) return device_fail(e, "hipStreamGetDevice");
+        if (sdev != cur)
+            return fail(MTGR_ERROR_INVALID_ARGUMENT, "stream of device %d while device %d is current", sdev, cur);
+    }
+    void* ws = nullptr;
+    st = scratch_of_current_device(&ws);
+    if (st != MTGR_SUCCESS) return st;
+    st = check_attn_common(p, offsets, seg, ts, rab, ws, MTGR_NOALLOC_SCRATCH_BYTES);
+    if (st != MTGR_SUCCESS) return st;
+    return attn_fwd_checked(p, offsets, seg, ts, q, k, v, rab, out, ws, s);
 }
 
 mtgr_status_t mtgr_hstu_attn_bwd(const mtgr_hstu_problem_t* p, const int32_t* offsets,

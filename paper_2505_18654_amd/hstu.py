@@ -32,6 +32,7 @@ MTGR_BWD_KEEP_DS = 8
 MTGR_BWD_DS_READY = 16
 MTGR_FWD_CAND_ROWS = 32
 MTGR_VALIDATE_SCRATCH_BYTES = 64
+MTGR_NOALLOC_SCRATCH_BYTES = 16 * 1024 * 1024
 MTGR_EMB_KEY_EMPTY = 0xFFFFFFFFFFFFFFFF
 MTGR_EMB_KEY_DELETED = 0xFFFFFFFFFFFFFFFE
 MTGR_EMB_STATE_WORDS = 8
@@ -39,6 +40,7 @@ MTGR_EMB_STATE_NEXT_ROW, MTGR_EMB_STATE_FREE_TOP, MTGR_EMB_STATE_NUM_KEYS, MTGR_
 
 EXPORTED = (
     "mtgr_hstu_attn_workspace_size", "mtgr_hstu_attn_plan", "mtgr_hstu_attn_fwd", "mtgr_hstu_attn_bwd",
+    "mtgr_hstu_attn_fwd_noalloc",
     "mtgr_group_layernorm_workspace_size", "mtgr_group_layernorm_fwd", "mtgr_group_layernorm_bwd",
     "mtgr_bias_silu_fwd", "mtgr_bias_silu_bwd",
     "mtgr_debug_validate_inputs", "mtgr_status_string", "mtgr_last_error_message", "mtgr_version",
@@ -103,6 +105,7 @@ def lib() -> ctypes.CDLL:
         L.mtgr_hstu_attn_workspace_size.argtypes = [P, ctypes.c_int, ctypes.POINTER(sz)]
         L.mtgr_hstu_attn_plan.argtypes = [P, vp, vp, vp, vp, sz, vp]
         L.mtgr_hstu_attn_fwd.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.mtgr_hstu_attn_fwd_noalloc.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp]
         L.mtgr_hstu_attn_bwd.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
         L.mtgr_group_layernorm_workspace_size.argtypes = [G, ctypes.c_int, ctypes.POINTER(sz)]
         L.mtgr_group_layernorm_fwd.argtypes = [G, vp, vp, vp, vp, vp, vp, vp, vp, vp]
@@ -190,6 +193,11 @@ def mtgr_hstu_attn_fwd(problem, offsets, seg, ts, q, k, v, rab, out, workspace, 
     _check(lib().mtgr_hstu_attn_fwd(ctypes.byref(problem), _ptr(offsets), _ptr(seg), _ptr(ts),
                                     _ptr(q), _ptr(k), _ptr(v), _ptr(rab), _ptr(out), _ptr(workspace),
                                     int(workspace_bytes), _stream(stream)))
+
+
+def mtgr_hstu_attn_fwd_noalloc(problem, offsets, seg, ts, q, k, v, rab, out, stream=None) -> None:
+    _check(lib().mtgr_hstu_attn_fwd_noalloc(ctypes.byref(problem), _ptr(offsets), _ptr(seg), _ptr(ts),
+                                            _ptr(q), _ptr(k), _ptr(v), _ptr(rab), _ptr(out), _stream(stream)))
 
 
 def mtgr_hstu_attn_bwd(problem, offsets, seg, ts, q, k, v, rab, dout, dq, dk, dv, drab, workspace,

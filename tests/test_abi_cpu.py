@@ -362,3 +362,41 @@ def test_embedding_call_checks():
         hstu.mtgr_embedding_rehash(t, emb_table(key_capacity=2048), stream=0)
     assert e.value.status == hstu.MTGR_ERROR_INVALID_ARGUMENT      # same key store
     assert other.key_capacity == 2048
+
+
+def noalloc(p, **over):
+    args = dict(offsets=FAKE, seg=FAKE, ts=FAKE, q=FAKE, k=FAKE, v=FAKE, rab=None, out=FAKE)
+    args.update(over)
+    hstu.mtgr_hstu_attn_fwd_noalloc(p, args["offsets"], args["seg"], args["ts"], args["q"], args["k"],
+                                    args["v"], args["rab"], args["out"], 0)
+
+
+def test_noalloc_refusals_before_any_device_call():
+    """The allocation-free forward rejects, on the host and before touching the device, a plan
+    larger than its scratch array, the MTGR_ATTN_PLANNED flag and invalid problems."""
+    big = prob(num_users=4096, total_tokens=6_000_000, max_seqlen=3000, heads=8)
+    assert hstu.mtgr_hstu_attn_workspace_size(big) > hstu.MTGR_NOALLOC_SCRATCH_BYTES
+    with pytest.raises(hstu.MtgrError) as e:
+        noalloc(big)
+    assert e.value.status == hstu.MTGR_ERROR_UNSUPPORTED
+    assert "scratch" in hstu.mtgr_last_error_message()
+    p = prob()
+    p.flags = hstu.MTGR_ATTN_PLANNED
+    with pytest.raises(hstu.MtgrError) as e:
+        noalloc(p)
+    assert e.value.status == hstu.MTGR_ERROR_INVALID_ARGUMENT
+    with pytest.raises(hstu.MtgrError) as e:
+        noalloc(prob(head_dim=48))
+    assert e.value.status == hstu.MTGR_ERROR_UNSUPPORTED
+    noalloc(prob(num_users=0, total_tokens=0))     # empty batch: a successful no-op
+
+
+def test_noalloc_scratch_covers_the_workloads():
+    """The five benchmark workloads fit the scratch (serving: 1024 users, 1.5M tokens)."""
+    from synth import make_layout
+    for name in ("tiny", "small", "mtgr_small", "mtgr_large", "serving"):
+        L = make_layout(name)
+        p = prob(num_users=L.num_users, total_tokens=L.total_tokens, max_seqlen=L.max_seqlen,
+                 heads=L.spec.heads, head_dim=L.spec.head_dim,
+                 dtype=BF16 if L.spec.dtype == "bf16" else FP32)
+        assert hstu.mtgr_hstu_attn_workspace_size(p) <= hstu.MTGR_NOALLOC_SCRATCH_BYTES, name

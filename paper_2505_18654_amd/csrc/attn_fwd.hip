@@ -29,6 +29,12 @@
 #ifndef MTGR_FWD_SB
 #define MTGR_FWD_SB 4
 #endif
+#ifndef MTGR_FWD_SGB
+#define MTGR_FWD_SGB 0
+#endif
+#ifndef MTGR_FWD_SGB_DS
+#define MTGR_FWD_SGB_DS 2
+#endif
 
 namespace mtgr {
 
@@ -226,7 +232,20 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
                     nxt = __builtin_amdgcn_mfma_f32_32x32x16_bf16(op[m], qreg[kk], nxt, 0, 0, 0);
                 }
             }
-            if ((m + 1) % SB == 0) __builtin_amdgcn_sched_barrier(0);   // scheduling region
+            if constexpr (MTGR_FWD_SGB == 0) {
+                if ((m + 1) % SB == 0) __builtin_amdgcn_sched_barrier(0);   // scheduling region
+            }
+        }
+        if constexpr (MTGR_FWD_SGB > 0) {
+            // one scheduling region per half-step, laid out as NM groups of
+            // {1 MFMA, SGB VALU, SGB_DS LDS reads}
+#pragma unroll
+            for (int m = 0; m < NM; m++) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x002, MTGR_FWD_SGB, 0);
+                __builtin_amdgcn_sched_group_barrier(0x100, MTGR_FWD_SGB_DS, 0);
+            }
+            __builtin_amdgcn_sched_barrier(0);
         }
     };
     // Without a relative bias, masked scores are zeroed before the SiLU (silu(0) = 0 exactly),

@@ -21,7 +21,11 @@ struct Vec;   // 16-byte chunk of the storage type
 template <>
 struct Vec<true> {
     static constexpr int N = 8;
-    __device__ static uint4 raw(const void* base, long long idx) { return *(const uint4*)((const uint16_t*)base + idx); }
+    __device__ static uint4 raw(const void* base, long long idx) {
+        typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+        const u32x4 v = __builtin_nontemporal_load((const u32x4*)((const uint16_t*)base + idx));
+        return make_uint4(v.x, v.y, v.z, v.w);
+    }
     __device__ static void unpack(const uint4 u, float* out) {
         const uint32_t w[4] = {u.x, u.y, u.z, u.w};
 #pragma unroll
@@ -52,7 +56,11 @@ struct Vec<true> {
 template <>
 struct Vec<false> {
     static constexpr int N = 4;
-    __device__ static uint4 raw(const void* base, long long idx) { return *(const uint4*)((const float*)base + idx); }
+    __device__ static uint4 raw(const void* base, long long idx) {
+        typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+        const u32x4 v = __builtin_nontemporal_load((const u32x4*)((const float*)base + idx));
+        return make_uint4(v.x, v.y, v.z, v.w);
+    }
     __device__ static void unpack(const uint4 u, float* out) {
         out[0] = __uint_as_float(u.x); out[1] = __uint_as_float(u.y);
         out[2] = __uint_as_float(u.z); out[3] = __uint_as_float(u.w);
@@ -75,7 +83,10 @@ __device__ __forceinline__ void load_param(const float* p, int off, float* out, 
 }  // namespace
 
 // NCH = 16-byte chunks per lane (d <= 64 * NCH * N).
-template <bool BF16, int NCH, bool GATE>
+// FULL: every lane owns exactly NCH chunks (d = 64 NCH N), so no chunk guard is needed; the
+// guards otherwise put branches around the loads, and the counters of loads in flight are then
+// waited to zero at the joins, which serialises the prefetch.
+template <bool BF16, int NCH, bool GATE, bool FULL>
 __global__ __launch_bounds__(WAVES * 64) void gln_fwd_kernel(GlnArgs a) {
     using V = Vec<BF16>;
     constexpr int N = V::N;
@@ -93,7 +104,7 @@ __global__ __launch_bounds__(WAVES * 64) void gln_fwd_kernel(GlnArgs a) {
 #pragma unroll
         for (int c = 0; c < NCH; c++) {
             const int ch = lane + 64 * c;
-            if (ch < nch) {
+            if (FULL || ch < nch) {
                 V::load(a.x, t * a.ld_x + ch * N, xr[c]);
                 if (GATE) V::load(a.u, t * a.ld_u + ch * N, ur[c]);
             }
@@ -108,7 +119,7 @@ __global__ __launch_bounds__(WAVES * 64) void gln_fwd_kernel(GlnArgs a) {
         for (int c = 0; c < NCH; c++) {
 #pragma unroll
             for (int i = 0; i < N; i++) z[c][i] = GATE ? xr[c][i] * ur[c][i] : xr[c][i];
-            if (lane + 64 * c < nch) {
+            if (FULL || lane + 64 * c < nch) {
 #pragma unroll
                 for (int i = 0; i < N; i++) sum += z[c][i];
             }
@@ -119,7 +130,7 @@ __global__ __launch_bounds__(WAVES * 64) void gln_fwd_kernel(GlnArgs a) {
         float sq = 0.f;
 #pragma unroll
         for (int c = 0; c < NCH; c++) {
-            if (lane + 64 * c < nch) {
+            if (FULL || lane + 64 * c < nch) {
 #pragma unroll
                 for (int i = 0; i < N; i++) {
                     const float dz = z[c][i] - mean;
@@ -134,7 +145,7 @@ __global__ __launch_bounds__(WAVES * 64) void gln_fwd_kernel(GlnArgs a) {
 #pragma unroll
             for (int c = 0; c < NCH; c++) {
                 const int ch = lane + 64 * c;
-                if (ch < nch) {
+                if (FULL || ch < nch) {
                     load_param(a.gamma, g * d + ch * N, gam[c], N);
                     load_param(a.beta, g * d + ch * N, bet[c], N);
                 }
@@ -143,7 +154,7 @@ __global__ __launch_bounds__(WAVES * 64) void gln_fwd_kernel(GlnArgs a) {
 #pragma unroll
         for (int c = 0; c < NCH; c++) {
             const int ch = lane + 64 * c;
-            if (ch < nch) {
+            if (FULL || ch < nch) {
                 float y[N];
 #pragma unroll
                 for (int i = 0; i < N; i++) y[i] = gam[c][i] * ((z[c][i] - mean) * rstd) + bet[c][i];
@@ -170,7 +181,7 @@ __global__ __launch_bounds__(WAVES * 64) void gln_fwd_kernel(GlnArgs a) {
 template <int NCH>
 constexpr int bwd_real_waves() { return NCH >= 4 ? BWD_WAVES / 2 : BWD_WAVES; }
 
-template <bool BF16, int NCH, bool GATE, bool LDS_ACC>
+template <bool BF16, int NCH, bool GATE, bool LDS_ACC, bool FULL>
 __global__ __launch_bounds__(bwd_real_waves<NCH>() * 64) void gln_bwd_kernel(GlnArgs a, float* __restrict__ part,
                                                                               int tpw) {
     using V = Vec<BF16>;
@@ -184,6 +195,15 @@ __global__ __launch_bounds__(bwd_real_waves<NCH>() * 64) void gln_bwd_kernel(Gln
     float* slot = part + (long long)blockIdx.x * accn;
     float* acc = LDS_ACC ? sAcc : slot;
     for (int i = threadIdx.x; i < accn; i += RW * 64) acc[i] = 0.f;
+    // With the LDS accumulator, gamma [G][d] is staged in LDS behind it, so that reloading a
+    // wave's gamma rows on a group change is an LDS read: a global load there would be counted
+    // with the rows in flight, and the wait for it would drain the prefetch.
+    const float* gsrc = a.gamma;
+    if constexpr (LDS_ACC) {
+        float* sGam = sAcc + accn;
+        for (int i = threadIdx.x; i < a.G * d; i += RW * 64) sGam[i] = a.gamma[i];
+        gsrc = sGam;
+    }
     __syncthreads();
     const long long t0 = ((long long)blockIdx.x * BWD_WAVES + (long long)w * WPW) * tpw;
     const long long t1 = min(t0 + (long long)WPW * tpw, a.T);
@@ -195,7 +215,7 @@ __global__ __launch_bounds__(bwd_real_waves<NCH>() * 64) void gln_bwd_kernel(Gln
 #pragma unroll
         for (int c = 0; c < NCH; c++) {
             const int ch = lane + 64 * c;
-            if (ch < nch) {
+            if (FULL || ch < nch) {
 #pragma unroll
                 for (int i = 0; i < N; i++) {
                     atomicAdd(&acc[gcur * d + ch * N + i], pg[c][i]);
@@ -217,7 +237,7 @@ __global__ __launch_bounds__(bwd_real_waves<NCH>() * 64) void gln_bwd_kernel(Gln
 #pragma unroll
         for (int c = 0; c < NCH; c++) {
             const int ch = lane + 64 * c;
-            if (ch < nch) {
+            if (FULL || ch < nch) {
                 r.x[c] = V::raw(a.x, t * a.ld_x + ch * N);
                 r.y[c] = V::raw(a.dy, t * a.ld_y + ch * N);
                 if (GATE) r.u[c] = V::raw(a.u, t * a.ld_u + ch * N);
@@ -227,22 +247,13 @@ __global__ __launch_bounds__(bwd_real_waves<NCH>() * 64) void gln_bwd_kernel(Gln
         r.m = a.mean[t];
         r.r = a.rstd[t];
     };
+    // PFD + 1 row buffers used round robin, the loop unrolled by PFD + 1 so that every buffer
+    // index is a compile-time constant: no register of a load in flight is ever copied (a copy
+    // would wait for that load and serialise the prefetch).  Token t + PFD is requested into the
+    // buffer that token t - 1 used, before token t is processed.
     constexpr int PFD = NCH <= 2 ? 2 : NCH <= 4 ? 1 : 0;
-    Rows ring[PFD > 0 ? PFD : 1] = {};
-#pragma unroll
-    for (int k = 0; k < PFD; k++)
-        if (t0 + k < t1) fetch(t0 + k, ring[k]);
-    for (long long t = t0; t < t1; t++) {
-        Rows cur;
-        if constexpr (PFD == 0) {
-            cur = Rows{};
-            fetch(t, cur);
-        } else {
-            cur = ring[0];
-#pragma unroll
-            for (int k = 0; k + 1 < PFD; k++) ring[k] = ring[k + 1];
-            if (t + PFD < t1) fetch(t + PFD, ring[PFD - 1]);
-        }
+    constexpr int NB = PFD + 1;
+    auto process = [&](long long t, const Rows& cur) {
         float xx[NCH][N], uu[NCH][N], dy[NCH][N];
 #pragma unroll
         for (int c = 0; c < NCH; c++) {
@@ -260,7 +271,7 @@ __global__ __launch_bounds__(bwd_real_waves<NCH>() * 64) void gln_bwd_kernel(Gln
 #pragma unroll
             for (int c = 0; c < NCH; c++) {
                 const int ch = lane + 64 * c;
-                if (ch < nch) load_param(a.gamma, g * d + ch * N, gam[c], N);
+                if (FULL || ch < nch) load_param(gsrc, g * d + ch * N, gam[c], N);
 #pragma unroll
                 for (int i = 0; i < N; i++) {
                     pg[c][i] = 0.f;
@@ -272,7 +283,7 @@ __global__ __launch_bounds__(bwd_real_waves<NCH>() * 64) void gln_bwd_kernel(Gln
         float s1 = 0.f, s2 = 0.f;
 #pragma unroll
         for (int c = 0; c < NCH; c++) {
-            if (lane + 64 * c < nch) {
+            if (FULL || lane + 64 * c < nch) {
 #pragma unroll
                 for (int i = 0; i < N; i++) {
                     xh[c][i] = (xx[c][i] * uu[c][i] - mean) * rstd;
@@ -289,7 +300,7 @@ __global__ __launch_bounds__(bwd_real_waves<NCH>() * 64) void gln_bwd_kernel(Gln
 #pragma unroll
         for (int c = 0; c < NCH; c++) {
             const int ch = lane + 64 * c;
-            if (ch < nch) {
+            if (FULL || ch < nch) {
                 float dz[N];
 #pragma unroll
                 for (int i = 0; i < N; i++) dz[i] = rstd * (dy[c][i] * gam[c][i] - m1 - xh[c][i] * m2);
@@ -307,6 +318,28 @@ __global__ __launch_bounds__(bwd_real_waves<NCH>() * 64) void gln_bwd_kernel(Gln
                 }
             }
         }
+    };
+    if constexpr (PFD == 0) {
+        for (long long t = t0; t < t1; t++) {
+            Rows cur = {};
+            fetch(t, cur);
+            process(t, cur);
+        }
+    } else {
+        Rows buf[NB] = {};
+#pragma unroll
+        for (int k = 0; k < PFD; k++) fetch(min(t0 + k, t1 - 1), buf[k]);
+        for (long long tb = t0; tb < t1; tb += NB) {
+#pragma unroll
+            for (int j = 0; j < NB; j++) {
+                const long long t = tb + j;
+                if (t >= t1) break;
+                // unconditional (near the end the last token is fetched again), so that every
+                // iteration issues the same loads and the wait counts stay exact
+                fetch(min(t + PFD, t1 - 1), buf[(j + PFD) % NB]);
+                process(t, buf[j]);
+            }
+        }
     }
     flush();
     __syncthreads();
@@ -314,21 +347,35 @@ __global__ __launch_bounds__(bwd_real_waves<NCH>() * 64) void gln_bwd_kernel(Gln
         for (int i = threadIdx.x; i < accn; i += RW * 64) slot[i] = sAcc[i];
 }
 
-// dgamma/dbeta = sum over workgroup slots (fixed order).  Block = 64 columns x 4 row sets.
+// dgamma/dbeta = sum over workgroup slots (fixed order).  Block = 32 columns x 8 slot sets
+// (slot s goes to set s % 8); each thread keeps four partial sums so that four loads are in
+// flight, then the partials and the sets are added in a fixed order (deterministic).
+constexpr int RED_COLS = 32, RED_SETS = 8;
 __global__ __launch_bounds__(256) void gln_param_reduce_kernel(const float* __restrict__ part,
                                                                int nslots, int accn, int gd,
                                                                float* __restrict__ dgamma,
                                                                float* __restrict__ dbeta) {
-    __shared__ float sRed[4][64];
-    const int c = threadIdx.x & 63, r = threadIdx.x >> 6;
-    const int e = blockIdx.x * 64 + c;
-    float sum = 0.f;
-    if (e < accn)
-        for (int s = r; s < nslots; s += 4) sum += part[(long long)s * accn + e];
-    sRed[r][c] = sum;
+    __shared__ float sRed[RED_SETS][RED_COLS];
+    const int c = threadIdx.x % RED_COLS, r = threadIdx.x / RED_COLS;
+    const int e = blockIdx.x * RED_COLS + c;
+    float s4[4] = {0.f, 0.f, 0.f, 0.f};
+    if (e < accn) {
+        int s = r;
+#pragma unroll 1
+        for (; s + 3 * RED_SETS < nslots; s += 4 * RED_SETS) {
+#pragma unroll
+            for (int k = 0; k < 4; k++) s4[k] += part[(long long)(s + k * RED_SETS) * accn + e];
+        }
+#pragma unroll
+        for (int k = 0; k < 4; k++)
+            if (s + k * RED_SETS < nslots) s4[k] += part[(long long)(s + k * RED_SETS) * accn + e];
+    }
+    sRed[r][c] = (s4[0] + s4[1]) + (s4[2] + s4[3]);
     __syncthreads();
     if (r == 0 && e < accn) {
-        const float tot = ((sRed[0][c] + sRed[1][c]) + sRed[2][c]) + sRed[3][c];
+        float tot = 0.f;
+#pragma unroll
+        for (int k = 0; k < RED_SETS; k++) tot += sRed[k][c];
         if (e < gd) dgamma[e] = tot;
         else dbeta[e - gd] = tot;
     }
@@ -337,30 +384,39 @@ __global__ __launch_bounds__(256) void gln_param_reduce_kernel(const float* __re
 template <bool BF16, int NCH>
 static hipError_t gln_launch(const GlnArgs& a, bool bwd, hipStream_t s) {
     const bool gate = a.u != nullptr;
+    const bool full = a.d == 64 * NCH * Vec<BF16>::N;
     if (!bwd) {
         const long long waves = (a.T + TOKENS_PER_WAVE - 1) / TOKENS_PER_WAVE;
         const int blocks = (int)((waves + WAVES - 1) / WAVES);
-        if (gate) gln_fwd_kernel<BF16, NCH, true><<<blocks, WAVES * 64, 0, s>>>(a);
-        else gln_fwd_kernel<BF16, NCH, false><<<blocks, WAVES * 64, 0, s>>>(a);
+        if (full) {
+            if (gate) gln_fwd_kernel<BF16, NCH, true, true><<<blocks, WAVES * 64, 0, s>>>(a);
+            else gln_fwd_kernel<BF16, NCH, false, true><<<blocks, WAVES * 64, 0, s>>>(a);
+        } else {
+            if (gate) gln_fwd_kernel<BF16, NCH, true, false><<<blocks, WAVES * 64, 0, s>>>(a);
+            else gln_fwd_kernel<BF16, NCH, false, false><<<blocks, WAVES * 64, 0, s>>>(a);
+        }
         return hipGetLastError();
     }
     int nslots, tpw;
     gln_bwd_partition(a.T, &nslots, &tpw);
     const int accn = 2 * a.G * a.d;
     const bool lds = accn * (int)sizeof(float) <= GLN_LDS_ACC_BYTES;
-    const size_t shm = lds ? accn * sizeof(float) : 0;
+    const size_t shm = lds ? (accn + a.G * a.d) * sizeof(float) : 0;   // accumulator, then gamma
     float* part = a.workspace;
     constexpr int threads = bwd_real_waves<NCH>() * 64;
-    if (lds) {
-        if (gate) gln_bwd_kernel<BF16, NCH, true, true><<<nslots, threads, shm, s>>>(a, part, tpw);
-        else gln_bwd_kernel<BF16, NCH, false, true><<<nslots, threads, shm, s>>>(a, part, tpw);
+    if (lds && full) {
+        if (gate) gln_bwd_kernel<BF16, NCH, true, true, true><<<nslots, threads, shm, s>>>(a, part, tpw);
+        else gln_bwd_kernel<BF16, NCH, false, true, true><<<nslots, threads, shm, s>>>(a, part, tpw);
+    } else if (lds) {
+        if (gate) gln_bwd_kernel<BF16, NCH, true, true, false><<<nslots, threads, shm, s>>>(a, part, tpw);
+        else gln_bwd_kernel<BF16, NCH, false, true, false><<<nslots, threads, shm, s>>>(a, part, tpw);
     } else {
-        if (gate) gln_bwd_kernel<BF16, NCH, true, false><<<nslots, threads, 0, s>>>(a, part, tpw);
-        else gln_bwd_kernel<BF16, NCH, false, false><<<nslots, threads, 0, s>>>(a, part, tpw);
+        if (gate) gln_bwd_kernel<BF16, NCH, true, false, false><<<nslots, threads, 0, s>>>(a, part, tpw);
+        else gln_bwd_kernel<BF16, NCH, false, false, false><<<nslots, threads, 0, s>>>(a, part, tpw);
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    gln_param_reduce_kernel<<<(accn + 63) / 64, 256, 0, s>>>(part, nslots, accn, a.G * a.d, a.dgamma,
+    gln_param_reduce_kernel<<<(accn + RED_COLS - 1) / RED_COLS, 256, 0, s>>>(part, nslots, accn, a.G * a.d, a.dgamma,
                                                             a.dbeta);
     return hipGetLastError();
 }

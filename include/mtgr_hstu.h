@@ -175,6 +175,38 @@ mtgr_status_t mtgr_hstu_attn_fwd(const mtgr_hstu_problem_t* p, const int32_t* of
                                  const void* k, const void* v, const float* rab, void* out,
                                  void* workspace, size_t workspace_bytes, mtgr_stream_t stream);
 
+/* Serving with the user side cached across requests (user sample aggregation, Sec. 4.1, Eq. 3;
+ * its serving cost, Sec. 6.5).  Candidates see the static tokens, the real-time tokens earlier
+ * than themselves, and themselves only (Sec. 4.2), and no user-side token sees a candidate, so
+ * a user's user-side keys and values (U | S | R) can be held by the caller across requests and
+ * each request brings only its candidates.  For every user b and candidate i of the request:
+ *   out[i,h,:] = ( sum over cached tokens j of b with M_ij = 1 of p_ij vc[j,h,:]  +  p_ii v[i,h,:] )
+ * with p_ij = silu(alpha q_i.kc_j + rab[h, bucket(|ts_i - ts_c[j]|)]) / n_b,
+ *      p_ii = silu(alpha q_i.k_i + rab[h, 0]) / n_b,  n_b = cached tokens of b + candidates of b
+ * (every token of the user, as in mtgr_hstu_attn_fwd), M_ij the mask of Sec. 4.2 from the
+ * cached tokens' segments (in the cache plan) and timestamps.  This equals the candidate rows
+ * of mtgr_hstu_attn_fwd on the concatenated sequence [cached | candidates] up to the order of
+ * the float sums.  (The user side of the first layer depends only on the user; at deeper layers
+ * it also depends on n_b, so a cache serves requests with the same candidate count.)
+ *   p: the request: B users, T = all candidates, max_seqlen >= candidates of any user; its
+ *     tokens should be candidates (seg = MTGR_SEG_CAND); q, k, v, out [T, H, dh] bf16.
+ *     head_dim 32, 64 or 128 (bf16 matrix cores; other shapes MTGR_ERROR_UNSUPPORTED).
+ *     Only MTGR_ATTN_PLANNED may be set (the request's plan in workspace).
+ *   pc: the cache: the same B, num_heads, head_dim and dtype; total_tokens, max_seqlen of the
+ *     cached tokens; ld_k / ld_v are the token strides of kc / vc.
+ *   offsets_c [B+1], ts_c [Tc] int32; kc, vc [Tc, H, dh] bf16 (device).
+ *   cache_plan: a workspace of at least mtgr_hstu_attn_workspace_size(pc, 0) bytes that
+ *     mtgr_hstu_attn_plan(pc, offsets_c, seg_c, ts_c, ...) filled (once per cache contents).
+ *   workspace: at least mtgr_hstu_attn_workspace_size(p, 0) bytes (the request's plan). */
+mtgr_status_t mtgr_hstu_attn_fwd_cached(const mtgr_hstu_problem_t* p, const int32_t* offsets,
+                                        const int8_t* seg, const int32_t* ts, const void* q,
+                                        const void* k, const void* v, const float* rab, void* out,
+                                        const mtgr_hstu_problem_t* pc, const int32_t* offsets_c,
+                                        const int32_t* ts_c, const void* kc, const void* vc,
+                                        const void* cache_plan, size_t cache_plan_bytes,
+                                        void* workspace, size_t workspace_bytes,
+                                        mtgr_stream_t stream);
+
 /* Bytes of the per-GPU device array that holds the plan of mtgr_hstu_attn_fwd_noalloc. */
 #define MTGR_NOALLOC_SCRATCH_BYTES (16u * 1024u * 1024u)
 

@@ -324,6 +324,73 @@ mtgr_status_t mtgr_hstu_attn_fwd_noalloc(const mtgr_hstu_problem_t* p, const int
     return attn_fwd_checked(p, offsets, seg, ts, q, k, v, rab, out, ws, s);
 }
 
+mtgr_status_t mtgr_hstu_attn_fwd_cached(const mtgr_hstu_problem_t* p, const int32_t* offsets,
+                                        const int8_t* seg, const int32_t* ts, const void* q, const void* k,
+                                        const void* v, const float* rab, void* out,
+                                        const mtgr_hstu_problem_t* pc, const int32_t* offsets_c,
+                                        const int32_t* ts_c, const void* kc, const void* vc,
+                                        const void* cache_plan, size_t cache_plan_bytes, void* workspace,
+                                        size_t workspace_bytes, mtgr_stream_t stream) {
+    mtgr_status_t st = check_attn_common(p, offsets, seg, ts, rab, workspace, workspace_bytes);
+    if (st != MTGR_SUCCESS) return st;
+    if (!pc) return fail(MTGR_ERROR_NULL_POINTER, "cache problem is NULL");
+    st = check_problem(pc);
+    if (st != MTGR_SUCCESS) return st;
+    if (pc->num_users != p->num_users || pc->num_heads != p->num_heads || pc->head_dim != p->head_dim ||
+        pc->dtype != p->dtype)
+        return fail(MTGR_ERROR_INVALID_ARGUMENT,
+                    "cache and request differ in num_users, num_heads, head_dim or dtype");
+    if (vec_path(p))
+        return fail(MTGR_ERROR_UNSUPPORTED, "the cached forward runs on the bf16 matrix cores (head_dim 32..128)");
+    if (p->flags & ~MTGR_ATTN_PLANNED)
+        return fail(MTGR_ERROR_INVALID_ARGUMENT, "only MTGR_ATTN_PLANNED applies to the cached forward");
+    if (p->num_users == 0) return ok();
+    if (!offsets_c) return fail(MTGR_ERROR_NULL_POINTER, "offsets_c is NULL");
+    if (((uintptr_t)offsets_c & 3u) != 0) return fail(MTGR_ERROR_INVALID_ARGUMENT, "offsets_c is not 4-byte aligned");
+    const AttnLayout Lc = attn_layout(pc);
+    if (pc->total_tokens > 0) {
+        if (!ts_c) return fail(MTGR_ERROR_NULL_POINTER, "ts_c is NULL");
+        if (((uintptr_t)ts_c & 3u) != 0) return fail(MTGR_ERROR_INVALID_ARGUMENT, "ts_c is not 4-byte aligned");
+        REQUIRE_PTR(kc, "kc");
+        REQUIRE_PTR(vc, "vc");
+        if (!cache_plan) return fail(MTGR_ERROR_NULL_POINTER, "cache_plan is NULL");
+        if (((uintptr_t)cache_plan & 255u) != 0)
+            return fail(MTGR_ERROR_INVALID_ARGUMENT, "cache_plan is not 256-byte aligned");
+        if (cache_plan_bytes < Lc.total)
+            return fail(MTGR_ERROR_WORKSPACE_TOO_SMALL, "cache_plan %zu bytes, need %zu", cache_plan_bytes, Lc.total);
+    }
+    if (p->total_tokens == 0) return ok();
+    REQUIRE_PTR(q, "q");
+    REQUIRE_PTR(k, "k");
+    REQUIRE_PTR(v, "v");
+    REQUIRE_PTR(out, "out");
+    hipStream_t s = (hipStream_t)stream;
+    const AttnLayout L = attn_layout(p);
+    if (!(p->flags & MTGR_ATTN_PLANNED)) {
+        st = schedule(p, L, offsets, seg, ts, workspace, s);
+        if (st != MTGR_SUCCESS) return st;
+    }
+    mtgr::AttnArgs a = make_args(p, L, offsets, seg, ts, workspace);
+    a.q = q;
+    a.k = k;
+    a.v = v;
+    a.rab = rab;
+    a.out = out;
+    a.kc = kc;
+    a.vc = vc;
+    a.ld_kc = pc->ld_k;
+    a.ld_vc = pc->ld_v;
+    a.offsets_k = offsets_c;
+    a.ts_k = ts_c;
+    const char* cp = (const char*)cache_plan;
+    a.tok_code_k = pc->total_tokens > 0 ? (const int*)(cp + Lc.off_code) : nullptr;
+    a.summ_k = pc->total_tokens > 0 ? (const int4*)(cp + Lc.off_summ) : nullptr;
+    a.ntile_k = pc->total_tokens > 0 ? Lc.ntile : 0;
+    hipError_t e = mtgr::launch_attn_fwd_cached_bf16(a, p->head_dim, (int)L.slots, s);
+    if (e != hipSuccess) return device_fail(e, "cached attention forward");
+    return ok();
+}
+
 mtgr_status_t mtgr_hstu_attn_bwd(const mtgr_hstu_problem_t* p, const int32_t* offsets,
                                  const int8_t* seg, const int32_t* ts, const void* q, const void* k,
                                  const void* v, const float* rab, const void* dout, void* dq,

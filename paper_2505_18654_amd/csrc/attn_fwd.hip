@@ -47,7 +47,12 @@ __device__ __forceinline__ uint4 ldg16(const uint16_t* p) { return *(const uint4
 
 }  // namespace
 
-template <int DH, bool RAB>
+// CACHED: the query rows are a request's candidates (a.q, a.offsets, a.seg, a.ts, a.summ) and the
+// keys are the users' cached user-side tokens (a.kc, a.vc, a.offsets_k, a.ts_k, a.tok_code_k,
+// a.summ_k).  Candidates see only user-side keys and themselves (Sec. 4.2), so no key tile holds
+// a candidate; each candidate's own term p_ii v_i is added after the tiles, and n_b counts both
+// sides.
+template <int DH, bool RAB, bool CACHED>
 __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
     constexpr int CPR = DH / 8;          // 16-byte chunks per row
     constexpr int KSTEPS = DH / 16;      // k-steps of S^T = K Q^T per 32-key half
@@ -70,15 +75,22 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
     const int2 item = a.items[blockIdx.x];
     if (item.x < 0) return;
     const int b = item.x, qt = item.y >> 8, h = item.y & 255;
-    const int ob = a.offsets[b], nb = a.offsets[b + 1] - ob;
+    const int ob = a.offsets[b], nb = a.offsets[b + 1] - ob;        // query rows of the user
+    int okb = ob, nkb = nb;                                          // key rows of the user
+    if constexpr (CACHED) {
+        okb = a.offsets_k[b];
+        nkb = a.offsets_k[b + 1] - okb;
+    }
     const int q0 = qt * BM;
-    const int ntk = (nb + BN - 1) / BN;
-    const float inv_n = 1.0f / (float)nb;
+    const int ntq = (nb + BN - 1) / BN;
+    const int ntk = (nkb + BN - 1) / BN;
+    const float inv_n = 1.0f / (float)(CACHED ? nb + nkb : nb);
     const float alpha = a.alpha;
     const int4* summ = a.summ + (long long)b * a.ntile;
+    const int4* summk = CACHED ? a.summ_k + (long long)b * a.ntile_k : summ;
 
     TileSummary sq = load_summary(summ, 2 * qt);
-    if (2 * qt + 1 < ntk) sq = combine(sq, load_summary(summ, 2 * qt + 1));
+    if (2 * qt + 1 < ntq) sq = combine(sq, load_summary(summ, 2 * qt + 1));
     if (a.cand_rows && !(sq.flags & TS_ANY_CAND)) return;   // no candidate row to form
 
     const int col = lane & 31, hh = lane >> 5;
@@ -89,8 +101,11 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
         qcode = token_code(a.seg[ob + qi]);
         qts = a.ts[ob + qi];
     }
-    const uint16_t* Kb = (const uint16_t*)a.k + (long long)ob * a.ld_k;
-    const uint16_t* Vb = (const uint16_t*)a.v + (long long)ob * a.ld_v;
+    const long long ldk = CACHED ? a.ld_kc : a.ld_k, ldv = CACHED ? a.ld_vc : a.ld_v;
+    const uint16_t* Kb = (const uint16_t*)(CACHED ? a.kc : a.k) + (long long)okb * ldk;
+    const uint16_t* Vb = (const uint16_t*)(CACHED ? a.vc : a.v) + (long long)okb * ldv;
+    const int* kts_g = (CACHED ? a.ts_k : a.ts) + okb;
+    const int* kcode_g = (CACHED ? a.tok_code_k : a.tok_code) + okb;
     const uint16_t* Q = (const uint16_t*)a.q;
     bf16x8 qreg[KSTEPS];
 #pragma unroll
@@ -119,15 +134,15 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
         for (int r = 0; r < 16; r++) oacc[i][r] = 0.f;
 
     auto class_of = [&](int t) {
-        const bool overlap = (t * BN < q0 + BM) && (q0 < t * BN + BN);
-        return tile_class(sq, load_summary(summ, t), overlap);
+        const bool overlap = !CACHED && (t * BN < q0 + BM) && (q0 < t * BN + BN);
+        return tile_class(sq, load_summary(summk, t), overlap);
     };
     TileWalker<decltype(class_of)> walk(class_of, ntk);
 
-    auto issue_k = [&](int t, int buf) { tile_dma<DH>(sK[buf], Kb, a.ld_k, t * BN, nb, h * DH, tid); };
+    auto issue_k = [&](int t, int buf) { tile_dma<DH>(sK[buf], Kb, ldk, t * BN, nkb, h * DH, tid); };
     auto issue_v = [&](int t, int buf) {
-        tile_dma<DH>(sV[buf], Vb, a.ld_v, t * BN, nb, h * DH, tid);
-        codes_dma(sVts[buf], sVcode[buf], a.ts + ob, a.tok_code + ob, t * BN, nb, tid);
+        tile_dma<DH>(sV[buf], Vb, ldv, t * BN, nkb, h * DH, tid);
+        codes_dma(sVts[buf], sVcode[buf], kts_g, kcode_g, t * BN, nkb, tid);
     };
 
     // p' for the accumulator value sv of key kl (relative to the tile):
@@ -286,11 +301,12 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
             using CQ = std::integral_constant<int, P ^ 1>;
             // top: V(t_i) (and its codes) landed; K(t_{i+1}) may still be in flight
             if (t1 < ntk) wait_vmcnt<NK>(); else wait_vmem();
-            if (tid < BN && t0 * BN + tid >= nb) sVcode[P][tid] = 0;
+            if (tid < BN && t0 * BN + tid >= nkb) sVcode[P][tid] = 0;
             lds_barrier();
             if (t1 < ntk) issue_v(t1, P ^ 1);                      // V(t_{i-1})'s buffer
             const bool partial = cls0 == TILE_PARTIAL;
-            const int qrel = qi - t0 * BN - 4 * hh;
+            // (cached: no key is the query itself, so the diagonal test never holds)
+            const int qrel = CACHED ? -(1 << 20) : qi - t0 * BN - 4 * hh;
             uint32_t pkA[4], pkB[4];
             // half 0 of t_i; next S = half 1 of t_i (same K buffer)
             if (!RAB && partial) premask(sA, C0{}, sVts[P], sVcode[P], qrel);
@@ -332,6 +348,49 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
         while (tile(C0{}) && tile(C1{})) {
         }
         __syncthreads();                                         // K buffers are reused below
+    }
+
+    if constexpr (CACHED) {
+        // The candidate's own term: p_ii v_i with s_ii = q_i . k_i (bias bucket 0), p rounded
+        // to bf16 as the tiles round P.  Lane (col, hh) holds features 16 kk + 8 hh .. + 7 of q
+        // in qreg, and O^T rows 32 db + 8 g + 4 hh + 0..3.
+        float dot = 0.f;
+        if (qvalid) {
+            const uint16_t* Kq = (const uint16_t*)a.k + (long long)(ob + qi) * a.ld_k + h * DH + 8 * hh;
+#pragma unroll
+            for (int kk = 0; kk < KSTEPS; kk++) {
+                const uint4 kv = ldg16(Kq + 16 * kk);
+                const uint4 qv = __builtin_bit_cast(uint4, qreg[kk]);
+                const uint32_t kw[4] = {kv.x, kv.y, kv.z, kv.w}, qw[4] = {qv.x, qv.y, qv.z, qv.w};
+#pragma unroll
+                for (int i = 0; i < 4; i++) {
+                    dot = __builtin_fmaf(__uint_as_float(qw[i] << 16), __uint_as_float(kw[i] << 16), dot);
+                    dot = __builtin_fmaf(__uint_as_float(qw[i] & 0xffff0000u), __uint_as_float(kw[i] & 0xffff0000u), dot);
+                }
+            }
+        }
+        dot += __shfl_xor(dot, 32, 64);   // the other 8 features of every k-step
+        float p;
+        if (RAB) {
+            float sg;
+            p = silu_sig(dot * alpha + sRab[0], sg);
+        } else {
+            p = dot * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(dot * c_exp));
+        }
+        p = __uint_as_float(f32_to_bf16_bits(p) << 16);
+        if (qvalid) {
+            const uint16_t* Vq = (const uint16_t*)a.v + (long long)(ob + qi) * a.ld_v + h * DH + 4 * hh;
+#pragma unroll
+            for (int db = 0; db < DBLK; db++)
+#pragma unroll
+                for (int g = 0; g < 4; g++) {
+                    const uint2 vv = *(const uint2*)(Vq + 32 * db + 8 * g);
+                    oacc[db][4 * g + 0] = __builtin_fmaf(p, __uint_as_float(vv.x << 16), oacc[db][4 * g + 0]);
+                    oacc[db][4 * g + 1] = __builtin_fmaf(p, __uint_as_float(vv.x & 0xffff0000u), oacc[db][4 * g + 1]);
+                    oacc[db][4 * g + 2] = __builtin_fmaf(p, __uint_as_float(vv.y << 16), oacc[db][4 * g + 2]);
+                    oacc[db][4 * g + 3] = __builtin_fmaf(p, __uint_as_float(vv.y & 0xffff0000u), oacc[db][4 * g + 3]);
+                }
+        }
     }
 
     // Output: O^T accumulators scaled by alpha / n_b (1 / n_b with a relative bias) -> bf16
@@ -445,12 +504,12 @@ __global__ __launch_bounds__(256) void attn_fwd_vec_kernel(AttnArgs a) {
     }
 }
 
-template <int DH>
+template <int DH, bool CACHED>
 static hipError_t fwd_bf16_dh(const AttnArgs& a, int slots, hipStream_t s) {
     if (a.rab)
-        attn_fwd_bf16_kernel<DH, true><<<slots, 256, 0, s>>>(a);
+        attn_fwd_bf16_kernel<DH, true, CACHED><<<slots, 256, 0, s>>>(a);
     else
-        attn_fwd_bf16_kernel<DH, false><<<slots, 256, 0, s>>>(a);
+        attn_fwd_bf16_kernel<DH, false, CACHED><<<slots, 256, 0, s>>>(a);
     return hipGetLastError();
 }
 
@@ -466,9 +525,18 @@ static hipError_t fwd_vec_dh(const AttnArgs& a, int slots, hipStream_t s) {
 hipError_t launch_attn_fwd_bf16(const AttnArgs& a, int head_dim, int slots, hipStream_t s) {
     switch (head_dim) {
         case 16: return fwd_vec_dh<16, uint16_t>(a, slots, s);
-        case 32: return fwd_bf16_dh<32>(a, slots, s);
-        case 64: return fwd_bf16_dh<64>(a, slots, s);
-        case 128: return fwd_bf16_dh<128>(a, slots, s);
+        case 32: return fwd_bf16_dh<32, false>(a, slots, s);
+        case 64: return fwd_bf16_dh<64, false>(a, slots, s);
+        case 128: return fwd_bf16_dh<128, false>(a, slots, s);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+hipError_t launch_attn_fwd_cached_bf16(const AttnArgs& a, int head_dim, int slots, hipStream_t s) {
+    switch (head_dim) {
+        case 32: return fwd_bf16_dh<32, true>(a, slots, s);
+        case 64: return fwd_bf16_dh<64, true>(a, slots, s);
+        case 128: return fwd_bf16_dh<128, true>(a, slots, s);
         default: return hipErrorInvalidValue;
     }
 }

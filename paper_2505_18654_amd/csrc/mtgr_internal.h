@@ -33,6 +33,16 @@ struct AttnArgs {
     float alpha;
     int nbuckets;
     int cand_rows;            // forward: write candidate rows only
+    // Cached forward (the query side above holds a request's candidates): the key side is a
+    // caller-held cache of the users' user-side tokens, with its own layout and plan.
+    const void* kc;
+    const void* vc;
+    long long ld_kc, ld_vc;
+    const int* offsets_k;     // [B+1] cache offsets
+    const int* ts_k;          // [Tc] cache timestamps
+    const int* tok_code_k;    // [Tc] cache token codes (from the cache's plan)
+    const int4* summ_k;       // [B][ntile_k] cache tile summaries (from the cache's plan)
+    int ntile_k;
 };
 
 // Number of physical work-list slots for tiles of `bm` rows (see build_schedule).
@@ -46,6 +56,8 @@ hipError_t launch_build_schedule(const int* offsets, int num_users, int heads, i
 hipError_t launch_fill_f32(float* p, long long n, float value, hipStream_t s);
 
 hipError_t launch_attn_fwd_bf16(const AttnArgs& a, int head_dim, int slots, hipStream_t s);
+// Candidates of a request against the users' cached user-side keys (bf16, head_dim 32..128).
+hipError_t launch_attn_fwd_cached_bf16(const AttnArgs& a, int head_dim, int slots, hipStream_t s);
 hipError_t launch_attn_fwd_f32(const AttnArgs& a, int head_dim, int slots, hipStream_t s);
 // Which backward kernels run (bf16).
 struct BwdPlan {

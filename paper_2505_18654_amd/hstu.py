@@ -40,7 +40,7 @@ MTGR_EMB_STATE_NEXT_ROW, MTGR_EMB_STATE_FREE_TOP, MTGR_EMB_STATE_NUM_KEYS, MTGR_
 
 EXPORTED = (
     "mtgr_hstu_attn_workspace_size", "mtgr_hstu_attn_plan", "mtgr_hstu_attn_fwd", "mtgr_hstu_attn_bwd",
-    "mtgr_hstu_attn_fwd_noalloc",
+    "mtgr_hstu_attn_fwd_noalloc", "mtgr_hstu_attn_fwd_cached",
     "mtgr_group_layernorm_workspace_size", "mtgr_group_layernorm_fwd", "mtgr_group_layernorm_bwd",
     "mtgr_bias_silu_fwd", "mtgr_bias_silu_bwd",
     "mtgr_debug_validate_inputs", "mtgr_status_string", "mtgr_last_error_message", "mtgr_version",
@@ -106,6 +106,8 @@ def lib() -> ctypes.CDLL:
         L.mtgr_hstu_attn_plan.argtypes = [P, vp, vp, vp, vp, sz, vp]
         L.mtgr_hstu_attn_fwd.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
         L.mtgr_hstu_attn_fwd_noalloc.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+        L.mtgr_hstu_attn_fwd_cached.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, P, vp, vp, vp, vp, vp, sz,
+                                                vp, sz, vp]
         L.mtgr_hstu_attn_bwd.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
         L.mtgr_group_layernorm_workspace_size.argtypes = [G, ctypes.c_int, ctypes.POINTER(sz)]
         L.mtgr_group_layernorm_fwd.argtypes = [G, vp, vp, vp, vp, vp, vp, vp, vp, vp]
@@ -193,6 +195,15 @@ def mtgr_hstu_attn_fwd(problem, offsets, seg, ts, q, k, v, rab, out, workspace, 
     _check(lib().mtgr_hstu_attn_fwd(ctypes.byref(problem), _ptr(offsets), _ptr(seg), _ptr(ts),
                                     _ptr(q), _ptr(k), _ptr(v), _ptr(rab), _ptr(out), _ptr(workspace),
                                     int(workspace_bytes), _stream(stream)))
+
+
+def mtgr_hstu_attn_fwd_cached(problem, offsets, seg, ts, q, k, v, rab, out, cache_problem, offsets_c, ts_c,
+                              kc, vc, cache_plan, cache_plan_bytes, workspace, workspace_bytes,
+                              stream=None) -> None:
+    _check(lib().mtgr_hstu_attn_fwd_cached(
+        ctypes.byref(problem), _ptr(offsets), _ptr(seg), _ptr(ts), _ptr(q), _ptr(k), _ptr(v), _ptr(rab),
+        _ptr(out), None if cache_problem is None else ctypes.byref(cache_problem), _ptr(offsets_c), _ptr(ts_c), _ptr(kc), _ptr(vc),
+        _ptr(cache_plan), int(cache_plan_bytes), _ptr(workspace), int(workspace_bytes), _stream(stream)))
 
 
 def mtgr_hstu_attn_fwd_noalloc(problem, offsets, seg, ts, q, k, v, rab, out, stream=None) -> None:

@@ -116,6 +116,38 @@ def attn_fwd(q, k, v, jag: Jagged, rab=None, alpha: float = 1.0, out=None, works
     return out
 
 
+@dataclass
+class UserCache:
+    """The user-side tokens (U | S | R) of a batch of users held across serving requests: their
+    layout, this layer's keys and values [Tc, H, dh], and the cache's plan (tile summaries and
+    token codes, built once by user_cache())."""
+    jag: Jagged
+    k: torch.Tensor
+    v: torch.Tensor
+    plan: torch.Tensor
+
+
+def user_cache(k, v, jag: Jagged) -> UserCache:
+    """Plans a user-side cache (mtgr_hstu_attn_plan on its layout) for attn_fwd_cached."""
+    return UserCache(jag, k, v, attn_plan(k, jag))
+
+
+def attn_fwd_cached(q, k, v, jag: Jagged, cache: UserCache, rab=None, alpha: float = 1.0, out=None,
+                    workspace=None, planned: bool = False):
+    """Candidate rows of a request (q, k, v, jag: the candidates) against the users' cached
+    user-side keys and values (mtgr_hstu_attn_fwd_cached).  Returns out [Tq, H, dh]."""
+    if out is None:
+        out = torch.empty_like(q, memory_format=torch.contiguous_format)
+    p = attn_problem(jag, q, k, v, out, rab, alpha, hstu.MTGR_ATTN_PLANNED if planned else 0)
+    pc = attn_problem(cache.jag, cache.k, cache.k, cache.v, cache.k)
+    if workspace is None:
+        workspace = workspace_for(p, q.device)
+    hstu.mtgr_hstu_attn_fwd_cached(p, jag.offsets, jag.seg, jag.ts, q, k, v, rab, out, pc, cache.jag.offsets,
+                                   cache.jag.ts, cache.k, cache.v, cache.plan, cache.plan.numel(), workspace,
+                                   workspace.numel())
+    return out
+
+
 def attn_bwd(q, k, v, dout, jag: Jagged, rab=None, alpha: float = 1.0, need_drab: bool = True,
              grads=None, workspace=None, planned: bool = False, parts: str = "all"):
     """Backward of Eq. 5: returns (dq, dk, dv, drab-or-None).

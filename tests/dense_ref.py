@@ -93,20 +93,26 @@ def dense_gln(x, u, gid, gamma, beta, eps=1e-5):
     return zn * gamma[g] + beta[g]
 
 
+def bf16_half_ulp(x):
+    """Half the spacing of bf16 numbers (8 significant bits) at |x|: the largest rounding error
+    of x, 2^(e - 9) for |x| in [2^(e-1), 2^e); 0 at 0."""
+    a = np.abs(x)
+    return np.where(a > 0, np.ldexp(1.0, np.frexp(a)[1] - 9), 0.0)
+
+
 def operand_rounding_bounds(offsets, seg, ts, q, k, v, dout, rab=None, alpha=1.0):
-    """Per-element bound of the error that rounding the MFMA operands P and dS to bf16 (half
-    an ulp, 2^-9 relative, round to nearest) adds to the attention outputs, for inputs whose
-    products cancel (e.g. activations with a non-zero mean): each output element is a sum of
-    terms, and rounding each P or dS factor perturbs the sum by at most 2^-9 times the sum
-    of the terms' magnitudes,
-        o_i: 2^-9 sum_j |p_ij| |v_j|        dv_j: 2^-9 sum_i |p_ij| |dout_i|
-        dq_i: 2^-9 alpha sum_j |dS_ij| |k_j|   dk_j: 2^-9 alpha sum_i |dS_ij| |q_i|
-    (p, dS with their 1/n_b, as in Eq. 5 and its chain rule).  numpy fp64 [T, H, dh] in,
+    """Per-element bound of the error that rounding the MFMA operands P and dS to bf16 (round to
+    nearest: at most half an ulp of each value, h(x)) adds to the attention outputs, for inputs
+    whose sums cancel (activations with a non-zero mean) or hold a single term (a candidate
+    that sees only itself): rounding every P or dS factor moves a sum by at most
+        o_i: sum_j h(p_ij) |v_j|           dv_j: sum_i h(p_ij) |dout_i|
+        dq_i: alpha sum_j h(dS_ij) |k_j|    dk_j: alpha sum_i h(dS_ij) |q_i|
+    with p, dS rounded before their factor 1/n_b, as the kernels do (alpha = 1: p = silu(s)).
+    numpy fp64 [T, H, dh] in,
     dict of [T, H, dh] bounds out; dense per user (small batches only)."""
     offsets = np.asarray(offsets)
     q, k, v, dout = (np.asarray(x, np.float64) for x in (q, k, v, dout))
     out = {name: np.zeros_like(q) for name in ("o", "dq", "dk", "dv")}
-    u = 2.0 ** -9
     for b in range(len(offsets) - 1):
         s0, s1 = int(offsets[b]), int(offsets[b + 1])
         n = s1 - s0
@@ -123,10 +129,12 @@ def operand_rounding_bounds(offsets, seg, ts, q, k, v, dout, rab=None, alpha=1.0
                 bk = bucket_torch(torch.from_numpy(gap)).clamp(max=rab.shape[1] - 1).numpy()
                 S = S + np.asarray(rab)[h][bk]
             sg = 1.0 / (1.0 + np.exp(-S))
-            P = np.where(M, S * sg, 0.0) / n
-            dS = np.where(M, (G @ V.T) * sg * (1.0 + S * (1.0 - sg)), 0.0) / n
-            out["o"][s0:s1, h] = u * np.abs(P) @ np.abs(V)
-            out["dv"][s0:s1, h] = u * np.abs(P).T @ np.abs(G)
-            out["dq"][s0:s1, h] = u * abs(alpha) * np.abs(dS) @ np.abs(K)
-            out["dk"][s0:s1, h] = u * abs(alpha) * np.abs(dS).T @ np.abs(Q)
+            # the kernels round p and dS before the factor 1/n_b (applied once per output)
+            P = np.where(M, S * sg, 0.0)
+            dS = np.where(M, (G @ V.T) * sg * (1.0 + S * (1.0 - sg)), 0.0)
+            hP, hdS = bf16_half_ulp(P) / n, bf16_half_ulp(dS) / n
+            out["o"][s0:s1, h] = hP @ np.abs(V)
+            out["dv"][s0:s1, h] = hP.T @ np.abs(G)
+            out["dq"][s0:s1, h] = abs(alpha) * hdS @ np.abs(K)
+            out["dk"][s0:s1, h] = abs(alpha) * hdS.T @ np.abs(Q)
     return out

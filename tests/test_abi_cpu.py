@@ -400,3 +400,46 @@ def test_noalloc_scratch_covers_the_workloads():
                  heads=L.spec.heads, head_dim=L.spec.head_dim,
                  dtype=BF16 if L.spec.dtype == "bf16" else FP32)
         assert hstu.mtgr_hstu_attn_workspace_size(p) <= hstu.MTGR_NOALLOC_SCRATCH_BYTES, name
+
+
+def cached(p, pc, **over):
+    args = dict(offsets=FAKE, seg=FAKE, ts=FAKE, q=FAKE, k=FAKE, v=FAKE, rab=None, out=FAKE, offsets_c=FAKE,
+                ts_c=FAKE, kc=FAKE, vc=FAKE, cache_plan=FAKE, cache_plan_bytes=1 << 30, workspace=FAKE,
+                workspace_bytes=1 << 30)
+    args.update(over)
+    hstu.mtgr_hstu_attn_fwd_cached(p, args["offsets"], args["seg"], args["ts"], args["q"], args["k"], args["v"],
+                                   args["rab"], args["out"], pc, args["offsets_c"], args["ts_c"], args["kc"],
+                                   args["vc"], args["cache_plan"], args["cache_plan_bytes"], args["workspace"],
+                                   args["workspace_bytes"], 0)
+
+
+@pytest.mark.parametrize("request_kw,cache_kw,over,status", [
+    (dict(), dict(heads=4), {}, hstu.MTGR_ERROR_INVALID_ARGUMENT),          # heads differ
+    (dict(), dict(num_users=5), {}, hstu.MTGR_ERROR_INVALID_ARGUMENT),      # users differ
+    (dict(dtype=FP32), dict(dtype=FP32), {}, hstu.MTGR_ERROR_UNSUPPORTED),  # matrix cores only
+    (dict(head_dim=16), dict(head_dim=16), {}, hstu.MTGR_ERROR_UNSUPPORTED),
+    (dict(), dict(), dict(kc=None), hstu.MTGR_ERROR_NULL_POINTER),
+    (dict(), dict(), dict(offsets_c=None), hstu.MTGR_ERROR_NULL_POINTER),
+    (dict(), dict(), dict(cache_plan=FAKE + 16), hstu.MTGR_ERROR_INVALID_ARGUMENT),
+    (dict(), dict(), dict(cache_plan_bytes=256), hstu.MTGR_ERROR_WORKSPACE_TOO_SMALL),
+])
+def test_cached_forward_validation(request_kw, cache_kw, over, status):
+    """Host-side checks of the cached forward: request and cache must agree in users, heads,
+    head_dim and dtype; the matrix-core shapes only; the cache's plan must be large enough."""
+    p = prob(**request_kw)
+    pc = prob(**dict(dict(total_tokens=300, max_seqlen=120), **cache_kw))
+    with pytest.raises(hstu.MtgrError) as e:
+        cached(p, pc, **over)
+    assert e.value.status == status
+
+
+def test_cached_forward_flags():
+    p = prob()
+    p.flags = hstu.MTGR_FWD_CAND_ROWS
+    with pytest.raises(hstu.MtgrError) as e:
+        cached(p, prob())
+    assert e.value.status == hstu.MTGR_ERROR_INVALID_ARGUMENT
+    with pytest.raises(hstu.MtgrError) as e:
+        hstu.mtgr_hstu_attn_fwd_cached(prob(), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE, None, FAKE, FAKE,
+                                       FAKE, FAKE, FAKE, 1 << 30, FAKE, 1 << 30, 0)
+    assert e.value.status == hstu.MTGR_ERROR_NULL_POINTER

@@ -164,46 +164,65 @@ def _silu(z):
     return z / (1.0 + np.exp(-z))
 
 
-def layer_fwd(offsets, seg, ts, x, params, heads: int, rab=None, alpha: float = 1.0, eps: float = 1e-5):
-    """One encoder layer forward.  x [T, d].  Returns (x_out, cache)."""
+def _keep(x):
+    return x
+
+
+def layer_fwd(offsets, seg, ts, x, params, heads: int, rab=None, alpha: float = 1.0, eps: float = 1e-5,
+              store=_keep):
+    """One encoder layer forward.  x [T, d].  Returns (x_out, cache).
+
+    `store` is applied to every intermediate that the layer keeps in memory between its steps
+    (the identity by default).  Training runs in bf16 mixed precision (Sec. 5, other
+    optimisations), so passing a rounding to bf16 gives the exact layer evaluated with
+    bf16-stored intermediates: each step's input is the stored value, each step computes
+    exactly.  The bias is added to the unrounded product, and the pre-activation kept for the
+    backward is the stored product plus the bias."""
     x = _f64(x)
     T, d = x.shape
     dh = d // heads
     P = {k: _f64(v) for k, v in params.items()}
     xt, m0, r0 = gln_fwd(x, None, seg, P["gamma_in"], P["beta_in"], eps)
-    h = xt @ P["w_in"] + P["b_in"]
-    a = _silu(h)
+    xt = store(xt)
+    z = xt @ P["w_in"]
+    a = store(_silu(z + P["b_in"]))
+    h = store(z) + P["b_in"]
     q, k, v, u = (a[:, i * d:(i + 1) * d] for i in range(4))
     o = attn_fwd(offsets, seg, ts, q.reshape(T, heads, dh), k.reshape(T, heads, dh),
                  v.reshape(T, heads, dh), rab, alpha).reshape(T, d)
+    o = store(o)
     y, m1, r1 = gln_fwd(o, u, seg, P["gamma"], P["beta"], eps)
-    x_out = y @ P["w_out"] + P["b_out"] + x
+    y = store(y)
+    x_out = store(y @ P["w_out"] + P["b_out"] + x)
     cache = dict(x=x, xt=xt, h=h, a=a, o=o, y=y)
     return x_out, cache
 
 
 def layer_bwd(offsets, seg, ts, dx_out, cache, params, heads: int, rab=None, alpha: float = 1.0,
-              eps: float = 1e-5):
-    """Backward of layer_fwd: returns dict of dx and every parameter gradient (drab if rab)."""
+              eps: float = 1e-5, store=_keep):
+    """Backward of layer_fwd: returns dict of dx and every parameter gradient (drab if rab).
+    `store` as in layer_fwd, applied to every gradient kept between steps and to the weight
+    gradients (the bias, Group-LN and relative-bias gradients stay in full precision)."""
     dx_out = _f64(dx_out)
     P = {k: _f64(v) for k, v in params.items()}
     x, xt, h, a, o, y = (cache[n] for n in ("x", "xt", "h", "a", "o", "y"))
     T, d = x.shape
     dh = d // heads
-    g = {"w_out": y.T @ dx_out, "b_out": dx_out.sum(0)}
-    dy = dx_out @ P["w_out"].T
+    g = {"w_out": store(y.T @ dx_out), "b_out": dx_out.sum(0)}
+    dy = store(dx_out @ P["w_out"].T)
     u = a[:, 3 * d:]
     do, du, g["gamma"], g["beta"] = gln_bwd(o, u, seg, P["gamma"], dy, eps)
+    do, du = store(do), store(du)
     q, k, v = (a[:, i * d:(i + 1) * d].reshape(T, heads, dh) for i in range(3))
     dq, dk, dv, drab = attn_bwd(offsets, seg, ts, q, k, v, do.reshape(T, heads, dh), rab, alpha)
-    da = np.concatenate([dq.reshape(T, d), dk.reshape(T, d), dv.reshape(T, d), du], axis=1)
+    da = store(np.concatenate([dq.reshape(T, d), dk.reshape(T, d), dv.reshape(T, d), du], axis=1))
     s = 1.0 / (1.0 + np.exp(-h))
-    dhh = da * s * (1.0 + h * (1.0 - s))
-    g["w_in"] = xt.T @ dhh
+    dhh = store(da * s * (1.0 + h * (1.0 - s)))
+    g["w_in"] = store(xt.T @ dhh)
     g["b_in"] = dhh.sum(0)
-    dxt = dhh @ P["w_in"].T
+    dxt = store(dhh @ P["w_in"].T)
     dx, _, g["gamma_in"], g["beta_in"] = gln_bwd(x, None, seg, P["gamma_in"], dxt, eps)
-    g["x"] = dx + dx_out
+    g["x"] = store(store(dx) + dx_out)
     if rab is not None:
         g["rab"] = drab
     return g

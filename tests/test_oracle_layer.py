@@ -60,3 +60,52 @@ def test_layer_forward_and_gradients_match_autograd(with_rab):
         np.testing.assert_allclose(g[name], t.grad.numpy(), rtol=1e-9, atol=1e-11, err_msg=name)
     if with_rab:
         np.testing.assert_allclose(g["rab"], trab.grad.numpy(), rtol=1e-9, atol=1e-11)
+
+
+def test_storage_hook_sees_each_kept_intermediate_once():
+    """The store hook (bf16-stored intermediates, Sec. 5's mixed precision) is applied exactly to
+    the values the layer keeps between steps: recorded with an identity hook, they are the exact
+    layer's intermediates, in order, and the results are unchanged."""
+    heads = 2
+    offsets, seg, ts, x, params, rab = tiny_batch(heads=heads)
+    out, cache = oracle.layer_fwd(offsets, seg, ts, x, params, heads, rab)
+    dout = np.random.default_rng(6).standard_normal(out.shape)
+    g = oracle.layer_bwd(offsets, seg, ts, dout, cache, params, heads, rab)
+    seen = []
+
+    def rec(a):
+        seen.append(np.array(a))
+        return a
+    out2, cache2 = oracle.layer_fwd(offsets, seg, ts, x, params, heads, rab, store=rec)
+    np.testing.assert_array_equal(out2, out)
+    fwd = [cache["xt"], cache["a"], cache["h"] - params["b_in"], cache["o"], cache["y"], out]
+    assert len(seen) == len(fwd)
+    for s, want in zip(seen, fwd):
+        np.testing.assert_allclose(s, want, rtol=0, atol=1e-12)
+    seen.clear()
+    g2 = oracle.layer_bwd(offsets, seg, ts, dout, cache2, params, heads, rab, store=rec)
+    for k in g:
+        np.testing.assert_array_equal(g2[k], g[k])
+    # w_out grad, dy, do, du, [dq|dk|dv|du], dh, w_in grad, dxt, dx of the input Group-LN, dx
+    assert len(seen) == 10
+    np.testing.assert_array_equal(seen[0], g["w_out"])
+    np.testing.assert_array_equal(seen[6], g["w_in"])
+    np.testing.assert_array_equal(seen[-1], g["x"])
+    np.testing.assert_allclose(seen[-2] + dout, g["x"], rtol=0, atol=1e-12)
+
+
+def test_storage_hook_rounds_to_bf16():
+    from synth.batches import round_bf16
+    heads = 2
+    offsets, seg, ts, x, params, rab = tiny_batch(heads=heads)
+    rb = lambda a: round_bf16(np.asarray(a)).astype(np.float64)
+    out, cache = oracle.layer_fwd(offsets, seg, ts, x, params, heads, rab, store=rb)
+    for name in ("xt", "a", "o", "y"):
+        np.testing.assert_array_equal(rb(cache[name]), cache[name], err_msg=name)
+    np.testing.assert_array_equal(rb(out), out)
+    exact, _ = oracle.layer_fwd(offsets, seg, ts, x, params, heads, rab)
+    rel = np.max(np.abs(out - exact)) / np.sqrt(np.mean(exact ** 2))
+    assert 0 < rel < 0.05
+    g = oracle.layer_bwd(offsets, seg, ts, np.ones_like(out), cache, params, heads, rab, store=rb)
+    for name in ("x", "w_in", "w_out"):
+        np.testing.assert_array_equal(rb(g[name]), g[name], err_msg=name)

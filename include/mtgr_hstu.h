@@ -305,6 +305,43 @@ mtgr_status_t mtgr_bias_silu_bwd(int64_t rows, int32_t cols, mtgr_dtype_t dtype,
                                  int64_t ld_h, const float* bias, const void* dout, int64_t ld_dout,
                                  void* dh, int64_t ld_dh, mtgr_stream_t stream);
 
+/* Elementwise out = a + b on [rows, cols] (the residual branch of the encoder layer's
+ * backward); the same layout rules as mtgr_bias_silu_fwd (out may be a or b). */
+mtgr_status_t mtgr_add(int64_t rows, int32_t cols, mtgr_dtype_t dtype, const void* a, int64_t ld_a,
+                       const void* b, int64_t ld_b, void* out, int64_t ld_out, mtgr_stream_t stream);
+
+/* Dense bf16 products of the encoder layer built around the attention (Sec. 4.2: the MLPs that
+ * project the Group-LN'd input to K, Q, V, U, read as one fused linear map followed by SiLU, and
+ * the top MLP of Eq. 6 read as one linear map plus the residual), fp32 accumulation on the bf16
+ * matrix cores, with the layer's elementwise work fused into the product:
+ *   layout MTGR_GEMM_NN: C[M,N] = A B,    A [M,K] (lda >= K), B [K,N] (ldb >= N)
+ *          MTGR_GEMM_NT: C[M,N] = A B^T,  A [M,K], B [N,K] (ldb >= K)   (input gradients)
+ *          MTGR_GEMM_TN: C[M,N] = A^T B,  A [K,M] (lda >= M), B [K,N]   (weight gradients;
+ *            colsum, if not NULL, receives the column sums of B over K as fp32 [N]: the bias
+ *            gradient; needs the workspace of mtgr_gemm_workspace_size)
+ *   epilogue MTGR_GEMM_EPI_NONE:          C = AB
+ *            MTGR_GEMM_EPI_BIAS_SILU:     C = AB (pre-activation), C2 = silu(AB + bias)
+ *            MTGR_GEMM_EPI_BIAS_RESIDUAL: C = AB + bias + R
+ *     (bias [N] fp32, 16-byte aligned; R, C2 [M,N] bf16 with strides ldr, ldc2; TN takes only
+ *     MTGR_GEMM_EPI_NONE)
+ * All matrices bf16 row-major with element strides; pointers 16-byte aligned, strides multiples
+ * of 8 elements and below 2^22.  Shapes: K >= 1; N a multiple of 128; K a multiple of 32 for
+ * NN / NT; M a multiple of 256 for TN (any M for NN / NT).  Other shapes return
+ * MTGR_ERROR_UNSUPPORTED.  The TN sums over K are split into fp32 partials that are added in a
+ * fixed order (the result is deterministic). */
+#define MTGR_GEMM_NN 0
+#define MTGR_GEMM_NT 1
+#define MTGR_GEMM_TN 2
+#define MTGR_GEMM_EPI_NONE 0
+#define MTGR_GEMM_EPI_BIAS_SILU 1
+#define MTGR_GEMM_EPI_BIAS_RESIDUAL 2
+mtgr_status_t mtgr_gemm_workspace_size(int32_t layout, int64_t M, int64_t N, int64_t K, size_t* bytes);
+mtgr_status_t mtgr_gemm_bf16(int32_t layout, int64_t M, int64_t N, int64_t K, const void* A, int64_t lda,
+                             const void* B, int64_t ldb, void* C, int64_t ldc, int32_t epilogue,
+                             const float* bias, const void* R, int64_t ldr, void* C2, int64_t ldc2,
+                             float* colsum, void* workspace, size_t workspace_bytes,
+                             mtgr_stream_t stream);
+
 /* Bytes of device scratch that mtgr_debug_validate_inputs needs. */
 #define MTGR_VALIDATE_SCRATCH_BYTES 64
 

@@ -660,6 +660,126 @@ mtgr_status_t mtgr_bias_silu_bwd(int64_t rows, int32_t cols, mtgr_dtype_t dtype,
     return ok();
 }
 
+mtgr_status_t mtgr_add(int64_t rows, int32_t cols, mtgr_dtype_t dtype, const void* a, int64_t ld_a, const void* b,
+                       int64_t ld_b, void* out, int64_t ld_out, mtgr_stream_t stream) {
+    const void* mats[3] = {a, b, out};
+    const int64_t lds[3] = {ld_a, ld_b, ld_out};
+    const char* names[3] = {"a", "b", "out"};
+    mtgr_status_t st = check_pointwise(rows, cols, dtype, mats, lds, names, 3, nullptr);
+    if (st != MTGR_SUCCESS) return st;
+    hipError_t e = mtgr::launch_add(rows, cols, dtype == MTGR_DTYPE_BF16, a, ld_a, b, ld_b, out, ld_out,
+                                    (hipStream_t)stream);
+    if (e != hipSuccess) return device_fail(e, "add");
+    return ok();
+}
+
+}  // extern "C"
+
+namespace {
+
+constexpr long long GEMM_MAX_LD = 1ll << 22;   // 32-bit per-lane copy offsets over 256 rows
+
+mtgr_status_t check_gemm(int layout, int64_t M, int64_t N, int64_t K, int epilogue) {
+    if (layout < MTGR_GEMM_NN || layout > MTGR_GEMM_TN)
+        return fail(MTGR_ERROR_INVALID_ARGUMENT, "layout %d is not MTGR_GEMM_NN / _NT / _TN", layout);
+    if (epilogue < MTGR_GEMM_EPI_NONE || epilogue > MTGR_GEMM_EPI_BIAS_RESIDUAL)
+        return fail(MTGR_ERROR_INVALID_ARGUMENT, "epilogue %d unknown", epilogue);
+    if (layout == MTGR_GEMM_TN && epilogue != MTGR_GEMM_EPI_NONE)
+        return fail(MTGR_ERROR_UNSUPPORTED, "MTGR_GEMM_TN takes no epilogue");
+    if (M < 0 || N < 0 || K < 0) return fail(MTGR_ERROR_INVALID_ARGUMENT, "negative size");
+    if (M >= (1ll << 31) || N >= (1ll << 31) || K >= (1ll << 31))
+        return fail(MTGR_ERROR_UNSUPPORTED, "sizes must be below 2^31");
+    if (N % 128 != 0) return fail(MTGR_ERROR_UNSUPPORTED, "N = %lld is not a multiple of 128", (long long)N);
+    if (layout != MTGR_GEMM_TN && K % 32 != 0)
+        return fail(MTGR_ERROR_UNSUPPORTED, "K = %lld is not a multiple of 32", (long long)K);
+    if (layout == MTGR_GEMM_TN && M % 256 != 0)
+        return fail(MTGR_ERROR_UNSUPPORTED, "M = %lld is not a multiple of 256 (MTGR_GEMM_TN)", (long long)M);
+    int mb, nb, s, per;
+    mtgr::gemm_plan(layout, M, N, K, &mb, &nb, &s, &per);
+    if ((long long)((mb + mtgr::XCDS - 1) / mtgr::XCDS) * mtgr::XCDS * nb * s >= (1ll << 24))
+        return fail(MTGR_ERROR_UNSUPPORTED, "problem too large for one launch");
+    return MTGR_SUCCESS;
+}
+
+mtgr_status_t check_ld(const void* p, const char* name, int64_t ld, int64_t min_ld) {
+    if (!p) return fail(MTGR_ERROR_NULL_POINTER, "%s is NULL", name);
+    if (!aligned16(p)) return fail(MTGR_ERROR_INVALID_ARGUMENT, "%s is not 16-byte aligned", name);
+    if (ld < min_ld || ld % 8 != 0)
+        return fail(MTGR_ERROR_INVALID_ARGUMENT, "ld of %s = %lld (needs >= %lld and a multiple of 8)", name,
+                    (long long)ld, (long long)min_ld);
+    if (ld >= GEMM_MAX_LD)
+        return fail(MTGR_ERROR_UNSUPPORTED, "ld of %s = %lld above %lld", name, (long long)ld, GEMM_MAX_LD);
+    return MTGR_SUCCESS;
+}
+
+}  // namespace
+
+extern "C" {
+
+mtgr_status_t mtgr_gemm_workspace_size(int32_t layout, int64_t M, int64_t N, int64_t K, size_t* bytes) {
+    if (!bytes) return fail(MTGR_ERROR_NULL_POINTER, "bytes is NULL");
+    mtgr_status_t st = check_gemm(layout, M, N, K, MTGR_GEMM_EPI_NONE);
+    if (st != MTGR_SUCCESS) return st;
+    *bytes = (M > 0 && N > 0 && K > 0) ? align256(mtgr::gemm_workspace_bytes(layout, M, N, K)) : 0;
+    return ok();
+}
+
+mtgr_status_t mtgr_gemm_bf16(int32_t layout, int64_t M, int64_t N, int64_t K, const void* A, int64_t lda,
+                             const void* B, int64_t ldb, void* C, int64_t ldc, int32_t epilogue, const float* bias,
+                             const void* R, int64_t ldr, void* C2, int64_t ldc2, float* colsum, void* workspace,
+                             size_t workspace_bytes, mtgr_stream_t stream) {
+    mtgr_status_t st = check_gemm(layout, M, N, K, epilogue);
+    if (st != MTGR_SUCCESS) return st;
+    if (colsum && layout != MTGR_GEMM_TN)
+        return fail(MTGR_ERROR_INVALID_ARGUMENT, "colsum is formed by MTGR_GEMM_TN only");
+    if (colsum && ((uintptr_t)colsum & 3u) != 0)
+        return fail(MTGR_ERROR_INVALID_ARGUMENT, "colsum is not 4-byte aligned");
+    hipStream_t s = (hipStream_t)stream;
+    if (M == 0 || N == 0) return ok();
+    if (K == 0) return fail(MTGR_ERROR_UNSUPPORTED, "K = 0");
+    const bool a_kr = layout == MTGR_GEMM_TN, b_kr = layout != MTGR_GEMM_NT;
+    if ((st = check_ld(A, "A", lda, a_kr ? M : K)) != MTGR_SUCCESS) return st;
+    if ((st = check_ld(B, "B", ldb, b_kr ? N : K)) != MTGR_SUCCESS) return st;
+    if ((st = check_ld(C, "C", ldc, N)) != MTGR_SUCCESS) return st;
+    if (epilogue != MTGR_GEMM_EPI_NONE) {
+        if (!bias) return fail(MTGR_ERROR_NULL_POINTER, "bias is NULL");
+        if (!aligned16(bias)) return fail(MTGR_ERROR_INVALID_ARGUMENT, "bias is not 16-byte aligned");
+    }
+    if (epilogue == MTGR_GEMM_EPI_BIAS_SILU && (st = check_ld(C2, "C2", ldc2, N)) != MTGR_SUCCESS) return st;
+    if (epilogue == MTGR_GEMM_EPI_BIAS_RESIDUAL && (st = check_ld(R, "R", ldr, N)) != MTGR_SUCCESS) return st;
+    mtgr::GemmArgs g{};
+    g.layout = layout;
+    g.epilogue = epilogue;
+    g.M = M;
+    g.N = N;
+    g.K = K;
+    g.A = A;
+    g.lda = lda;
+    g.B = B;
+    g.ldb = ldb;
+    g.C = C;
+    g.ldc = ldc;
+    g.C2 = C2;
+    g.ldc2 = ldc2;
+    g.R = R;
+    g.ldr = ldr;
+    g.bias = bias;
+    g.colsum = colsum;
+    mtgr::gemm_plan(layout, M, N, K, &g.mblocks, &g.nblocks, &g.splits, &g.ks_per_split);
+    if (layout == MTGR_GEMM_TN) {
+        const size_t need = align256(mtgr::gemm_workspace_bytes(layout, M, N, K));
+        if (workspace_bytes < need)
+            return fail(MTGR_ERROR_WORKSPACE_TOO_SMALL, "workspace %zu bytes, need %zu", workspace_bytes, need);
+        if (!workspace) return fail(MTGR_ERROR_NULL_POINTER, "workspace is NULL");
+        if (!aligned16(workspace)) return fail(MTGR_ERROR_INVALID_ARGUMENT, "workspace is not 16-byte aligned");
+        g.partial = (float*)workspace;
+        g.colsum_partial = g.partial + (size_t)g.splits * M * N;
+    }
+    hipError_t e = mtgr::launch_gemm_bf16(g, s);
+    if (e != hipSuccess) return device_fail(e, "gemm");
+    return ok();
+}
+
 mtgr_status_t mtgr_debug_validate_inputs(const mtgr_hstu_problem_t* p, const int32_t* offsets,
                                          const int8_t* seg, const int8_t* group_ids,
                                          int32_t num_groups, void* scratch, size_t scratch_bytes,

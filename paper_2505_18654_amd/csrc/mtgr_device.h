@@ -230,7 +230,7 @@ typedef __attribute__((address_space(3))) void lds_void;
 // chunks x 2 halves (the suppliers of one transposing read).
 template <int CPR>
 __device__ __forceinline__ int swz(int row) {
-    if constexpr (CPR == 16) return ((row & 3) << 2) | ((row >> 2) & 3);
+    if constexpr (CPR == 16 || CPR == 32) return ((row & 3) << 2) | ((row >> 2) & 3);
     else if constexpr (CPR == 8)
         return ((row >> 1) & 1) | (((row >> 2) & 1) << 1) | ((((row >> 1) ^ (row >> 3)) & 1) << 2);
     else return (row >> 2) & (CPR - 1);
@@ -362,9 +362,11 @@ __device__ __forceinline__ bf16x8 lds_read_tr(const uint16_t* tile, uint32_t o0,
 // row0 < nrows.  Instruction i of wave w of the 256-thread workgroup fills the 64 chunks
 // (16 bytes each) of LDS block 4 i + w, i.e. tile rows RPI i + (64 / CPR) w + lane / CPR with
 // RPI = 256 / CPR; when the tile has fewer than 256 chunks only the first waves issue.  A
-// lane's row within the block and its chunk (the swizzle depends on row mod 16 only) are the
-// same for every instruction, so each instruction needs one wave-uniform base address and one
-// per-lane 32-bit offset.  The caller guarantees ROWS * ld * 2 < 2^31.
+// lane's row within the block is the same for every instruction, and so is its chunk when RPI
+// is a multiple of 16 (the swizzle depends on row mod 16 only); with 32 chunks per row (RPI 8)
+// the source chunk alternates between even and odd instructions.  Each instruction needs one
+// wave-uniform base address and one per-lane 32-bit offset.  The caller guarantees
+// ROWS * ld * 2 < 2^31.
 template <int DH, int ROWS = 64>
 __device__ __forceinline__ void tile_dma(uint16_t* tile, const uint16_t* base, long long ld, int row0,
                                          int nrows, int col0, int tid) {
@@ -376,20 +378,24 @@ __device__ __forceinline__ void tile_dma(uint16_t* tile, const uint16_t* base, l
     asm volatile("" : "+v"(lane));
     const int w = tid >> 6;
     const int rl = w * (64 / CPR) + lane / CPR;             // row within block 0 of this wave
-    const int cl = (lane % CPR) ^ swz<CPR>(rl);             // source chunk
+    // source chunk of the lane in instruction i (tile row i * RPI + rl)
+    auto src_chunk = [&](int i) {
+        return (lane % CPR) ^ swz<CPR>(RPI % 16 == 0 ? rl : i * RPI + rl);
+    };
     const uint16_t* tbase = base + (long long)row0 * ld + col0;
     const uint32_t ltile = __builtin_amdgcn_readfirstlane(lds_address(tile) + (uint32_t)w * 1024u);
     if (NCH < 256 && w * 64 >= NCH) return;
     if (row0 + ROWS <= nrows) {
-        const uint32_t voff = (uint32_t)(rl * ld + cl * 8) * 2u;
 #pragma unroll
-        for (int i = 0; i < (NCH + 255) / 256; i++)
+        for (int i = 0; i < (NCH + 255) / 256; i++) {
+            const uint32_t voff = (uint32_t)(rl * ld + src_chunk(i) * 8) * 2u;
             lds_dma16(ltile + (uint32_t)i * 4096u, uniform_ptr(tbase + (long long)i * RPI * ld), voff);
+        }
     } else {
         const int last = nrows - 1 - row0;                  // >= 0: the tile holds a valid row
 #pragma unroll
         for (int i = 0; i < (NCH + 255) / 256; i++) {
-            const uint32_t voff = (uint32_t)(min(i * RPI + rl, last) * ld + cl * 8) * 2u;
+            const uint32_t voff = (uint32_t)(min(i * RPI + rl, last) * ld + src_chunk(i) * 8) * 2u;
             lds_dma16(ltile + (uint32_t)i * 4096u, uniform_ptr(tbase), voff);
         }
     }

@@ -117,6 +117,37 @@ hipError_t launch_bias_silu(long long rows, int cols, bool bf16, bool backward, 
                             const float* bias, const void* g, long long ld_g, void* out, long long ld_out,
                             hipStream_t s);
 
+// Dense bf16 products of the encoder layer (gemm.hip).
+constexpr int GEMM_NN = 0, GEMM_NT = 1, GEMM_TN = 2;
+constexpr int GEMM_EPI_NONE = 0, GEMM_EPI_BIAS_SILU = 1, GEMM_EPI_BIAS_RESIDUAL = 2;
+struct GemmArgs {
+    int layout, epilogue;
+    long long M, N, K;
+    const void* A;
+    long long lda;
+    const void* B;
+    long long ldb;
+    void* C;
+    long long ldc;
+    void* C2;                 // BIAS_SILU: the activation
+    long long ldc2;
+    const void* R;            // BIAS_RESIDUAL: the residual
+    long long ldr;
+    const float* bias;        // [N] fp32
+    float* colsum;            // TN: [N] column sums of B, or NULL
+    float* partial;           // TN: [splits][M][N] fp32 workspace
+    float* colsum_partial;    // TN: [splits][N] fp32 workspace
+    int mblocks, nblocks, splits, ks_per_split;
+};
+void gemm_plan(int layout, long long M, long long N, long long K, int* mblocks, int* nblocks, int* splits,
+               int* ks_per_split);
+size_t gemm_workspace_bytes(int layout, long long M, long long N, long long K);
+hipError_t launch_gemm_bf16(const GemmArgs& g, hipStream_t s);
+
+// Elementwise out = a + b (bf16 or fp32) on [rows, cols] with row strides.
+hipError_t launch_add(long long rows, int cols, bool bf16, const void* a, long long lda, const void* b,
+                      long long ldb, void* out, long long ldo, hipStream_t s);
+
 // Debug validation of a jagged batch: `first` (VALIDATE_CONDITIONS 64-bit slots of device
 // memory) receives per condition the smallest failing index, ~0 if none.
 constexpr int VALIDATE_CONDITIONS = 6;

@@ -74,7 +74,35 @@ __global__ __launch_bounds__(256) void bias_silu_kernel(long long rows, int cols
     }
 }
 
+// out = a + b (the encoder layer's residual branch in the backward).
+template <bool BF16>
+__global__ __launch_bounds__(256) void add_kernel(long long rows, int cols, const void* a, long long lda,
+                                                  const void* b, long long ldb, void* out, long long ldo) {
+    using C = Chunk<BF16>;
+    constexpr int N = C::N;
+    const int nch = cols / N;
+    for (long long r = blockIdx.x; r < rows; r += gridDim.x) {
+        for (int ch = threadIdx.x; ch < nch; ch += blockDim.x) {
+            float x[N], y[N];
+            C::load(a, r * lda + ch * N, x);
+            C::load(b, r * ldb + ch * N, y);
+#pragma unroll
+            for (int i = 0; i < N; i++) x[i] += y[i];
+            C::store(out, r * ldo + ch * N, x);
+        }
+    }
+}
+
 }  // namespace
+
+hipError_t launch_add(long long rows, int cols, bool bf16, const void* a, long long lda, const void* b,
+                      long long ldb, void* out, long long ldo, hipStream_t s) {
+    if (rows <= 0 || cols <= 0) return hipSuccess;
+    const int grid = (int)(rows < 16384 ? rows : 16384);
+    if (bf16) add_kernel<true><<<grid, 256, 0, s>>>(rows, cols, a, lda, b, ldb, out, ldo);
+    else add_kernel<false><<<grid, 256, 0, s>>>(rows, cols, a, lda, b, ldb, out, ldo);
+    return hipGetLastError();
+}
 
 hipError_t launch_bias_silu(long long rows, int cols, bool bf16, bool backward, const void* h, long long ld_h,
                             const float* bias, const void* g, long long ld_g, void* out, long long ld_out,

@@ -33,6 +33,8 @@ MTGR_BWD_DS_READY = 16
 MTGR_FWD_CAND_ROWS = 32
 MTGR_VALIDATE_SCRATCH_BYTES = 64
 MTGR_NOALLOC_SCRATCH_BYTES = 16 * 1024 * 1024
+MTGR_GEMM_NN, MTGR_GEMM_NT, MTGR_GEMM_TN = 0, 1, 2
+MTGR_GEMM_EPI_NONE, MTGR_GEMM_EPI_BIAS_SILU, MTGR_GEMM_EPI_BIAS_RESIDUAL = 0, 1, 2
 MTGR_EMB_KEY_EMPTY = 0xFFFFFFFFFFFFFFFF
 MTGR_EMB_KEY_DELETED = 0xFFFFFFFFFFFFFFFE
 MTGR_EMB_STATE_WORDS = 8
@@ -42,7 +44,7 @@ EXPORTED = (
     "mtgr_hstu_attn_workspace_size", "mtgr_hstu_attn_plan", "mtgr_hstu_attn_fwd", "mtgr_hstu_attn_bwd",
     "mtgr_hstu_attn_fwd_noalloc", "mtgr_hstu_attn_fwd_cached",
     "mtgr_group_layernorm_workspace_size", "mtgr_group_layernorm_fwd", "mtgr_group_layernorm_bwd",
-    "mtgr_bias_silu_fwd", "mtgr_bias_silu_bwd",
+    "mtgr_bias_silu_fwd", "mtgr_bias_silu_bwd", "mtgr_add", "mtgr_gemm_workspace_size", "mtgr_gemm_bf16",
     "mtgr_debug_validate_inputs", "mtgr_status_string", "mtgr_last_error_message", "mtgr_version",
     "mtgr_embedding_init", "mtgr_embedding_dedup_workspace_size", "mtgr_embedding_dedup",
     "mtgr_embedding_lookup_workspace_size", "mtgr_embedding_lookup", "mtgr_embedding_gather",
@@ -116,6 +118,10 @@ def lib() -> ctypes.CDLL:
         i64 = ctypes.c_int64
         L.mtgr_bias_silu_fwd.argtypes = [i64, i32, ctypes.c_int, vp, i64, vp, vp, i64, vp]
         L.mtgr_bias_silu_bwd.argtypes = [i64, i32, ctypes.c_int, vp, i64, vp, vp, i64, vp, i64, vp]
+        L.mtgr_add.argtypes = [i64, i32, ctypes.c_int, vp, i64, vp, i64, vp, i64, vp]
+        L.mtgr_gemm_workspace_size.argtypes = [i32, i64, i64, i64, ctypes.POINTER(sz)]
+        L.mtgr_gemm_bf16.argtypes = [i32, i64, i64, i64, vp, i64, vp, i64, vp, i64, i32, vp, vp, i64, vp, i64, vp,
+                                     vp, sz, vp]
         E = ctypes.POINTER(EmbeddingTable)
         L.mtgr_embedding_init.argtypes = [E, vp]
         L.mtgr_embedding_dedup_workspace_size.argtypes = [i64, ctypes.POINTER(sz)]
@@ -248,6 +254,25 @@ def mtgr_bias_silu_fwd(rows, cols, dtype, h, ld_h, bias, out, ld_out, stream=Non
 def mtgr_bias_silu_bwd(rows, cols, dtype, h, ld_h, bias, dout, ld_dout, dh, ld_dh, stream=None) -> None:
     _check(lib().mtgr_bias_silu_bwd(int(rows), int(cols), int(dtype), _ptr(h), int(ld_h), _ptr(bias), _ptr(dout),
                                     int(ld_dout), _ptr(dh), int(ld_dh), _stream(stream)))
+
+
+def mtgr_add(rows, cols, dtype, a, ld_a, b, ld_b, out, ld_out, stream=None) -> None:
+    _check(lib().mtgr_add(int(rows), int(cols), int(dtype), _ptr(a), int(ld_a), _ptr(b), int(ld_b), _ptr(out),
+                          int(ld_out), _stream(stream)))
+
+
+def mtgr_gemm_workspace_size(layout, M, N, K) -> int:
+    out = ctypes.c_size_t(0)
+    _check(lib().mtgr_gemm_workspace_size(int(layout), int(M), int(N), int(K), ctypes.byref(out)))
+    return out.value
+
+
+def mtgr_gemm_bf16(layout, M, N, K, A, lda, B, ldb, C, ldc, epilogue=MTGR_GEMM_EPI_NONE, bias=None, R=None,
+                   ldr=0, C2=None, ldc2=0, colsum=None, workspace=None, workspace_bytes=0, stream=None) -> None:
+    _check(lib().mtgr_gemm_bf16(int(layout), int(M), int(N), int(K), _ptr(A), int(lda), _ptr(B), int(ldb),
+                                _ptr(C), int(ldc), int(epilogue), _ptr(bias), _ptr(R), int(ldr), _ptr(C2),
+                                int(ldc2), _ptr(colsum), _ptr(workspace), int(workspace_bytes),
+                                _stream(stream)))
 
 
 def mtgr_debug_validate_inputs(problem, offsets, seg, group_ids, num_groups, scratch, scratch_bytes,

@@ -5,12 +5,14 @@
     Vt = Eq. 5 attention (dynamic mask, 1 / n_b)
     X' = GroupLN(Vt (*) U) W_out + b_out + X             Eq. 6; the top MLP as one linear map
 
-The projection and output products are plain GEMMs and go to the BLAS library (hipBLASLt
-through torch.matmul); Group-LN, bias + SiLU and the attention run in this package's HIP
-kernels through the C ABI.  Q, K, V, U are column views of the one [T, 4d] activation, which the
-kernels take with their token stride, and their gradients are written into the same layout,
-so the backward's input-projection GEMMs read one [T, 4d] gradient.  The bias gradients are
-column sums left to torch.
+Every step runs in this package's HIP kernels through the C ABI: the projection product with
+bias + SiLU in its epilogue (it keeps the pre-activation for the backward), the output product
+with bias + residual in its epilogue, the input-gradient products (A B^T), the weight-gradient
+products (A^T B, split over tokens) with the bias gradients as fused column sums, Group-LN,
+the attention and the residual add of the input gradient.  Q, K, V, U are column views of the
+one [T, 4d] activation, which the kernels take with their token stride, and their gradients are
+written into the same layout, so the backward's input-projection products read one [T, 4d]
+gradient.  torch only allocates.
 """
 from __future__ import annotations
 
@@ -45,14 +47,13 @@ def layer_fwd(x: torch.Tensor, jag: ops.Jagged, P: LayerParams, heads: int, rab=
     """Returns (x_out [T, d], ctx for layer_bwd)."""
     T, d = x.shape
     xt, m0, r0 = ops.gln_fwd(x, None, jag.seg, P.gamma_in, P.beta_in, eps)
-    h = xt @ P.w_in                                          # [T, 4d]
+    h = torch.empty((T, 4 * d), dtype=x.dtype, device=x.device)    # pre-activation
     a = torch.empty_like(h)
-    hstu.mtgr_bias_silu_fwd(T, 4 * d, ops._dtype_code(h), h, 4 * d, P.b_in, a, 4 * d)
+    ops.gemm(xt, P.w_in, "nn", out=h, bias=P.b_in, silu_out=a)
     q, k, v, u = _split(a, d, heads)
     o = ops.attn_fwd(q, k, v, jag, rab, alpha, workspace=workspace, planned=planned)
     y, m1, r1 = ops.gln_fwd(o.view(T, d), u, jag.seg, P.gamma, P.beta, eps)
-    x_out = torch.addmm(x, y, P.w_out)
-    x_out += P.b_out.to(x_out.dtype)
+    x_out = ops.gemm(y, P.w_out, "nn", bias=P.b_out, residual=x)
     ctx = dict(x=x, xt=xt, m0=m0, r0=r0, h=h, a=a, o=o, y=y, m1=m1, r1=r1)
     return x_out, ctx
 
@@ -66,8 +67,9 @@ def layer_bwd(dx_out: torch.Tensor, ctx: dict, jag: ops.Jagged, P: LayerParams, 
     stage-by-stage checks."""
     x, xt, h, a, o, y = (ctx[n] for n in ("x", "xt", "h", "a", "o", "y"))
     T, d = x.shape
-    g = {"w_out": y.t() @ dx_out, "b_out": dx_out.sum(0, dtype=torch.float32)}
-    dy = dx_out @ P.w_out.t()
+    g = {"b_out": torch.empty(d, dtype=torch.float32, device=x.device)}
+    g["w_out"] = ops.gemm(y, dx_out, "tn", colsum=g["b_out"])
+    dy = ops.gemm(dx_out, P.w_out, "nt")
     da = torch.empty_like(a)
     dq, dk, dv, du = _split(da, d, heads)
     q, k, v, u = _split(a, d, heads)
@@ -84,11 +86,11 @@ def layer_bwd(dx_out: torch.Tensor, ctx: dict, jag: ops.Jagged, P: LayerParams, 
     if keep is not None:
         keep.update(dy=dy, do=do, da=da.clone())
     hstu.mtgr_bias_silu_bwd(T, 4 * d, ops._dtype_code(h), h, 4 * d, P.b_in, da, 4 * d, da, 4 * d)
-    g["b_in"] = da.sum(0, dtype=torch.float32)
-    g["w_in"] = xt.t() @ da
-    dxt = da @ P.w_in.t()
+    g["b_in"] = torch.empty(4 * d, dtype=torch.float32, device=x.device)
+    g["w_in"] = ops.gemm(xt, da, "tn", colsum=g["b_in"])
+    dxt = ops.gemm(da, P.w_in, "nt")
     dx, _, g["gamma_in"], g["beta_in"] = ops.gln_bwd(dxt, x, None, jag.seg, P.gamma_in, ctx["m0"], ctx["r0"], eps)
-    g["x"] = dx + dx_out
+    g["x"] = ops.add(dx, dx_out)
     if keep is not None:
         keep.update(dh=da, dxt=dxt, dx_gln=dx)
     return g

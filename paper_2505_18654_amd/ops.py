@@ -223,3 +223,53 @@ def gln_workspace(x, groups: int) -> torch.Tensor:
     p = hstu.gln_problem(T, d, groups, _dtype_code(x))
     n = hstu.mtgr_group_layernorm_workspace_size(p, True)
     return torch.empty(max(n, 256), dtype=torch.uint8, device=x.device)
+
+
+_GEMM_LAYOUTS = {"nn": hstu.MTGR_GEMM_NN, "nt": hstu.MTGR_GEMM_NT, "tn": hstu.MTGR_GEMM_TN}
+
+
+def _row_ld(t: torch.Tensor) -> int:
+    if t.dim() != 2 or t.dtype != torch.bfloat16 or (t.shape[1] > 1 and t.stride(1) != 1):
+        raise ValueError("GEMM operands are 2-D bf16 with a dense inner dim")
+    return t.stride(0) if t.shape[0] > 1 else t.shape[1]
+
+
+def gemm(a, b, layout: str = "nn", out=None, bias=None, residual=None, silu_out=None, colsum=None,
+         workspace=None):
+    """bf16 product through mtgr_gemm_bf16: 'nn' a @ b, 'nt' a @ b.T, 'tn' a.T @ b, with the
+    encoder layer's fused epilogues (bias + SiLU into `silu_out`, or bias + residual) and, for
+    'tn', the fp32 column sums of b into `colsum`.  Returns `out`."""
+    lay = _GEMM_LAYOUTS[layout]
+    if layout == "nn":
+        (M, K), N = a.shape, b.shape[1]
+    elif layout == "nt":
+        (M, K), N = a.shape, b.shape[0]
+    else:
+        (K, M), N = a.shape, b.shape[1]
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.bfloat16, device=a.device)
+    epi = hstu.MTGR_GEMM_EPI_NONE
+    if silu_out is not None:
+        epi = hstu.MTGR_GEMM_EPI_BIAS_SILU
+    elif residual is not None:
+        epi = hstu.MTGR_GEMM_EPI_BIAS_RESIDUAL
+    ws_bytes = 0
+    if layout == "tn":
+        ws_bytes = hstu.mtgr_gemm_workspace_size(lay, M, N, K)
+        if workspace is None or workspace.numel() < ws_bytes:
+            workspace = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device=a.device)
+        ws_bytes = workspace.numel()
+    hstu.mtgr_gemm_bf16(lay, M, N, K, a, _row_ld(a), b, _row_ld(b), out, _row_ld(out), epi, bias,
+                        residual, _row_ld(residual) if residual is not None else 0, silu_out,
+                        _row_ld(silu_out) if silu_out is not None else 0, colsum, workspace, ws_bytes)
+    return out
+
+
+def add(a, b, out=None):
+    """out = a + b through mtgr_add (2-D, dense inner dim)."""
+    if out is None:
+        out = torch.empty_like(a)
+    rows, cols = a.shape
+    hstu.mtgr_add(rows, cols, _dtype_code(a), a, _token_stride(a, cols), b, _token_stride(b, cols), out,
+                  _token_stride(out, cols))
+    return out

@@ -19,7 +19,7 @@ FAKE = 0x7f0000000000           # 256-byte aligned non-NULL address, never deref
 def declared_functions():
     text = "".join(open(h).read() for h in HEADERS)
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(mtgr_[a-z_]+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(mtgr_[a-z0-9_]+)\s*\(", text)))
 
 
 def test_library_exports_every_declared_function():
@@ -443,3 +443,80 @@ def test_cached_forward_flags():
         hstu.mtgr_hstu_attn_fwd_cached(prob(), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE, None, FAKE, FAKE,
                                        FAKE, FAKE, FAKE, 1 << 30, FAKE, 1 << 30, 0)
     assert e.value.status == hstu.MTGR_ERROR_NULL_POINTER
+
+
+# ------------------------------------------------------------------ dense products
+NN, NT, TN = hstu.MTGR_GEMM_NN, hstu.MTGR_GEMM_NT, hstu.MTGR_GEMM_TN
+EPI_SILU, EPI_RES = hstu.MTGR_GEMM_EPI_BIAS_SILU, hstu.MTGR_GEMM_EPI_BIAS_RESIDUAL
+
+
+def gemm(layout=NN, M=512, N=256, K=256, A=FAKE, lda=None, B=FAKE, ldb=None, C=FAKE, ldc=None, epilogue=0,
+         bias=None, R=None, ldr=0, C2=None, ldc2=0, colsum=None, workspace=FAKE, workspace_bytes=1 << 30):
+    lda = lda if lda is not None else (M if layout == TN else K)
+    ldb = ldb if ldb is not None else (K if layout == NT else N)
+    ldc = ldc if ldc is not None else N
+    hstu.mtgr_gemm_bf16(layout, M, N, K, A, lda, B, ldb, C, ldc, epilogue, bias, R, ldr, C2, ldc2, colsum,
+                        workspace, workspace_bytes, 0)
+
+
+@pytest.mark.parametrize("kw, status", [
+    (dict(layout=3), hstu.MTGR_ERROR_INVALID_ARGUMENT),
+    (dict(epilogue=3), hstu.MTGR_ERROR_INVALID_ARGUMENT),
+    (dict(N=200), hstu.MTGR_ERROR_UNSUPPORTED),                        # N % 128
+    (dict(K=100), hstu.MTGR_ERROR_UNSUPPORTED),                        # NN: K % 32
+    (dict(layout=NT, K=48), hstu.MTGR_ERROR_UNSUPPORTED),
+    (dict(layout=TN, M=300), hstu.MTGR_ERROR_UNSUPPORTED),             # TN: M % 256
+    (dict(layout=TN, epilogue=EPI_SILU, bias=FAKE, C2=FAKE, ldc2=256), hstu.MTGR_ERROR_UNSUPPORTED),
+    (dict(K=0), hstu.MTGR_ERROR_UNSUPPORTED),
+    (dict(M=-1), hstu.MTGR_ERROR_INVALID_ARGUMENT),
+    (dict(A=None), hstu.MTGR_ERROR_NULL_POINTER),
+    (dict(C=FAKE + 8), hstu.MTGR_ERROR_INVALID_ARGUMENT),              # misaligned
+    (dict(lda=100), hstu.MTGR_ERROR_INVALID_ARGUMENT),                 # ld < K
+    (dict(ldb=260), hstu.MTGR_ERROR_INVALID_ARGUMENT),                 # ld % 8
+    (dict(ldc=1 << 22), hstu.MTGR_ERROR_UNSUPPORTED),                  # ld too large
+    (dict(epilogue=EPI_SILU, C2=FAKE, ldc2=256), hstu.MTGR_ERROR_NULL_POINTER),       # no bias
+    (dict(epilogue=EPI_SILU, bias=FAKE + 4, C2=FAKE, ldc2=256), hstu.MTGR_ERROR_INVALID_ARGUMENT),
+    (dict(epilogue=EPI_SILU, bias=FAKE), hstu.MTGR_ERROR_NULL_POINTER),               # no C2
+    (dict(epilogue=EPI_RES, bias=FAKE, R=FAKE, ldr=128), hstu.MTGR_ERROR_INVALID_ARGUMENT),
+    (dict(colsum=FAKE), hstu.MTGR_ERROR_INVALID_ARGUMENT),             # colsum needs TN
+    (dict(layout=TN, colsum=FAKE + 2), hstu.MTGR_ERROR_INVALID_ARGUMENT),
+    (dict(layout=TN, workspace=None), hstu.MTGR_ERROR_NULL_POINTER),
+    (dict(layout=TN, workspace_bytes=1024), hstu.MTGR_ERROR_WORKSPACE_TOO_SMALL),
+])
+def test_gemm_argument_checks(kw, status):
+    with pytest.raises(hstu.MtgrError) as e:
+        gemm(**kw)
+    assert e.value.status == status, str(e.value)
+
+
+def test_gemm_empty_output_is_a_noop():
+    gemm(M=0, A=None, B=None, C=None)
+    gemm(layout=TN, N=0, A=None, B=None, C=None, workspace=None, workspace_bytes=0)
+
+
+def test_gemm_workspace_sizes():
+    assert hstu.mtgr_gemm_workspace_size(NN, 4096, 2048, 512) == 0
+    assert hstu.mtgr_gemm_workspace_size(NT, 4096, 512, 2048) == 0
+    # weight gradient of the projection at 2^20 tokens, d = 512: one 256 x 128 tile per
+    # (m, n) block, enough K splits for two workgroups per CU, fp32 partials plus column sums
+    ws = hstu.mtgr_gemm_workspace_size(TN, 512, 2048, 1 << 20)
+    tiles = 2 * 16
+    splits = -(-512 // tiles)
+    assert ws >= splits * (512 * 2048 + 2048) * 4
+    # a short K is not split
+    assert hstu.mtgr_gemm_workspace_size(TN, 256, 128, 40) == (256 * 128 + 128) * 4
+    # the exact size is accepted, one byte less is refused
+    need = hstu.mtgr_gemm_workspace_size(TN, 256, 128, 1000)
+    with pytest.raises(hstu.MtgrError) as e:
+        gemm(layout=TN, M=256, N=128, K=1000, workspace_bytes=need - 1)
+    assert e.value.status == hstu.MTGR_ERROR_WORKSPACE_TOO_SMALL
+
+
+def test_add_argument_checks():
+    with pytest.raises(hstu.MtgrError) as e:
+        hstu.mtgr_add(10, 60, BF16, FAKE, 64, FAKE, 64, FAKE, 64, 0)          # cols % 8
+    assert e.value.status == hstu.MTGR_ERROR_INVALID_ARGUMENT
+    with pytest.raises(hstu.MtgrError) as e:
+        hstu.mtgr_add(10, 64, BF16, FAKE, 64, None, 64, FAKE, 64, 0)
+    assert e.value.status == hstu.MTGR_ERROR_NULL_POINTER
+    hstu.mtgr_add(0, 64, BF16, None, 64, None, 64, None, 64, 0)

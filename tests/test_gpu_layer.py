@@ -7,9 +7,9 @@ bar of token tensors over the whole tensor (they are heavy-tailed: max/rms of dW
 12, so their bf16 storage rounding is subtracted first).  The whole layer is also compared end
 to end with the fp64 oracle layer
 (oracle.layer_fwd / layer_bwd, pinned to torch autograd in test_oracle_layer.py); there the
-bf16 rounding of every stored intermediate compounds, so that comparison is reported and only
-bounded loosely (it catches wiring mistakes, such as a swapped projection block, not rounding).
-The GEMMs run in the BLAS library."""
+bf16 rounding of every stored intermediate compounds; that comparison is held to a tolerance
+derived from the oracle run with bf16-stored intermediates (see the end of run()).
+Every stage, the products included, runs in the library's kernels."""
 import os
 
 import numpy as np
@@ -19,6 +19,7 @@ import torch
 import oracle
 from paper_2505_18654_amd import layer, ops
 from synth import SEG_CAND, SEG_HIST, SEG_RT, SEG_USER, make_layout
+from synth.batches import round_bf16
 from tests.dense_ref import operand_rounding_bounds
 from tests.gpu_util import TOL, custom_layout, per_user_err, rel_err, say, tensor_err, to_np
 
@@ -93,7 +94,9 @@ def run(L, heads, rab_buckets, label):
     xt_r, _, _ = oracle.gln_fwd(xn, None, L.seg, P["gamma_in"], P["beta_in"])
     e["xt"] = tok(ctx["xt"], xt_r)
     e["h"] = tok(ctx["h"], D["xt"] @ P["w_in"])
-    e["a"] = tok(ctx["a"], silu(D["h"] + P["b_in"]))
+    # the activation is formed in the product's epilogue from the fp32 accumulator (not from the
+    # stored pre-activation h): its input is the stored xt
+    e["a"] = tok(ctx["a"], silu(D["xt"] @ P["w_in"] + P["b_in"]))
     q, k, v, u = (D["a"][:, i * d:(i + 1) * d] for i in range(4))
     # The attention stage takes the layer's own activations (SiLU outputs, non-zero mean), so its
     # sums cancel: each output also gets the bound of its bf16 P / dS operand rounding.
@@ -132,15 +135,33 @@ def run(L, heads, rab_buckets, label):
     say(f"[layer] {label} stages " + " ".join(f"{k}={v:.1e}" for k, v in e.items()))
     bad = {k: v for k, v in e.items() if not v <= TOL["bf16"]}
     assert not bad, (label, bad)
-    # end to end against the fp64 layer (bf16 roundings of every stored intermediate compound:
-    # reported, and bounded loosely to catch wiring mistakes the stage checks would not)
+    # End to end against the exact fp64 layer.  Every intermediate the device keeps is bf16, so
+    # the device's outputs carry the compounded storage rounding of the whole chain.  The
+    # tolerance is derived from the oracle itself: the same exact layer evaluated with
+    # bf16-stored intermediates (oracle store hook) shows how far storage rounding alone moves
+    # each output; the device, which rounds at the same points (plus its bf16 attention
+    # operands and fp32 sums), is held to twice that plus the stage bar.
     ref, cache = oracle.layer_fwd(L.offsets, L.seg, L.ts, xn, P, heads, rab_np)
     gr = oracle.layer_bwd(L.offsets, L.seg, L.ts, dxn, cache, P, heads, rab_np)
-    ee = {"x_out": tok(out, ref), "dx": tok(g["x"], gr["x"])}
-    for name in ("w_in", "b_in", "w_out", "gamma_in", "beta_in", "gamma", "beta"):
-        ee[name] = rel_err(to_np(g[name]), gr[name])
-    say(f"[layer] {label} end-to-end " + " ".join(f"{k}={v:.1e}" for k, v in ee.items()))
-    assert max(ee.values()) <= 0.2, (label, ee)
+    rb = lambda a: round_bf16(np.asarray(a)).astype(np.float64)
+    ref_s, cache_s = oracle.layer_fwd(L.offsets, L.seg, L.ts, xn, P, heads, rab_np, store=rb)
+    gr_s = oracle.layer_bwd(L.offsets, L.seg, L.ts, dxn, cache_s, P, heads, rab_np, store=rb)
+
+    def lit(got, want):
+        return per_user_err(L, users, np.asarray(got).reshape(T, -1), np.asarray(want).reshape(T, -1), "bf16",
+                            tol)["literal"]
+    ee, es, ed = {}, {}, {}
+    for name, got, want, want_s in (("x_out", to_np(out), ref, ref_s), ("dx", to_np(g["x"]), gr["x"], gr_s["x"])):
+        ee[name], es[name], ed[name] = lit(got, want), lit(want_s, want), lit(got, want_s)
+    for name in ("w_in", "b_in", "w_out", "b_out", "gamma_in", "beta_in", "gamma", "beta") + (
+            ("rab",) if rab is not None else ()):
+        got = to_np(g[name])
+        ee[name], es[name], ed[name] = rel_err(got, gr[name]), rel_err(gr_s[name], gr[name]), rel_err(got, gr_s[name])
+    say(f"[layer] {label} end-to-end vs exact " + " ".join(f"{k}={v:.1e}" for k, v in ee.items()))
+    say(f"[layer] {label} storage rounding alone " + " ".join(f"{k}={v:.1e}" for k, v in es.items()))
+    say(f"[layer] {label} vs bf16-stored oracle " + " ".join(f"{k}={v:.1e}" for k, v in ed.items()))
+    over = {k: (ee[k], 2 * es[k] + tol) for k in ee if not ee[k] <= 2 * es[k] + tol}
+    assert not over, (label, over)
 
 
 def test_layer_small_config():

@@ -171,6 +171,9 @@ def main():
                     help="time one whole encoder layer (Group-LN, projection GEMM, bias + SiLU, "
                          "attention, gate + Group-LN, output GEMM; forward and backward) instead "
                          "of the attention path, and print its own JSON line")
+    ap.add_argument("--no-gemm-detail", action="store_true",
+                    help="with --layer: skip timing each dense product on its own after the timed "
+                         "region (for kernel traces of the layer steps alone)")
     ap.add_argument("--embedding", action="store_true",
                     help="time the dynamic embedding table instead (de-duplication, lookup with "
                          "insertion, gather and sparse SGD of the workload's sparse IDs) and print "
@@ -380,7 +383,9 @@ def main():
 
 def bench_layer(args, layout):
     """One encoder layer (Sec. 4.2) forward + backward on the workload's batch: synthetic
-    bf16 input and seeded parameters; the GEMMs go to the BLAS library."""
+    bf16 input and seeded parameters; every step, the dense products included, runs in the
+    library's kernels.  After the timed region each product is timed on its own (HIP events on
+    the stream it runs on) against the dense bf16 MFMA peak."""
     import torch
     from paper_2505_18654_amd import layer, ops
     spec = layout.spec
@@ -428,7 +433,49 @@ def bench_layer(args, layout):
                        "pass": "fwd" if fwd_only else "fwd+bwd", "layer": True},
             "tflops": (f_attn + f_gemm) / (ms * 1e-3) / 1e12,
             "flop_split": {"attention": f_attn, "gemm": f_gemm}}
+    if not args.no_gemm_detail:
+        line["gemm"] = layer_gemm_times(x, dxo, P, fwd_only)
+        line["gemm_ms"] = sum(v["ms"] for v in line["gemm"].values())
     print(json.dumps(line), flush=True)
+
+
+def layer_gemm_times(x, dxo, P, fwd_only, reps=20):
+    """Each dense product of the layer timed alone: ms per call, TFLOP/s and the fraction of
+    the 2.5 PFLOP/s dense bf16 MFMA peak."""
+    import torch
+    from paper_2505_18654_amd import ops
+    T, d = x.shape
+    h = torch.empty((T, 4 * d), dtype=torch.bfloat16, device="cuda")
+    a = torch.empty_like(h)
+    y = torch.empty_like(x)
+    b_in = torch.empty(4 * d, device="cuda")
+    b_out = torch.empty(d, device="cuda")
+    ws = torch.empty(max(ops.hstu.mtgr_gemm_workspace_size(ops.hstu.MTGR_GEMM_TN, d, 4 * d, T), 256),
+                     dtype=torch.uint8, device="cuda")
+    cases = {"proj_fwd_nn_bias_silu": ((T, 4 * d, d), lambda: ops.gemm(y, P.w_in, "nn", out=h, bias=P.b_in,
+                                                                          silu_out=a)),
+             "out_fwd_nn_bias_residual": ((T, d, d), lambda: ops.gemm(y, P.w_out, "nn", bias=P.b_out, residual=x))}
+    if not fwd_only:
+        cases.update({
+            "out_dgrad_nt": ((T, d, d), lambda: ops.gemm(dxo, P.w_out, "nt")),
+            "out_wgrad_tn_colsum": ((d, d, T), lambda: ops.gemm(y, dxo, "tn", colsum=b_out, workspace=ws)),
+            "proj_wgrad_tn_colsum": ((d, 4 * d, T), lambda: ops.gemm(y, a, "tn", colsum=b_in, workspace=ws)),
+            "proj_dgrad_nt": ((T, d, 4 * d), lambda: ops.gemm(a, P.w_in, "nt")),
+        })
+    out = {}
+    for name, ((M, N, K), fn) in cases.items():
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        tf = 2.0 * M * N * K / (ms * 1e-3) / 1e12
+        out[name] = {"M": M, "N": N, "K": K, "ms": ms, "tflops": tf, "frac": tf / 2500.0}
+    return out
 
 
 def bench_embedding(args, layout):

@@ -325,9 +325,9 @@ mtgr_status_t mtgr_add(int64_t rows, int32_t cols, mtgr_dtype_t dtype, const voi
  *     (bias [N] fp32, 16-byte aligned; R, C2 [M,N] bf16 with strides ldr, ldc2; TN takes only
  *     MTGR_GEMM_EPI_NONE)
  * All matrices bf16 row-major with element strides; pointers 16-byte aligned, strides multiples
- * of 8 elements and below 2^22.  Shapes: K >= 1; N a multiple of 128; K a multiple of 32 for
- * NN / NT; M a multiple of 256 for TN (any M for NN / NT).  Other shapes return
- * MTGR_ERROR_UNSUPPORTED.  The TN sums over K are split into fp32 partials that are added in a
+ * of 8 elements and below 2^22.  Shapes: K >= 1; N a multiple of 8; K a multiple of 32 for
+ * NN / NT (any K for TN); M a multiple of 8 for TN (any M for NN / NT).  Other shapes return
+ * MTGR_ERROR_UNSUPPORTED; M = 0 or N = 0 does nothing.  The TN sums over K are split into fp32 partials that are added in a
  * fixed order (the result is deterministic). */
 #define MTGR_GEMM_NN 0
 #define MTGR_GEMM_NT 1

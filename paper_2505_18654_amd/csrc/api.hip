@@ -689,11 +689,11 @@ mtgr_status_t check_gemm(int layout, int64_t M, int64_t N, int64_t K, int epilog
     if (M < 0 || N < 0 || K < 0) return fail(MTGR_ERROR_INVALID_ARGUMENT, "negative size");
     if (M >= (1ll << 31) || N >= (1ll << 31) || K >= (1ll << 31))
         return fail(MTGR_ERROR_UNSUPPORTED, "sizes must be below 2^31");
-    if (N % 128 != 0) return fail(MTGR_ERROR_UNSUPPORTED, "N = %lld is not a multiple of 128", (long long)N);
+    if (N % 8 != 0) return fail(MTGR_ERROR_UNSUPPORTED, "N = %lld is not a multiple of 8", (long long)N);
     if (layout != MTGR_GEMM_TN && K % 32 != 0)
         return fail(MTGR_ERROR_UNSUPPORTED, "K = %lld is not a multiple of 32", (long long)K);
-    if (layout == MTGR_GEMM_TN && M % 256 != 0)
-        return fail(MTGR_ERROR_UNSUPPORTED, "M = %lld is not a multiple of 256 (MTGR_GEMM_TN)", (long long)M);
+    if (layout == MTGR_GEMM_TN && M % 8 != 0)
+        return fail(MTGR_ERROR_UNSUPPORTED, "M = %lld is not a multiple of 8 (MTGR_GEMM_TN)", (long long)M);
     int mb, nb, s, per;
     mtgr::gemm_plan(layout, M, N, K, &mb, &nb, &s, &per);
     if ((long long)((mb + mtgr::XCDS - 1) / mtgr::XCDS) * mtgr::XCDS * nb * s >= (1ll << 24))

@@ -11,15 +11,26 @@
 //              split over K into fp32 partials that a second kernel adds in a fixed order, with
 //              the column sums of B (the bias gradient) formed on the way.
 //
-// Workgroup: 4 waves, a 256 (m) x 128 (n) tile of C, k in steps of 32 through three LDS stages
-// filled by global_load_lds one or two steps ahead.  The products are computed transposed,
-// C^T block = B^T A^T (v_mfma_f32_32x32x16_bf16), so that a lane's accumulators hold one row of
-// C at 4 consecutive columns per register group: the epilogue reads bias / residual and writes
-// C in 8-byte pieces per row without an LDS round trip.  An operand whose k index is contiguous
-// in memory (A of NN / NT, B of NT) sits in LDS as [rows][32 k] and is read 16 bytes per lane;
-// one whose k index runs over rows (B of NN / TN, A of TN) sits as [32 k][cols] and is read
-// with the transposing ds_read_b64_tr_b16, the supplier rows chosen so that both operands use
-// the natural k order of the instruction (lane half hf holds k = 8 hf .. 8 hf + 7).
+// Workgroup: 4 waves, a 256 (m) x 128 (n) tile of C, two workgroups per CU (so that one
+// workgroup's prologue, barrier hand-overs and epilogue run under the other's MFMAs).  Wave w
+// computes the 128 x 64 part (m half w % 2, n half w / 2) as 4 x 2 blocks of 32 x 32.  k
+// advances in steps of 32 through three LDS stages filled by global_load_lds two steps ahead.
+// Within a step the two k16 halves are software-pipelined: the operands of the second half are
+// read under the first half's MFMAs, the barrier that hands over the next stage sits between
+// the halves, and the next stage's first operands are read under the second half's MFMAs.
+// Every per-lane address (copy offsets, LDS read bases) is computed once per tile; per step
+// only the stage offset (one add per base) and the scalar copy sources move.
+// The products are computed transposed, C^T block = B^T A^T (v_mfma_f32_32x32x16_bf16), so
+// that a lane's accumulators hold one row of C at 4 consecutive columns per register group:
+// the epilogue reads bias / residual and writes C in 8-byte pieces per row without an LDS
+// round trip.  An operand whose k index is contiguous in memory (A of NN / NT, B of NT) sits in
+// LDS as [rows][32 k] and is read 16 bytes per lane; one whose k index runs over rows (B of
+// NN / TN, A of TN) sits as [32 k][cols] and is read with the transposing ds_read_b64_tr_b16,
+// the supplier rows chosen so that both operands use the natural k order of the instruction
+// (lane half hf holds k = 8 hf .. 8 hf + 7).  Both layouts are swizzled so that every operand
+// read and every copy is free of bank conflicts.
+#include <type_traits>
+
 #include "mtgr_device.h"
 #include "mtgr_internal.h"
 
@@ -29,29 +40,38 @@ namespace {
 
 constexpr int GBM = 256, GBN = 128, GBK = 32, GSTAGES = 3;
 constexpr int A_ELEMS = GBM * GBK, B_ELEMS = GBN * GBK;
+constexpr uint32_t A_BYTES = A_ELEMS * 2, B_BYTES = B_ELEMS * 2;     // one stage of each operand
+constexpr int QA = A_ELEMS / 8 / 256, QB = B_ELEMS / 8 / 256;         // copy instructions per wave
+constexpr int NI = QA + QB;                                          // ... per stage
+constexpr int NBN = 2, NBM = 4;                                      // 32 x 32 blocks per wave (n, m)
 
-// Operand read from a [32 k][cols] tile (CPR 16-byte chunks per row): lane l receives column
-// c0 + l % 32 at k rows k0 + 8 hf + 0..7 (hf = l / 32), the natural k order of the MFMA operand.
-template <int CPR>
-__device__ __forceinline__ bf16x8 kr_read(const uint16_t* tile, int k0, int c0, int lane) {
-    const int j = lane & 15, hf = lane >> 5;
-    const int row = k0 + 8 * hf + (j >> 2);
-    const int colx = c0 + 16 * ((lane >> 4) & 1) + 4 * (j & 3);
-    const uint16_t* p0 = tile + 8 * tile_chunk<CPR>(row, colx >> 3) + (colx & 7);
-    const uint16_t* p1 = tile + 8 * tile_chunk<CPR>(row + 4, colx >> 3) + (colx & 7);
-    const short4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4*)p0);
-    const short4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4*)p1);
-    const short __attribute__((ext_vector_type(8))) v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-    return __builtin_bit_cast(bf16x8, v);
-}
-
-// Operand read from a [rows][32 k] tile: row r, k16 step ks, natural k order.
-__device__ __forceinline__ bf16x8 kc_read(const uint16_t* tile, int r, int ks, int lane) {
-    return tile_read8<4>(tile, r, 2 * ks + (lane >> 5));
-}
+template <int V>
+using IC = std::integral_constant<int, V>;
 
 __device__ __forceinline__ float silu(float z) {
     return z * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-1.4426950408889634f * z));
+}
+
+// Wait until this wave's copies of the stage about to be read have landed, with `later` (0 or
+// 1) stages issued after it still in flight.
+__device__ __forceinline__ void wait_stage(int later) {
+    if (later >= 1) wait_vmcnt<NI>();
+    else wait_vmem();
+}
+
+// Instruction order of one half step: the scheduler alternates one LDS read with one MFMA
+// while both last, then issues the rest (left alone it issues the reads after the MFMAs, so
+// that the next half waits for them).
+template <int READS, int MFMAS>
+__device__ __forceinline__ void interleave_reads() {
+    constexpr int P = READS < MFMAS ? READS : MFMAS;
+#pragma unroll
+    for (int k = 0; k < P; k++) {
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);    // one LDS read
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);    // one MFMA
+    }
+    if constexpr (READS > P) __builtin_amdgcn_sched_group_barrier(0x100, READS - P, 0);
+    if constexpr (MFMAS > P) __builtin_amdgcn_sched_group_barrier(0x008, MFMAS - P, 0);
 }
 
 }  // namespace
@@ -61,12 +81,12 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmArgs g) {
     constexpr bool A_KR = LAYOUT == GEMM_TN;      // A stored [K][M]
     constexpr bool B_KR = LAYOUT != GEMM_NT;      // B stored [K][N]
     constexpr bool SPLIT = LAYOUT == GEMM_TN;     // fp32 partials per K split
-    __shared__ __align__(16) uint16_t sA[GSTAGES][A_ELEMS];
-    __shared__ __align__(16) uint16_t sB[GSTAGES][B_ELEMS];
-    __shared__ float sCol[COLSUM ? 2 * GBN : 1];
+    __shared__ __align__(16) uint16_t smA[GSTAGES][A_ELEMS];
+    __shared__ __align__(16) uint16_t smB[GSTAGES][B_ELEMS];
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int col = lane & 31, hf = lane >> 5;
+    const int wm = w & 1, wn = w >> 1;
     // workgroups of one XCD (blockIdx % 8) take the n blocks of one m block one after another,
     // so the A rows of that block stay in the XCD's L2
     const int bid = blockIdx.x, x = bid % XCDS, jx = bid / XCDS;
@@ -76,95 +96,232 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmArgs g) {
     const int split = blockIdx.y;
     const int nks = (int)((g.K + GBK - 1) / GBK);
     const int ks_begin = split * g.ks_per_split;
-    const int ks_end = min(nks, ks_begin + g.ks_per_split);
-    const int nk = max(ks_end - ks_begin, 0);
-    const uint16_t* A = (const uint16_t*)g.A;
-    const uint16_t* B = (const uint16_t*)g.B;
+    const int nk = min(nks, ks_begin + g.ks_per_split) - ks_begin;     // >= 1 by the plan
     const bool colsum = COLSUM && mb == 0;
+    const int M = (int)g.M, N = (int)g.N, K = (int)g.K;
 
-    auto issue = [&](int i) {
-        const int st = i % GSTAGES;
-        const int k0 = (ks_begin + i) * GBK;
-        if constexpr (A_KR) tile_dma<GBM, GBK>(sA[st], A, g.lda, k0, (int)g.K, m0, tid);
-        else tile_dma<GBK, GBM>(sA[st], A, g.lda, m0, (int)g.M, k0, tid);
-        if constexpr (B_KR) tile_dma<GBN, GBK>(sB[st], B, g.ldb, k0, (int)g.K, n0, tid);
-        else tile_dma<GBK, GBN>(sB[st], B, g.ldb, n0, (int)g.N, k0, tid);
+    // ---- copies: per-lane offsets computed once; per step only scalar bases move.
+    // Instruction q of wave w fills LDS block 4 q + w (1 KB) of a tile (tile_dma's layout).
+    const uint32_t wblk = __builtin_amdgcn_readfirstlane((uint32_t)w * 1024u);
+    const uint32_t ldsA = lds_address(&smA[0][0]) + wblk;
+    const uint32_t ldsB = lds_address(&smB[0][0]) + wblk;
+    // [rows][32 k] tile (4 chunks per row, 64 rows per instruction): rows past `valid` clamp
+    auto kc_offsets = [&](uint32_t* vo, int nq, long long ld, int valid) {
+        const int rl = w * 16 + (lane >> 2);
+        const int c = (lane & 3) ^ swz<4>(rl);
+        for (int q = 0; q < nq; q++) vo[q] = (uint32_t)(min(64 * q + rl, valid - 1) * ld + 8 * c) * 2u;
     };
-    constexpr int NI = GBM * GBK / 8 / 256 + GBN * GBK / 8 / 256;   // copy instructions per stage
+    // [32 k][cols] tile (CPR chunks per row, 256 / CPR rows per instruction): columns past
+    // `cvalid` clamp, rows past `rvalid` clamp (the last step of a ragged K only)
+    auto kr_offsets = [&](auto cprc, uint32_t* vo, long long ld, int cvalid, int rvalid) {
+        constexpr int CPR = decltype(cprc)::value, RPI = 256 / CPR, NQ = 32 * CPR / 256;
+        const int rl = w * (64 / CPR) + lane / CPR;
+#pragma unroll
+        for (int q = 0; q < NQ; q++) {
+            const int c = min((lane % CPR) ^ swz<CPR>(RPI * q + rl), (cvalid >> 3) - 1);
+            vo[q] = (uint32_t)(min(RPI * q + rl, rvalid - 1) * ld + 8 * c) * 2u;
+        }
+    };
+    uint32_t voA[QA], voB[QB];
+    if constexpr (A_KR) kr_offsets(IC<GBM / 8>{}, voA, g.lda, M - m0, GBK);
+    else kc_offsets(voA, QA, g.lda, min(GBM, M - m0));
+    if constexpr (B_KR) kr_offsets(IC<GBN / 8>{}, voB, g.ldb, N - n0, GBK);
+    else kc_offsets(voB, QB, g.ldb, min(GBN, N - n0));
+    // source of the next k step to copy: k-contiguous operands move 32 columns, k-row operands
+    // 32 rows; the copies are issued in k order, so the pointers only advance
+    const char* pa = (const char*)g.A + 2 * (A_KR ? (long long)m0 : (long long)m0 * g.lda);
+    const char* pb = (const char*)g.B + 2 * (B_KR ? (long long)n0 : (long long)n0 * g.ldb);
+    const long long stepA = 2ll * (A_KR ? GBK * g.lda : GBK), stepB = 2ll * (B_KR ? GBK * g.ldb : GBK);
+    pa += ks_begin * stepA;
+    pb += ks_begin * stepB;
 
-    floatx16 acc[4][2];
+    auto issue = [&](int st, int i) {
+        uint32_t ra[QA], rb[QB];
 #pragma unroll
-    for (int a = 0; a < 4; a++)
+        for (int q = 0; q < QA; q++) ra[q] = voA[q];
 #pragma unroll
-        for (int b = 0; b < 2; b++)
-#pragma unroll
-            for (int r = 0; r < 16; r++) acc[a][b][r] = 0.f;
-    float csum = 0.f;
-
-    if (nk > 0) issue(0);
-    if (nk > 1) issue(1);
-    for (int i = 0; i < nk; i++) {
-        const int st = i % GSTAGES;
-        if (i + 1 < nk) wait_vmcnt<NI>(); else wait_vmem();
-        const int k0 = (ks_begin + i) * GBK;
+        for (int q = 0; q < QB; q++) rb[q] = voB[q];
         if constexpr (A_KR) {
-            // the last k step of a ragged K: rows past K hold copies of row K - 1 (the copy
-            // clamps); zero them in both tiles so that they add nothing
-            const int valid = (int)min(g.K - k0, (long long)GBK);
+            const int k0 = (ks_begin + i) * GBK;
+            if (k0 + GBK > K) {               // ragged last step: clamp the k rows
+                kr_offsets(IC<GBM / 8>{}, ra, g.lda, M - m0, K - k0);
+                kr_offsets(IC<GBN / 8>{}, rb, g.ldb, N - n0, K - k0);
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < QA; q++) lds_dma16(ldsA + (uint32_t)st * A_BYTES + 4096u * q, pa, ra[q]);
+#pragma unroll
+        for (int q = 0; q < QB; q++) lds_dma16(ldsB + (uint32_t)st * B_BYTES + 4096u * q, pb, rb[q]);
+        pa += stepA;
+        pb += stepB;
+    };
+    // The last k step of a ragged K (TN only): rows past K hold copies of row K - 1; zero them
+    // in both tiles so that they add nothing, then hand the stage over again.
+    auto zero_tail = [&](int st, int i) {
+        if constexpr (A_KR) {
+            const int valid = K - (ks_begin + i) * GBK;
             if (valid < GBK) {
-                lds_barrier();
-                uint4* za = (uint4*)sA[st];
-                uint4* zb = (uint4*)sB[st];
+                uint4* za = (uint4*)smA[st];
+                uint4* zb = (uint4*)smB[st];
                 for (int c = tid; c < (GBK - valid) * (GBM / 8); c += 256) za[valid * (GBM / 8) + c] = make_uint4(0, 0, 0, 0);
                 for (int c = tid; c < (GBK - valid) * (GBN / 8); c += 256) zb[valid * (GBN / 8) + c] = make_uint4(0, 0, 0, 0);
+                lds_barrier();
             }
         }
-        lds_barrier();
-        if (i + 2 < nk) issue(i + 2);      // into the stage read in step i - 1
-        const uint16_t* tA = sA[st];
-        const uint16_t* tB = sB[st];
+    };
+
+    // ---- operand reads: per-lane LDS addresses computed once; k16 step and block offsets go
+    // into the 16-bit immediate of each ds_read, the stage offset into a per-step add.
+    // k-contiguous operand rows r0 + 32 b: chunk (2 ks + hf) ^ swz(r0) (the swizzle depends on
+    // the row mod 16 only), block b at + 2048 b bytes
+    auto kc_base = [&](int r0, int ks) { return 16u * (uint32_t)(r0 * 4 + ((2 * ks + hf) ^ swz<4>(r0))); };
+    // k-row operand column block c0 (CPR chunks per row), supplier rows of k16 step 0 (step 1:
+    // 16 rows further, + 256 CPR bytes)
+    auto kr_base = [&](auto cprc, int c0, int part) {
+        constexpr int CPR = decltype(cprc)::value;
+        const int j = lane & 15;
+        const int row = 8 * hf + (j >> 2) + 4 * part;
+        const int colx = c0 + 16 * ((lane >> 4) & 1) + 4 * (j & 3);
+        return 16u * (uint32_t)tile_chunk<CPR>(row, colx >> 3) + 2u * (uint32_t)(colx & 7);
+    };
+    constexpr uint32_t KS_A = 256u * (GBM / 8), KS_B = 256u * (GBN / 8);     // k16 step of a k-row tile
+    // bases: kr [block][supplier half]; kc [0][k16 step]
+    uint32_t rbA[NBM][2], rbB[NBN][2];
+    const uint32_t lA = lds_address(&smA[0][0]), lB = lds_address(&smB[0][0]);
+#pragma unroll
+    for (int h = 0; h < 2; h++) {
+#pragma unroll
+        for (int q = 0; q < NBM; q++)
+            rbA[q][h] = lA + (A_KR ? kr_base(IC<GBM / 8>{}, 128 * wm + 32 * q, h) : kc_base(128 * wm + col, h));
+#pragma unroll
+        for (int q = 0; q < NBN; q++)
+            rbB[q][h] = lB + (B_KR ? kr_base(IC<GBN / 8>{}, 64 * wn + 32 * q, h) : kc_base(64 * wn + col, h));
+    }
+    typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
+    auto rd16 = [&](uint32_t addr) { return *(const lds_bf16x8*)(uintptr_t)addr; };
+    auto rdtr = [&](uint32_t o0, uint32_t o1) {
+        const short4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4*)(uintptr_t)o0);
+        const short4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4*)(uintptr_t)o1);
+        const short __attribute__((ext_vector_type(8))) v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+        return __builtin_bit_cast(bf16x8, v);
+    };
+    // stage-shifted copies of the read bases: `cur` for the stage being computed, `nxt` for the
+    // next one (one VALU add per base and step)
+    uint32_t curA[NBM][2], curB[NBN][2], nxtA[NBM][2], nxtB[NBN][2];
+    auto shift = [&](uint32_t (&dA)[NBM][2], uint32_t (&dB)[NBN][2], int st) {
+#pragma unroll
+        for (int h = 0; h < 2; h++) {
+#pragma unroll
+            for (int q = 0; q < NBM; q++)
+                if (A_KR || q == 0) dA[q][h] = rbA[q][h] + (uint32_t)st * A_BYTES;
+#pragma unroll
+            for (int q = 0; q < NBN; q++)
+                if (B_KR || q == 0) dB[q][h] = rbB[q][h] + (uint32_t)st * B_BYTES;
+        }
+    };
+    auto read_ops = [&](bf16x8* ao, bf16x8* bo, const uint32_t (&bA)[NBM][2], const uint32_t (&bB)[NBN][2],
+                        auto ksc) {
+        constexpr uint32_t KS = decltype(ksc)::value;
+#pragma unroll
+        for (int a = 0; a < NBN; a++) {
+            if constexpr (B_KR) ao[a] = rdtr(bB[a][0] + KS * KS_B, bB[a][1] + KS * KS_B);
+            else ao[a] = rd16(bB[0][KS] + 2048u * a);
+        }
+#pragma unroll
+        for (int b = 0; b < NBM; b++) {
+            if constexpr (A_KR) bo[b] = rdtr(bA[b][0] + KS * KS_A, bA[b][1] + KS * KS_A);
+            else bo[b] = rd16(bA[0][KS] + 2048u * b);
+        }
+    };
+
+    floatx16 acc[NBN][NBM];
+#pragma unroll
+    for (int a = 0; a < NBN; a++)
+#pragma unroll
+        for (int b = 0; b < NBM; b++)
+#pragma unroll
+            for (int r = 0; r < 16; r++) acc[a][b][r] = 0.f;
+    float csum[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    auto mfmas = [&](const bf16x8* ao, const bf16x8* bo) {
+#pragma unroll
+        for (int a = 0; a < NBN; a++)
+#pragma unroll
+            for (int b = 0; b < NBM; b++)
+                acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ao[a], bo[b], acc[a][b], 0, 0, 0);
+    };
+    auto colsum_step = [&](int st) {
         if (COLSUM && colsum) {
-            // bias gradient: column sums of B over this K split (two threads per column)
-            const int c = tid & (GBN - 1), h = tid >> 7;
-#pragma unroll 4
-            for (int r = 16 * h; r < 16 * h + 16; r++)
-                csum += bf16_to_f32(tB[8 * tile_chunk<GBN / 8>(r, c >> 3) + (c & 7)]);
-        }
+            // bias gradient: column sums of B over this K split, 8 columns x 2 rows per thread
+            const int c = tid & 15, rg = tid >> 4;
 #pragma unroll
-        for (int ks = 0; ks < GBK / 16; ks++) {
-            bf16x8 aop[4], bop[2];
+            for (int r = 2 * rg; r < 2 * rg + 2; r++) {
+                const bf16x8 v = tile_read8<GBN / 8>(smB[st], r, c);
 #pragma unroll
-            for (int a = 0; a < 4; a++) {
-                if constexpr (B_KR) aop[a] = kr_read<GBN / 8>(tB, 16 * ks, 32 * a, lane);
-                else aop[a] = kc_read(tB, 32 * a + col, ks, lane);
+                for (int e = 0; e < 8; e++) csum[e] += (float)v[e];
             }
-#pragma unroll
-            for (int b = 0; b < 2; b++) {
-                if constexpr (A_KR) bop[b] = kr_read<GBM / 8>(tA, 16 * ks, 64 * w + 32 * b, lane);
-                else bop[b] = kc_read(tA, 64 * w + 32 * b + col, ks, lane);
-            }
-#pragma unroll
-            for (int a = 0; a < 4; a++)
-#pragma unroll
-                for (int b = 0; b < 2; b++)
-                    acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(aop[a], bop[b], acc[a][b], 0, 0, 0);
         }
+    };
+
+    bf16x8 a0[NBN], b0[NBM], a1[NBN], b1[NBM];
+    // LDS reads per operand set: 2 per transposed operand, 1 per k-contiguous one
+    constexpr int READS = NBM * (A_KR ? 2 : 1) + NBN * (B_KR ? 2 : 1);
+
+    issue(0, 0);
+    if (nk > 1) issue(1, 1);
+    if (nk > 2) issue(2, 2);
+    const int later0 = min(nk - 1, GSTAGES - 1);      // stages issued after stage 0
+    if (later0 == 2) wait_vmcnt<2 * NI>();
+    else wait_stage(later0);
+    lds_barrier();
+    if (nk == 1) zero_tail(0, 0);
+    shift(curA, curB, 0);
+    read_ops(a0, b0, curA, curB, IC<0>{});
+    // One k step per iteration.  The second half's operands are read under the first half's
+    // MFMAs, and the next stage's first operands under the second half's; the waits are ones
+    // the compiler sees, so it adds none of its own in front of the MFMAs.  No MFMA sits in a
+    // branch (the accumulators stay in place): after the last step the next-stage reads touch
+    // a stale slot and are not used, and the hand-over barrier is harmless.
+    int st = 0, nx = 1;
+    for (int i = 0; i < nk; i++) {
+        wait_lgkm_seen();                       // a0 / b0 (read a half step ago) have landed
+        colsum_step(st);
+        read_ops(a1, b1, curA, curB, IC<1>{});
+        shift(nxtA, nxtB, nx);
+        mfmas(a0, b0);
+        interleave_reads<READS, NBN * NBM>();
+        wait_stage(min(nk - 2 - i, 1));
+        lds_barrier_seen();                     // stage i + 1 visible; every wave done with stage i
+        if (i + GSTAGES < nk) issue(st, i + GSTAGES);     // into the slot of stage i
+        if (A_KR && i + 2 == nk) zero_tail(nx, i + 1);
+        read_ops(a0, b0, nxtA, nxtB, IC<0>{});
+        mfmas(a1, b1);
+        interleave_reads<READS, NBN * NBM>();
+#pragma unroll
+        for (int h = 0; h < 2; h++) {
+#pragma unroll
+            for (int q = 0; q < NBM; q++) curA[q][h] = nxtA[q][h];
+#pragma unroll
+            for (int q = 0; q < NBN; q++) curB[q][h] = nxtB[q][h];
+        }
+        st = nx;
+        nx = nx == GSTAGES - 1 ? 0 : nx + 1;
     }
 
-    // acc[a][b] holds C^T of rows n0 + 32 a + 8 (r / 4) + 4 hf + r % 4, columns m0 + 64 w + 32 b + col:
-    // lane row gm of C, columns gn .. gn + 3 per register group q = r / 4.
+    // acc[a][b] holds C^T of rows n0 + 64 wn + 32 a + 8 (r / 4) + 4 hf + r % 4, columns
+    // m0 + 128 wm + 32 b + col: lane row gm of C, columns gn .. gn + 3 per register group q = r / 4.
 #pragma unroll
-    for (int b = 0; b < 2; b++) {
-        const long long gm = m0 + 64 * w + 32 * b + col;
-        if (gm >= g.M) continue;
+    for (int b = 0; b < NBM; b++) {
+        const long long gm = m0 + 128 * wm + 32 * b + col;
+        if (gm >= M) continue;
 #pragma unroll
-        for (int a = 0; a < 4; a++) {
+        for (int a = 0; a < NBN; a++) {
 #pragma unroll
             for (int q = 0; q < 4; q++) {
-                const int gn = n0 + 32 * a + 8 * q + 4 * hf;
+                const int gn = n0 + 64 * wn + 32 * a + 8 * q + 4 * hf;
+                if (gn >= N) continue;
                 float v[4] = {acc[a][b][4 * q], acc[a][b][4 * q + 1], acc[a][b][4 * q + 2], acc[a][b][4 * q + 3]};
                 if constexpr (SPLIT) {
-                    float* P = g.partial + ((long long)split * g.M + gm) * g.N + gn;
+                    float* P = g.partial + ((long long)split * M + gm) * N + gn;
                     *(float4*)P = make_float4(v[0], v[1], v[2], v[3]);
                     continue;
                 }
@@ -188,11 +345,23 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmArgs g) {
                 }
             }
         }
+        // one 32-row block at a time: the epilogue's loads are not hoisted across blocks
+        __builtin_amdgcn_sched_barrier(0);
     }
     if (COLSUM && colsum) {
-        sCol[tid] = csum;
-        __syncthreads();
-        if (tid < GBN) g.colsum_partial[(long long)split * g.N + n0 + tid] = sCol[tid] + sCol[tid + GBN];
+        // the 16 row groups' sums of each column, added through LDS (stage memory is free now)
+        lds_barrier();
+        float* red = (float*)smA[0];                // [16 row groups][128 columns]
+        const int c = tid & 15, rg = tid >> 4;
+#pragma unroll
+        for (int e = 0; e < 8; e++) red[rg * GBN + 8 * c + e] = csum[e];
+        lds_barrier();
+        if (tid < GBN) {
+            float s = 0.f;
+#pragma unroll
+            for (int r = 0; r < 16; r++) s += red[r * GBN + tid];
+            if (n0 + tid < N) g.colsum_partial[(long long)split * N + n0 + tid] = s;
+        }
     }
 }
 
@@ -221,7 +390,7 @@ __global__ __launch_bounds__(256) void gemm_split_reduce_kernel(GemmArgs g) {
 void gemm_plan(int layout, long long M, long long N, long long K, int* mblocks, int* nblocks, int* splits,
                int* ks_per_split) {
     *mblocks = (int)((M + GBM - 1) / GBM);
-    *nblocks = (int)(N / GBN);
+    *nblocks = (int)((N + GBN - 1) / GBN);
     const int nks = (int)((K + GBK - 1) / GBK);
     int s = 1;
     if (*mblocks == 0 || *nblocks == 0 || nks == 0) {     // empty product: nothing is launched

@@ -318,6 +318,20 @@ __device__ __forceinline__ void wait_vmcnt_seen() {
     asm volatile("" ::: "memory");
 }
 
+// This wave's LDS operations (and scalar loads) have completed, as a real s_waitcnt that the
+// compiler's counter bookkeeping sees: reads issued before it need no further wait.
+__device__ __forceinline__ void wait_lgkm_seen() {
+    __builtin_amdgcn_s_waitcnt(0xC07F);      // lgkmcnt(0); vmcnt and expcnt at their maxima
+    asm volatile("" ::: "memory");
+}
+
+// lds_barrier with the LDS wait visible to the compiler (see wait_lgkm_seen).
+__device__ __forceinline__ void lds_barrier_seen() {
+    wait_lgkm_seen();
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
 // Workgroup barrier for LDS hand-offs: this wave's LDS reads and writes have completed, and
 // no other wave passes until all waves arrive.  Copies into LDS must be waited for first.
 __device__ __forceinline__ void lds_barrier() {
@@ -367,9 +381,13 @@ __device__ __forceinline__ bf16x8 lds_read_tr(const uint16_t* tile, uint32_t o0,
 // the source chunk alternates between even and odd instructions.  Each instruction needs one
 // wave-uniform base address and one per-lane 32-bit offset.  The caller guarantees
 // ROWS * ld * 2 < 2^31.
-template <int DH, int ROWS = 64>
+//
+// With CLAMP_COLS, columns at or past `ncols` (a multiple of 8, > col0) are replaced by the
+// last valid 16-byte chunk of the row: the copy stays inside the matrix, and the tile columns
+// past the edge hold values that the caller never stores.
+template <int DH, int ROWS = 64, bool CLAMP_COLS = false>
 __device__ __forceinline__ void tile_dma(uint16_t* tile, const uint16_t* base, long long ld, int row0,
-                                         int nrows, int col0, int tid) {
+                                         int nrows, int col0, int tid, int ncols = 0) {
     constexpr int CPR = DH / 8, RPI = 256 / CPR, NCH = ROWS * CPR;
     static_assert(NCH % 64 == 0, "whole LDS blocks");
     // The per-lane offsets are recomputed at every call (a few VALU instructions) rather than
@@ -380,7 +398,9 @@ __device__ __forceinline__ void tile_dma(uint16_t* tile, const uint16_t* base, l
     const int rl = w * (64 / CPR) + lane / CPR;             // row within block 0 of this wave
     // source chunk of the lane in instruction i (tile row i * RPI + rl)
     auto src_chunk = [&](int i) {
-        return (lane % CPR) ^ swz<CPR>(RPI % 16 == 0 ? rl : i * RPI + rl);
+        const int c = (lane % CPR) ^ swz<CPR>(RPI % 16 == 0 ? rl : i * RPI + rl);
+        if constexpr (CLAMP_COLS) return min(c, ((ncols - col0) >> 3) - 1);
+        else return c;
     };
     const uint16_t* tbase = base + (long long)row0 * ld + col0;
     const uint32_t ltile = __builtin_amdgcn_readfirstlane(lds_address(tile) + (uint32_t)w * 1024u);

@@ -462,10 +462,10 @@ def gemm(layout=NN, M=512, N=256, K=256, A=FAKE, lda=None, B=FAKE, ldb=None, C=F
 @pytest.mark.parametrize("kw, status", [
     (dict(layout=3), hstu.MTGR_ERROR_INVALID_ARGUMENT),
     (dict(epilogue=3), hstu.MTGR_ERROR_INVALID_ARGUMENT),
-    (dict(N=200), hstu.MTGR_ERROR_UNSUPPORTED),                        # N % 128
+    (dict(N=204), hstu.MTGR_ERROR_UNSUPPORTED),                        # N % 8
     (dict(K=100), hstu.MTGR_ERROR_UNSUPPORTED),                        # NN: K % 32
     (dict(layout=NT, K=48), hstu.MTGR_ERROR_UNSUPPORTED),
-    (dict(layout=TN, M=300), hstu.MTGR_ERROR_UNSUPPORTED),             # TN: M % 256
+    (dict(layout=TN, M=300), hstu.MTGR_ERROR_UNSUPPORTED),             # TN: M % 8
     (dict(layout=TN, epilogue=EPI_SILU, bias=FAKE, C2=FAKE, ldc2=256), hstu.MTGR_ERROR_UNSUPPORTED),
     (dict(K=0), hstu.MTGR_ERROR_UNSUPPORTED),
     (dict(M=-1), hstu.MTGR_ERROR_INVALID_ARGUMENT),
@@ -497,11 +497,11 @@ def test_gemm_empty_output_is_a_noop():
 def test_gemm_workspace_sizes():
     assert hstu.mtgr_gemm_workspace_size(NN, 4096, 2048, 512) == 0
     assert hstu.mtgr_gemm_workspace_size(NT, 4096, 512, 2048) == 0
-    # weight gradient of the projection at 2^20 tokens, d = 512: one 256 x 128 tile per
-    # (m, n) block, enough K splits for two workgroups per CU, fp32 partials plus column sums
+    # weight gradient of the projection at 2^20 tokens, d = 512: one 256 x 256 tile per
+    # (m, n) block, enough K splits for one workgroup per CU, fp32 partials plus column sums
     ws = hstu.mtgr_gemm_workspace_size(TN, 512, 2048, 1 << 20)
-    tiles = 2 * 16
-    splits = -(-512 // tiles)
+    tiles = 2 * 8
+    splits = -(-256 // tiles)
     assert ws >= splits * (512 * 2048 + 2048) * 4
     # a short K is not split
     assert hstu.mtgr_gemm_workspace_size(TN, 256, 128, 40) == (256 * 128 + 128) * 4

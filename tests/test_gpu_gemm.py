@@ -74,6 +74,8 @@ def product_ref(layout, A, B):
     ("nt", 999, 256, 1024), ("nt", 37, 512, 2048), ("nt", 4096, 1024, 4096),
     ("tn", 256, 1024, 1000), ("tn", 512, 128, 17), ("tn", 256, 128, 40000), ("tn", 768, 3072, 4099),
     ("tn", 1024, 4096, 1),
+    # edges that are not whole 256 x 256 tiles: N, and M of A^T B, only multiples of 8
+    ("nn", 300, 136, 64), ("nt", 513, 264, 96), ("tn", 264, 1000, 777), ("tn", 8, 8, 5),
 ])
 def test_gemm_plain(layout, M, N, K):
     say(f"[gemm] plain {layout} M={M} N={N} K={K}")
@@ -152,7 +154,7 @@ def test_gemm_strided_operands():
     ops.gemm(A, B, "nn", out=C)
     Bt = rand_bf16((N, K), 14, cols=K + 32)
     D = ops.gemm(A, Bt, "nt")
-    At = rand_bf16((K, M - 88), 15, cols=M + 40)           # TN: M a multiple of 256 -> 512
+    At = rand_bf16((K, M - 88), 15, cols=M + 40)
     G = rand_bf16((K, N), 16, cols=4 * N)
     cs = torch.empty(N, device="cuda")
     E = ops.gemm(At, G, "tn", colsum=cs)

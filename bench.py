@@ -61,17 +61,31 @@ def candidate_pairs(layout) -> np.ndarray:
     return out
 
 
-def source_hash() -> str:
+# The sources each kernel is compiled from (its own file plus the shared device headers): a
+# counter figure stays valid while none of them changes.
+KERNEL_SOURCES = {
+    "attn_fwd_bf16_kernel": ["attn_fwd.hip"],
+    "attn_bwd_dkdv_bf16_kernel": ["attn_bwd_dkdv.hip", "attn_bwd_common.h"],
+    "attn_bwd_dq_ds_bf16_kernel": ["attn_bwd_dqds.hip", "attn_bwd_common.h"],
+    "gln_fwd_kernel": ["group_ln.hip"],
+    "gln_bwd_kernel": ["group_ln.hip"],
+    "gemm_bf16_kernel": ["gemm.hip"],
+}
+SHARED_SOURCES = ["mtgr_device.h", "mtgr_internal.h"]
+
+
+def source_hash(kernel: str) -> str:
     h = hashlib.sha256()
-    for name in sorted(os.listdir(CSRC)):
+    for name in sorted(KERNEL_SOURCES[kernel] + SHARED_SOURCES):
         with open(os.path.join(CSRC, name), "rb") as f:
             h.update(name.encode() + f.read())
     return h.hexdigest()[:16]
 
 
-def measured_traffic(kernel: str, workload: str):
-    """HBM bytes per launch from the committed rocprofv3 counter runs, if they were taken
-    on the current kernel sources (else None)."""
+def measured_traffic(kernel: str, workload: str, field: str = "bytes_per_launch"):
+    """HBM bytes per launch (or another counter-derived figure of the kernel, such as its
+    effective shader clock) from the committed rocprofv3 counter runs, if they were taken on the
+    current kernel sources (else None)."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
     try:
         with open(path) as f:
@@ -79,9 +93,9 @@ def measured_traffic(kernel: str, workload: str):
     except (OSError, ValueError):
         return None
     entry = data.get(f"{kernel}@{workload}")
-    if not entry or entry.get("source_hash") != source_hash():
+    if not entry or entry.get("source_hash") != source_hash(kernel):
         return None
-    return entry.get("bytes_per_launch")
+    return entry.get(field)
 
 
 def cpu_baseline(layout, budget_s: float):
@@ -109,10 +123,40 @@ def cpu_baseline(layout, budget_s: float):
     tokens = int(sum(layout.offsets[b + 1] - layout.offsets[b] for b in chosen))
     threads = int(os.environ.get("OMP_NUM_THREADS", 0)) or len(os.sched_getaffinity(0))
     return {"value": tokens / t, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "cpu_model": cpu_model(), "cpus_visible": len(os.sched_getaffinity(0)),
             "sample": f"{len(chosen)} of {layout.num_users} users ({tokens} tokens, "
                       f"{int(pairs[chosen].sum())} visible pairs x {H} heads), same path fwd+bwd, "
                       f"fp64, {t:.1f} s",
             "seconds": round(t, 2)}
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+NOMINAL_MHZ = 2400.0      # the clock at which the published MI355X peaks are quoted
+
+
+def shader_clock_mhz(seconds: float = 0.05) -> float:
+    """Shader clock while every CU's matrix cores are busy (mtgr_debug_clock_probe: a back-to-
+    back MFMA loop per workgroup, shader-clock cycles over constant-rate ticks), median over
+    the workgroups.  Run right after the timed region, on a GPU at its working temperature."""
+    import torch
+    from paper_2505_18654_amd import hstu
+    blocks = torch.cuda.get_device_properties(0).multi_processor_count
+    out = torch.zeros(3 * blocks, dtype=torch.int64, device="cuda")
+    iters = max(int(seconds * NOMINAL_MHZ * 1e6 / 128), 1)        # 4 MFMAs of 32 cycles each
+    khz = hstu.mtgr_debug_clock_probe(iters, blocks, out)
+    torch.cuda.synchronize()
+    o = out.view(blocks, 3).cpu().numpy().astype(np.float64)
+    return float(np.median(o[:, 0] / o[:, 1] * khz / 1e3))
 
 
 def _oracle_step(layout, users) -> float:
@@ -235,7 +279,11 @@ def main():
     ws = ops.workspace_for(ops.attn_problem(jag, q, k, v, o, rab), "cuda", backward=not fwd_only)
     gws = ops.gln_workspace(y, gamma.shape[0])
 
-    # backward: the dK/dV kernel stores dS, then dQ is formed from it (two calls, timed apart)
+    # backward: on the matrix-core path the dK/dV kernel stores dS, then dQ is formed from it
+    # (two calls, timed apart); on the vector path (fp32, or bf16 with head_dim 16) the two
+    # kernels each recompute S and dP
+    mfma_path = spec.dtype == "bf16" and dh in (32, 64, 128)
+    part_dkdv, part_dq = ("dkdv_keep_ds", "dq_from_ds") if mfma_path else ("dkdv", "dq")
     stages = ["plan", "attn_fwd", "gln_fwd"] + ([] if fwd_only else ["gln_bwd", "attn_bwd_dkdv", "attn_bwd_dq"])
 
     def run(name):
@@ -250,10 +298,10 @@ def main():
                         workspace=gws)
         elif name == "attn_bwd_dkdv":
             ops.attn_bwd(q, k, v, dx.view(T, H, dh), jag, rab, grads=(dq, dk, dv, drab), workspace=ws,
-                         planned=True, parts="dkdv_keep_ds")
+                         planned=True, parts=part_dkdv)
         elif name == "attn_bwd_dq":
             ops.attn_bwd(q, k, v, dx.view(T, H, dh), jag, rab, grads=(dq, dk, dv, drab), workspace=ws,
-                         planned=True, parts="dq_from_ds")
+                         planned=True, parts=part_dq)
 
     for _ in range(args.warmup):
         for s in stages:
@@ -283,13 +331,31 @@ def main():
     # algorithmic split of F_bwd = 8 dh per pair: the dK/dV kernel forms dP, dV and dK (6 dh),
     # the dQ kernel dQ (2 dh); recomputation of S is not counted
     kflops = {"attn_fwd": f_fwd, "attn_bwd_dkdv": f_bwd * 3 / 4, "attn_bwd_dq": f_bwd / 4}
-    kname = {"attn_fwd": "attn_fwd_bf16_kernel", "attn_bwd_dq": "attn_bwd_dq_ds_bf16_kernel",
-             "attn_bwd_dkdv": "attn_bwd_dkdv_bf16_kernel"}
+    if mfma_path:
+        kname = {"attn_fwd": "attn_fwd_bf16_kernel", "attn_bwd_dq": "attn_bwd_dq_ds_bf16_kernel",
+                 "attn_bwd_dkdv": "attn_bwd_dkdv_bf16_kernel"}
+        bound, peak = "mfma", PEAK_BF16
+    else:   # fp32 vector FMAs (the published fp32 vector peak: 256 CUs x 128 FMA lanes x 2 x 2.4 GHz)
+        kname = {"attn_fwd": "attn_fwd_vec_kernel", "attn_bwd_dq": "attn_bwd_dq_vec_kernel",
+                 "attn_bwd_dkdv": "attn_bwd_dkdv_vec_kernel"}
+        bound, peak = "alu", PEAK_FP32
     dom = max((s for s in kflops if s in stage_ms), key=lambda s: stage_ms[s])
     achieved = kflops[dom] / (stage_ms[dom] * 1e-3)
-    roofline = {"bound": "mfma", "kernel": kname[dom], "achieved": achieved / 1e12, "peak": PEAK_BF16 / 1e12,
-                "unit": "TFLOP/s", "frac": achieved / PEAK_BF16,
-                "traffic": measured_traffic(kname[dom], args.workload)}
+    mhz = shader_clock_mhz()
+    peak_clk = peak * mhz / NOMINAL_MHZ
+    roofline = {"bound": bound, "kernel": kname[dom], "achieved": achieved / 1e12, "peak": peak / 1e12,
+                "unit": "TFLOP/s", "frac": achieved / peak,
+                "traffic": measured_traffic(kname[dom], args.workload) if kname[dom] in KERNEL_SOURCES else None,
+                "peak_at_measured_clock": peak_clk / 1e12, "frac_at_measured_clock": achieved / peak_clk}
+    kmhz = measured_traffic(kname[dom], args.workload, "clock_mhz") if kname[dom] in KERNEL_SOURCES else None
+    if kmhz:
+        roofline["frac_at_kernel_clock"] = achieved / (peak * kmhz / NOMINAL_MHZ)
+    clock = {"measured_mhz": round(mhz, 1), "nominal_mhz": NOMINAL_MHZ,
+             "how": "median shader clock over all CUs during a back-to-back MFMA loop run right after "
+                    "the timed region (mtgr_debug_clock_probe)",
+             "dominant_kernel_mhz": kmhz,
+             "dominant_kernel_how": "GRBM_GUI_ACTIVE / 8 over the kernel's dispatch duration in the committed "
+                                    "counter run on the same sources (profiles/traffic.json), or null"}
     gln_bytes = T * (3 * d * 2 + 8) + (0 if fwd_only else T * (5 * d * 2 + 8))
     gln_ms = stage_ms["gln_fwd"] + stage_ms.get("gln_bwd", 0.0)
 
@@ -367,10 +433,12 @@ def main():
                    "rab_buckets": spec.rab_buckets, "pass": "fwd" if fwd_only else "fwd+bwd"},
         "tflops": tflops,
         "pct_bf16_peak": 100.0 * tflops * 1e12 / PEAK_BF16,
+        "pct_of_path_peak": 100.0 * tflops * 1e12 / peak,
         "visible_pairs": pairs,
         "stage_ms": {s: round(v, 4) for s, v in stage_ms.items()},
         "gln": {"bound": "hbm", "achieved_GBps": gln_bytes / (gln_ms * 1e-3) / 1e9, "peak_GBps": PEAK_HBM / 1e9},
         "roofline": roofline,
+        "clock": clock,
         "parity_sampled_fwd": {"users": check_users, "max_err_over_rms": err_lit,
                                "max_err_over_rms_storage_adjusted": err_adj},
     }

@@ -342,6 +342,16 @@ mtgr_status_t mtgr_gemm_bf16(int32_t layout, int64_t M, int64_t N, int64_t K, co
                              float* colsum, void* workspace, size_t workspace_bytes,
                              mtgr_stream_t stream);
 
+/* Measurement aid (no part of the method): the shader clock while the matrix cores are busy.
+ * Launches `blocks` workgroups of 256 threads that each issue `mfma_iterations` x 4
+ * v_mfma_f32_32x32x16_bf16 per wave back to back, and writes per workgroup
+ * out[3 b] = shader-clock cycles and out[3 b + 1] = constant-rate counter ticks around that
+ * loop (out[3 b + 2] is a checksum), device memory, int64, 3 * blocks entries.
+ * *wall_clock_khz (host) receives the constant counter's rate; the clock in kHz is
+ * out[3 b] / out[3 b + 1] * *wall_clock_khz.  blocks in [1, 65536]. */
+mtgr_status_t mtgr_debug_clock_probe(int32_t mfma_iterations, int32_t blocks, int64_t* out,
+                                     int32_t* wall_clock_khz, mtgr_stream_t stream);
+
 /* Bytes of device scratch that mtgr_debug_validate_inputs needs. */
 #define MTGR_VALIDATE_SCRATCH_BYTES 64
 

@@ -21,7 +21,7 @@ LIB_NAME = "libmtgr_hstu.so"
 LIB_PATH = os.path.join(HERE, LIB_NAME)
 SOURCES = ["api.hip", "schedule.hip", "attn_fwd.hip", "attn_bwd.hip", "attn_bwd_dq.hip",
            "attn_bwd_dkdv.hip", "attn_bwd_dqds.hip", "group_ln.hip", "validate.hip",
-           "pointwise.hip", "embedding.hip", "gemm.hip"]
+           "pointwise.hip", "embedding.hip", "gemm.hip", "clock.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 

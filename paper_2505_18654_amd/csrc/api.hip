@@ -780,6 +780,22 @@ mtgr_status_t mtgr_gemm_bf16(int32_t layout, int64_t M, int64_t N, int64_t K, co
     return ok();
 }
 
+mtgr_status_t mtgr_debug_clock_probe(int32_t mfma_iterations, int32_t blocks, int64_t* out,
+                                     int32_t* wall_clock_khz, mtgr_stream_t stream) {
+    if (mfma_iterations < 1 || blocks < 1 || blocks > 65536)
+        return fail(MTGR_ERROR_INVALID_ARGUMENT, "mfma_iterations = %d, blocks = %d", mfma_iterations, blocks);
+    if (!out || !wall_clock_khz) return fail(MTGR_ERROR_NULL_POINTER, "out or wall_clock_khz is NULL");
+    if (((uintptr_t)out & 7u) != 0) return fail(MTGR_ERROR_INVALID_ARGUMENT, "out is not 8-byte aligned");
+    int dev = 0, khz = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev);
+    if (e != hipSuccess) return device_fail(e, "wall clock rate");
+    *wall_clock_khz = khz;
+    e = mtgr::launch_clock_probe(mfma_iterations, blocks, (long long*)out, (hipStream_t)stream);
+    if (e != hipSuccess) return device_fail(e, "clock probe");
+    return ok();
+}
+
 mtgr_status_t mtgr_debug_validate_inputs(const mtgr_hstu_problem_t* p, const int32_t* offsets,
                                          const int8_t* seg, const int8_t* group_ids,
                                          int32_t num_groups, void* scratch, size_t scratch_bytes,

@@ -139,6 +139,7 @@ struct GemmArgs {
     float* colsum_partial;    // TN: [splits][N] fp32 workspace
     int mblocks, nblocks, splits, ks_per_split;
 };
+hipError_t launch_clock_probe(int iters, int blocks, long long* out, hipStream_t s);
 void gemm_plan(int layout, long long M, long long N, long long K, int* mblocks, int* nblocks, int* splits,
                int* ks_per_split);
 size_t gemm_workspace_bytes(int layout, long long M, long long N, long long K);

@@ -45,7 +45,7 @@ EXPORTED = (
     "mtgr_hstu_attn_fwd_noalloc", "mtgr_hstu_attn_fwd_cached",
     "mtgr_group_layernorm_workspace_size", "mtgr_group_layernorm_fwd", "mtgr_group_layernorm_bwd",
     "mtgr_bias_silu_fwd", "mtgr_bias_silu_bwd", "mtgr_add", "mtgr_gemm_workspace_size", "mtgr_gemm_bf16",
-    "mtgr_debug_validate_inputs", "mtgr_status_string", "mtgr_last_error_message", "mtgr_version",
+    "mtgr_debug_validate_inputs", "mtgr_debug_clock_probe", "mtgr_status_string", "mtgr_last_error_message", "mtgr_version",
     "mtgr_embedding_init", "mtgr_embedding_dedup_workspace_size", "mtgr_embedding_dedup",
     "mtgr_embedding_lookup_workspace_size", "mtgr_embedding_lookup", "mtgr_embedding_gather",
     "mtgr_embedding_sgd_workspace_size", "mtgr_embedding_sgd", "mtgr_embedding_evict",
@@ -119,6 +119,7 @@ def lib() -> ctypes.CDLL:
         L.mtgr_bias_silu_fwd.argtypes = [i64, i32, ctypes.c_int, vp, i64, vp, vp, i64, vp]
         L.mtgr_bias_silu_bwd.argtypes = [i64, i32, ctypes.c_int, vp, i64, vp, vp, i64, vp, i64, vp]
         L.mtgr_add.argtypes = [i64, i32, ctypes.c_int, vp, i64, vp, i64, vp, i64, vp]
+        L.mtgr_debug_clock_probe.argtypes = [i32, i32, vp, ctypes.POINTER(i32), vp]
         L.mtgr_gemm_workspace_size.argtypes = [i32, i64, i64, i64, ctypes.POINTER(sz)]
         L.mtgr_gemm_bf16.argtypes = [i32, i64, i64, i64, vp, i64, vp, i64, vp, i64, i32, vp, vp, i64, vp, i64, vp,
                                      vp, sz, vp]
@@ -273,6 +274,15 @@ def mtgr_gemm_bf16(layout, M, N, K, A, lda, B, ldb, C, ldc, epilogue=MTGR_GEMM_E
                                 _ptr(C), int(ldc), int(epilogue), _ptr(bias), _ptr(R), int(ldr), _ptr(C2),
                                 int(ldc2), _ptr(colsum), _ptr(workspace), int(workspace_bytes),
                                 _stream(stream)))
+
+
+def mtgr_debug_clock_probe(mfma_iterations, blocks, out, stream=None) -> int:
+    """Launches the clock probe into `out` (device int64 [3 * blocks]); returns the constant
+    counter's rate in kHz."""
+    khz = ctypes.c_int32(0)
+    _check(lib().mtgr_debug_clock_probe(int(mfma_iterations), int(blocks), _ptr(out), ctypes.byref(khz),
+                                        _stream(stream)))
+    return khz.value
 
 
 def mtgr_debug_validate_inputs(problem, offsets, seg, group_ids, num_groups, scratch, scratch_bytes,

@@ -520,3 +520,14 @@ def test_add_argument_checks():
         hstu.mtgr_add(10, 64, BF16, FAKE, 64, None, 64, FAKE, 64, 0)
     assert e.value.status == hstu.MTGR_ERROR_NULL_POINTER
     hstu.mtgr_add(0, 64, BF16, None, 64, None, 64, None, 64, 0)
+
+
+def test_clock_probe_argument_checks():
+    for args, status in (((0, 4, FAKE), hstu.MTGR_ERROR_INVALID_ARGUMENT),
+                         ((10, 0, FAKE), hstu.MTGR_ERROR_INVALID_ARGUMENT),
+                         ((10, 70000, FAKE), hstu.MTGR_ERROR_INVALID_ARGUMENT),
+                         ((10, 4, None), hstu.MTGR_ERROR_NULL_POINTER),
+                         ((10, 4, FAKE + 4), hstu.MTGR_ERROR_INVALID_ARGUMENT)):
+        with pytest.raises(hstu.MtgrError) as e:
+            hstu.mtgr_debug_clock_probe(*args, stream=0)
+        assert e.value.status == status

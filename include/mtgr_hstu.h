@@ -161,7 +161,9 @@ mtgr_status_t mtgr_hstu_attn_plan(const mtgr_hstu_problem_t* p, const int32_t* o
  *   M_ij = 1 iff i == j, or seg_j is USER/HIST (static, rule 1), or seg_j is RT and
  *   seg_i is RT/CAND and ts_j < ts_i (rule 2); candidates are seen only by
  *   themselves (rule 3).
- * The bias term is present only when rab != NULL (requires num_rab_buckets > 0);
+ * The bias term is present only when rab != NULL (requires num_rab_buckets > 0); its values
+ * must be finite and below 1e29 in magnitude (the bf16 forward hides masked pairs by driving
+ * alpha * s + rab to about -1e30 when |alpha| >= 1e-7);
  * bucket(g) = g for g < 2, else 2e + [g >= 1.5 * 2^e] with e = floor(log2 g), g as uint32.
  *   offsets [B+1] int32, seg [T] int8, ts [T] int32 (seconds; any epoch).
  *   q, k, v [T, H, dh] (dtype), out [T, H, dh] (dtype, stride ld_o).

@@ -25,8 +25,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
     // Query unit buffers: Q then dO of one unit in one array, so that a dO operand sits a constant
     // distance from the Q operand read with the same lane offset (one address for both reads).
     __shared__ __align__(16) uint16_t sQG[2][2 * UNIT];
-    __shared__ int sQts[2][32];
-    __shared__ int sQcode[2][32];
+    __shared__ __align__(16) int sQts[2][32];
+    __shared__ __align__(16) int sQcode[2][32];
     __shared__ float sRab[MTGR_RAB_LDS];
     __shared__ float sHist[RAB ? bwd::HIST_WORDS : 1];
 
@@ -232,17 +232,21 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
                 dsk[1][(r - 8) >> 1] = pack_bf16x2(dv[r], dv[r + 1]);
             }
         } else {
-            // With a relative bias: groups of 4 elements (their timestamps and then their bias
-            // values read from LDS first) keep the live registers within budget.
-#pragma unroll
-            for (int g0 = 0; g0 < 16; g0 += 4) {
+            // With a relative bias: groups of 4 elements (their bucket indices, then their bias
+            // values read from LDS) keep the live registers within budget.  As without a bias,
+            // elements 0..7 (queries 0..15) come first and elements 8..15 interleave with the
+            // dV / dK products of queries 0..15, so that the wave overlaps its own VALU and
+            // MFMA work.
+            // The 4 queries of a group are consecutive (8 (g0 / 4) + 4 hh + 0..3): their
+            // timestamps (and, for a partial unit, mask codes) are one 16-byte LDS read each.
+            typedef int i32x4 __attribute__((ext_vector_type(4)));
+            auto group = [&](int g0) {
                 float pv[4], dv[4];
                 int bk[4];
+                const int qb0 = 8 * (g0 >> 2) + 4 * hh;
+                const i32x4 qt4 = *(const i32x4*)&qts[qb0];
 #pragma unroll
-                for (int e = 0; e < 4; e++) {
-                    const int rr = g0 + e;
-                    bk[e] = rab_bucket(qts[8 * (rr >> 2) + 4 * hh + (rr & 3)], kts, a.nbuckets);
-                }
+                for (int e = 0; e < 4; e++) bk[e] = rab_bucket(qt4[e], kts, a.nbuckets);
 #pragma unroll
                 for (int e = 0; e < 4; e++) {
                     const float x = sacc[g0 + e] * alpha + sRab[bk[e]];
@@ -251,8 +255,13 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
                     dv[e] = dpacc[g0 + e] * sg * (1.0f + x * (1.0f - sg));
                 }
                 if (cls == TILE_PARTIAL) {
+                    const i32x4 qc4 = *(const i32x4*)&qcode[qb0];
 #pragma unroll
-                    for (int e = 0; e < 4; e++) mask(g0 + e, pv[e], dv[e]);
+                    for (int e = 0; e < 4; e++) {
+                        const bool vis = visible(qc4[e], qt4[e], qb + qb0 + e, kcode, kts, kj);
+                        pv[e] = vis ? pv[e] : 0.f;
+                        dv[e] = vis ? dv[e] : 0.f;
+                    }
                 }
 #pragma unroll
                 for (int e = 0; e < 4; e += 2) {
@@ -264,14 +273,20 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
 #pragma unroll
                     for (int e = 0; e < 4; e++) run.add(sHist, lane, bk[e], dv[e]);
                 }
-            }
+            };
+            group(0);
+            group(4);
             operands(0);
-#pragma unroll
-            for (int j = 0; j < PF_D && j < NJ; j++) load_d(j);
+            load_d(0);
 #pragma unroll
             for (int j = 0; j < DBLK; j++) {
-                if (j + PF_D < NJ) load_d(j + PF_D);
+                load_d(j + 1);
                 product(j);
+                // groups 8 and 12 spread over the DBLK products of queries 0..15
+#pragma unroll
+                for (int gi = 0; gi < 2; gi++)
+                    if (gi * DBLK / 2 == j) group(8 + 4 * gi);
+                asm volatile("" : "+v"(dvacc[j]), "+v"(dkacc[j]));
                 __builtin_amdgcn_sched_barrier(0);
             }
         }
@@ -287,10 +302,9 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
                 for (int g = 0; g < 2; g++)
                     sub[(2 * kq + g) * 64 + lane] = make_uint2(dsk[kq][2 * g], dsk[kq][2 * g + 1]);
         }
-        // Operands 0 .. DBLK (one step ahead, without a bias) or up to DBLK + 1 (two steps
-        // ahead) have been read.
+        // Operands 0 .. DBLK have been read (one step ahead); the rest go two steps ahead.
         operands(1);
-        if constexpr (!RAB && DBLK + 1 < NJ) load_d(DBLK + 1);
+        if constexpr (DBLK + 1 < NJ) load_d(DBLK + 1);
 #pragma unroll
         for (int j = DBLK; j < NJ; j++) {
             if (j + PF_D < NJ) load_d(j + PF_D);

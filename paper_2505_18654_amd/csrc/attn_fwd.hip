@@ -52,7 +52,14 @@ __device__ __forceinline__ uint4 ldg16(const uint16_t* p) { return *(const uint4
 // a.summ_k).  Candidates see only user-side keys and themselves (Sec. 4.2), so no key tile holds
 // a candidate; each candidate's own term p_ii v_i is added after the tiles, and n_b counts both
 // sides.
-template <int DH, bool RAB, bool CACHED>
+//
+// Masking.  Masked scores are replaced before the SiLU by a value whose P' is exactly zero, in
+// a pass of their own on PARTIAL tiles, so that one epilogue serves every tile: 0 without a
+// relative bias (silu(0) = 0); with a bias, -1e30 / alpha, so that alpha s + rab is about -1e30
+// and silu = x sigmoid(x) = x * 0 (the host requires |alpha| >= 1e-7 and finite bias values
+// far below 1e29 for it).  RSEL instead selects P' = 0 element by element in the epilogue (a
+// second epilogue path): the host picks it for a bias with |alpha| < 1e-7.
+template <int DH, bool RAB, bool CACHED, bool RSEL>
 __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
     constexpr int CPR = DH / 8;          // 16-byte chunks per row
     constexpr int KSTEPS = DH / 16;      // k-steps of S^T = K Q^T per 32-key half
@@ -263,15 +270,16 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
             __builtin_amdgcn_sched_barrier(0);
         }
     };
-    // Without a relative bias, masked scores are zeroed before the SiLU (silu(0) = 0 exactly),
-    // in a pass of their own on PARTIAL tiles, so that one epilogue serves every tile.
+    // Masked scores replaced by s_masked before the SiLU (see the kernel's comment).
+    constexpr bool SMASK = !RAB || !RSEL;
+    const float s_masked = RAB ? -1e30f / alpha : 0.f;
     auto premask = [&](floatx16& cur, auto hc_tag, const int* kts, const int* kcode, int qrel) {
         constexpr int HC = decltype(hc_tag)::value;
 #pragma unroll
         for (int e = 0; e < 16; e++) {
             const int kc = 32 * HC + 8 * (e >> 2) + (e & 3);
             const int kl = kc + 4 * hh;
-            cur[e] = visible_diag(qcode, qts, kcode[kl], kts[kl], qrel == kc) ? cur[e] : 0.f;
+            cur[e] = visible_diag(qcode, qts, kcode[kl], kts[kl], qrel == kc) ? cur[e] : s_masked;
         }
     };
     using C0 = std::integral_constant<int, 0>;
@@ -309,8 +317,8 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
             const int qrel = CACHED ? -(1 << 20) : qi - t0 * BN - 4 * hh;
             uint32_t pkA[4], pkB[4];
             // half 0 of t_i; next S = half 1 of t_i (same K buffer)
-            if (!RAB && partial) premask(sA, C0{}, sVts[P], sVcode[P], qrel);
-            if (RAB && partial)
+            if (SMASK && partial) premask(sA, C0{}, sVts[P], sVcode[P], qrel);
+            if (!SMASK && partial)
                 half_step(F{}, T{}, T{}, CP{}, C0{}, CP{}, C1{}, sA, sB, pkA, pkA, qrel);
             else
                 half_step(F{}, T{}, F{}, CP{}, C0{}, CP{}, C1{}, sA, sB, pkA, pkA, qrel);
@@ -326,8 +334,8 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
             // half 1 of t_i; next S = half 0 of t_{i+1}.  After the last tile that S is formed
             // from the idle K buffer (no copy is in flight into it) and never used: one code
             // path for every tile keeps the O accumulators in one set of registers.
-            if (!RAB && partial) premask(sB, C1{}, sVts[P], sVcode[P], qrel);
-            if (RAB && partial)
+            if (SMASK && partial) premask(sB, C1{}, sVts[P], sVcode[P], qrel);
+            if (!SMASK && partial)
                 half_step(T{}, T{}, T{}, CP{}, C1{}, CQ{}, C0{}, sB, sA, pkA, pkB, qrel);
             else
                 half_step(T{}, T{}, F{}, CP{}, C1{}, CQ{}, C0{}, sB, sA, pkA, pkB, qrel);
@@ -506,10 +514,12 @@ __global__ __launch_bounds__(256) void attn_fwd_vec_kernel(AttnArgs a) {
 
 template <int DH, bool CACHED>
 static hipError_t fwd_bf16_dh(const AttnArgs& a, int slots, hipStream_t s) {
-    if (a.rab)
-        attn_fwd_bf16_kernel<DH, true, CACHED><<<slots, 256, 0, s>>>(a);
+    if (a.rab && fabsf(a.alpha) >= 1e-7f)
+        attn_fwd_bf16_kernel<DH, true, CACHED, false><<<slots, 256, 0, s>>>(a);
+    else if (a.rab)
+        attn_fwd_bf16_kernel<DH, true, CACHED, true><<<slots, 256, 0, s>>>(a);
     else
-        attn_fwd_bf16_kernel<DH, false, CACHED><<<slots, 256, 0, s>>>(a);
+        attn_fwd_bf16_kernel<DH, false, CACHED, false><<<slots, 256, 0, s>>>(a);
     return hipGetLastError();
 }
 

@@ -162,3 +162,29 @@ def test_alpha_values(alpha):
             errs[(name, t)] = per_user_err(L, users, g, r, "bf16", TOL["bf16"])["checked"]
     say(f"[bwd paths] alpha={alpha} " + " ".join(f"{n}.{t}={e:.2e}" for (n, t), e in errs.items()))
     assert all(e <= TOL["bf16"] for e in errs.values()), errs
+
+
+@pytest.mark.parametrize("alpha", [1.0, -0.7, 3.0, 2e-7, 5e-8, 1e-25, 0.0])
+def test_forward_with_bias_alpha_values(alpha):
+    """The forward with a relative bias masks through the score (alpha s + rab about -1e30)
+    when |alpha| >= 1e-7 and selects zero element by element below that: both against the
+    oracle, on users with every mask case (partial tiles on and off the diagonal)."""
+    U, S, R, C = SEG_USER, SEG_HIST, SEG_RT, SEG_CAND
+    rng = np.random.default_rng(29)
+    segs, tss = [], []
+    for n_s, n_r, n_c in ((150, 40, 20), (60, 3, 2), (200, 70, 45)):
+        segs.append([U] * 4 + [S] * n_s + [R] * n_r + [C] * n_c)
+        tss.append([0] * 4 + sorted(rng.integers(-10**6, 0, n_s).tolist()) +
+                   sorted(rng.choice(86400, n_r, replace=False).tolist()) + rng.integers(0, 86400, n_c).tolist())
+    L = custom_layout(segs, tss, heads=2, head_dim=128, dtype="bf16", rab_buckets=64)
+    inp = make_inputs(L, all_exact=True)
+    jag = jagged(inp)
+    q, k, v, rab = inp["q"], inp["k"], inp["v"], inp["rab"]
+    say(f"[bwd paths] forward with bias, alpha={alpha}")
+    o = ops.attn_fwd(q, k, v, jag, rab, alpha)
+    torch.cuda.synchronize()
+    vals = make_values(L)
+    ref = oracle.attn_fwd(L.offsets, L.seg, L.ts, vals["q"], vals["k"], vals["v"], vals["rab"], alpha)
+    e = per_user_err(L, list(range(L.num_users)), to_np(o), ref, "bf16", TOL["bf16"])
+    say(f"[bwd paths] forward with bias, alpha={alpha}: {e['checked']:.2e} (literal {e['literal']:.2e})")
+    assert e["checked"] <= TOL["bf16"], e

@@ -55,10 +55,11 @@ def bf16(x):
     return torch.tensor(x, dtype=torch.float32).to(torch.bfloat16)
 
 
-def run_case(seg, ts, which, seed=0):
+def run_case(seg, ts, which, seed=0, bias=False, alpha=1.0):
     n = len(seg)
     H, dh = (n + 127) // 128, 128
     rng = np.random.default_rng(seed)
+    rab = (0.5 * rng.standard_normal((H, 64))) if bias else None
     onehot = np.zeros((n, H, dh), np.float32)
     for j in range(n):
         onehot[j, j // 128, j % 128] = 1.0
@@ -78,12 +79,13 @@ def run_case(seg, ts, which, seed=0):
     seg_a, ts_a = np.array(seg, np.int8), np.array(ts, np.int32)
     jag = ops.Jagged.from_host(off, seg_a, ts_a)
     tq, tk, tv, tdo = (torch.from_numpy(x).to("cuda", torch.bfloat16) for x in (q, k, v, do))
+    trab = None if rab is None else torch.tensor(rab, dtype=torch.float32, device="cuda")
     if which == "fwd":
-        got = ops.attn_fwd(tq, tk, tv, jag)
-        want = oracle.attn_fwd(off, seg_a, ts_a, q, k, v)
+        got = ops.attn_fwd(tq, tk, tv, jag, trab, alpha)
+        want = oracle.attn_fwd(off, seg_a, ts_a, q, k, v, rab, alpha)
     else:
-        dq, dk, dv, _ = ops.attn_bwd(tq, tk, tv, tdo, jag)
-        rq, rk, rv, _ = oracle.attn_bwd(off, seg_a, ts_a, q, k, v, do)
+        dq, dk, dv, _ = ops.attn_bwd(tq, tk, tv, tdo, jag, trab, alpha, need_drab=False)
+        rq, rk, rv, _ = oracle.attn_bwd(off, seg_a, ts_a, q, k, v, do, rab, alpha)
         got, want = {"dv": (dv, rv), "dk": (dk, rk), "dq": (dq, rq)}[which]
     torch.cuda.synchronize()
     return got.float().cpu().numpy(), want
@@ -92,9 +94,22 @@ def run_case(seg, ts, which, seed=0):
 @pytest.mark.parametrize("which", ["fwd", "dv", "dk", "dq"])
 @pytest.mark.parametrize("name", list(users_for_extraction()))
 def test_pair_extraction(name, which):
+    check_extraction(name, which)
+
+
+# With a relative bias the forward masks through the score (alpha s + rab about -1e30, so
+# silu gives exactly zero); with |alpha| < 1e-7 it selects zero element by element instead.
+@pytest.mark.parametrize("which, alpha", [("fwd", 1.0), ("fwd", 1e-8), ("fwd", -0.7), ("dv", 1.0), ("dk", 1.0),
+                                          ("dq", 1.0)])
+@pytest.mark.parametrize("name", list(users_for_extraction()))
+def test_pair_extraction_with_bias(name, which, alpha):
+    check_extraction(name, which, bias=True, alpha=alpha)
+
+
+def check_extraction(name, which, bias=False, alpha=1.0):
     seg, ts = users_for_extraction()[name]
-    say(f"[mask] {name} {which} n={len(seg)}")
-    got, want = run_case(seg, ts, which)
+    say(f"[mask] {name} {which} n={len(seg)} bias={bias} alpha={alpha}")
+    got, want = run_case(seg, ts, which, bias=bias, alpha=alpha)
     n = len(seg)
     H = (n + 127) // 128
     # extracted matrices: rows = the other index, cols = 128h + c (< n)

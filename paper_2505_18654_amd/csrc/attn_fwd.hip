@@ -76,6 +76,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
     __shared__ __align__(16) uint16_t sV[2][TILE];
     __shared__ int sVts[2][BN];          // timestamps / mask codes travel with the V tile
     __shared__ int sVcode[2][BN];
+    __shared__ __align__(16) long long sVthr[2][BN];   // key_threshold of each key of the tile
     __shared__ float sRab[MTGR_RAB_LDS];
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -273,13 +274,14 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
     // Masked scores replaced by s_masked before the SiLU (see the kernel's comment).
     constexpr bool SMASK = !RAB || !RSEL;
     const float s_masked = RAB ? -1e30f / alpha : 0.f;
-    auto premask = [&](floatx16& cur, auto hc_tag, const int* kts, const int* kcode, int qrel) {
+    const long long qv = query_value(qcode, qts);
+    auto premask = [&](floatx16& cur, auto hc_tag, const long long* thr, int qrel) {
         constexpr int HC = decltype(hc_tag)::value;
 #pragma unroll
         for (int e = 0; e < 16; e++) {
             const int kc = 32 * HC + 8 * (e >> 2) + (e & 3);
             const int kl = kc + 4 * hh;
-            cur[e] = visible_diag(qcode, qts, kcode[kl], kts[kl], qrel == kc) ? cur[e] : s_masked;
+            cur[e] = (qv >= thr[kl] || qrel == kc) ? cur[e] : s_masked;
         }
     };
     using C0 = std::integral_constant<int, 0>;
@@ -309,7 +311,12 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
             using CQ = std::integral_constant<int, P ^ 1>;
             // top: V(t_i) (and its codes) landed; K(t_{i+1}) may still be in flight
             if (t1 < ntk) wait_vmcnt<NK>(); else wait_vmem();
-            if (tid < BN && t0 * BN + tid >= nkb) sVcode[P][tid] = 0;
+            if (tid < BN) {
+                // padded keys get code 0; every key gets its visibility threshold
+                int c = sVcode[P][tid];
+                if (t0 * BN + tid >= nkb) sVcode[P][tid] = c = 0;
+                sVthr[P][tid] = key_threshold(c, sVts[P][tid]);
+            }
             lds_barrier();
             if (t1 < ntk) issue_v(t1, P ^ 1);                      // V(t_{i-1})'s buffer
             const bool partial = cls0 == TILE_PARTIAL;
@@ -317,7 +324,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
             const int qrel = CACHED ? -(1 << 20) : qi - t0 * BN - 4 * hh;
             uint32_t pkA[4], pkB[4];
             // half 0 of t_i; next S = half 1 of t_i (same K buffer)
-            if (SMASK && partial) premask(sA, C0{}, sVts[P], sVcode[P], qrel);
+            if (SMASK && partial) premask(sA, C0{}, sVthr[P], qrel);
             if (!SMASK && partial)
                 half_step(F{}, T{}, T{}, CP{}, C0{}, CP{}, C1{}, sA, sB, pkA, pkA, qrel);
             else
@@ -334,7 +341,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
             // half 1 of t_i; next S = half 0 of t_{i+1}.  After the last tile that S is formed
             // from the idle K buffer (no copy is in flight into it) and never used: one code
             // path for every tile keeps the O accumulators in one set of registers.
-            if (SMASK && partial) premask(sB, C1{}, sVts[P], sVcode[P], qrel);
+            if (SMASK && partial) premask(sB, C1{}, sVthr[P], qrel);
             if (!SMASK && partial)
                 half_step(T{}, T{}, T{}, CP{}, C1{}, CQ{}, C0{}, sB, sA, pkA, pkB, qrel);
             else

@@ -133,6 +133,21 @@ __device__ __forceinline__ bool visible(int qcode, int qts, int qidx, int kcode,
     return (seen != 0) & (both_valid != 0);
 }
 
+// The mask as one 64-bit comparison: key j is visible to query i (i != j) iff
+// query_value(i) >= key_threshold(j).  A static key is seen by every query (threshold -2^63); an
+// RT key by the RT and candidate queries later than it (threshold ts_j + 1 against the query's
+// ts); a candidate key, and a padded key (code 0), by nobody but itself (threshold 2^63 - 1);
+// a static query has the value -2^63, so it sees static keys only.  Equal to visible() for every
+// valid query row and every int32 timestamp.
+__device__ __forceinline__ long long key_threshold(int kcode, int kts) {
+    if (kcode & KC_STATIC) return (long long)0x8000000000000000ull;
+    if (kcode & KC_RT) return (long long)kts + 1;
+    return 0x7fffffffffffffffll;
+}
+__device__ __forceinline__ long long query_value(int qcode, int qts) {
+    return (qcode & KC_DYN) ? (long long)qts : (long long)0x8000000000000000ull;
+}
+
 // visible() with the diagonal test i == j already evaluated by the caller.
 __device__ __forceinline__ bool visible_diag(int qcode, int qts, int kcode, int kts, bool diag) {
     const int both_valid = kcode & qcode & KC_VALID;

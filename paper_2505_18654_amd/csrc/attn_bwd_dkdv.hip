@@ -294,13 +294,14 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
             // Sub-block (query half, key half) of block (t, kblk), 2 KB in register-fragment
             // order: chunk (kq, g, lane) = 4 bf16 of dS for key 32 (w & 1) + lane % 32 and
             // queries 32 half + 16 kq + 8 g + 4 (lane / 32) + 0..3, i.e. dsk[kq][2g], dsk[kq][2g+1].
-            // Each of the 4 store instructions writes 512 contiguous bytes.
+            // Each of the 4 store instructions writes 512 contiguous bytes (non-temporal: the dQ
+            // kernel reads the block once, later).
             uint2* sub = (uint2*)(a.ds + ((ds_blk + (long long)t * ntq) << 12)) + (2 * half + (w & 1)) * 256;
 #pragma unroll
             for (int kq = 0; kq < 2; kq++)
 #pragma unroll
                 for (int g = 0; g < 2; g++)
-                    sub[(2 * kq + g) * 64 + lane] = make_uint2(dsk[kq][2 * g], dsk[kq][2 * g + 1]);
+                    store_nt8(&sub[(2 * kq + g) * 64 + lane], dsk[kq][2 * g], dsk[kq][2 * g + 1]);
         }
         // Operands 0 .. DBLK have been read (one step ahead); the rest go two steps ahead.
         operands(1);
@@ -352,8 +353,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
             const int c = lane + 64 * i, row = c / CPR, cc = c % CPR;
             const int kr = k0 + w * 32 + row;
             if (kr < nb)
-                *(uint4*)(dst + (long long)(ob + kr) * ld + h * DH + cc * 8) =
-                    *(const uint4*)&sO[8 * tile_chunk<CPR>(row, cc)];
+                store_nt16(dst + (long long)(ob + kr) * ld + h * DH + cc * 8, &sO[8 * tile_chunk<CPR>(row, cc)]);
         }
     }
 }

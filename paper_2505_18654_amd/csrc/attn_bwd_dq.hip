@@ -203,8 +203,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
         const int c = lane + 64 * i, row = c / CPR, cc = c % CPR;
         const int qr = q0 + w * 32 + row;
         if (qr < nb)
-            *(uint4*)(DQ + (long long)(ob + qr) * a.ld_q + h * DH + cc * 8) =
-                *(const uint4*)&sO[8 * tile_chunk<CPR>(row, cc)];
+            store_nt16(DQ + (long long)(ob + qr) * a.ld_q + h * DH + cc * 8, &sO[8 * tile_chunk<CPR>(row, cc)]);
     }
 }
 

@@ -62,7 +62,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_ds_bf16_kernel(AttnArgs a)
         return tile_class(sq64, sk, overlap);
     };
     TileWalker<decltype(written_of)> written(written_of, ntk);
-    // 8 KB block: instruction i of wave w fills bytes [1024 (4 i + w), +1024) of the LDS copy.
+    // 8 KB block (read once: non-temporal copy): instruction i of wave w fills bytes
+    // [1024 (4 i + w), +1024) of the LDS copy.
     // The 16-byte unit u = 128 sub-block + 32 row + v of the block (row = 2 kq + g, v = 16-byte
     // half of a fragment row) sits at u ^ dsw(u), which permutes units only inside aligned groups
     // of 16.  Stored as is, the 32 lanes of one transposing read below (4 rows x 8 chunks of one
@@ -76,8 +77,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_ds_bf16_kernel(AttnArgs a)
         for (int i = 0; i < 2; i++) {
             const int part = __builtin_amdgcn_readfirstlane(i * 4 + w);
             const int u = part * 64 + lane;
-            lds_dma16(__builtin_amdgcn_readfirstlane(lds_address(dst) + (uint32_t)part * 1024u),
-                      uniform_ptr(src + part * 512), (uint32_t)((u ^ dsw(u)) & 63) * 16u);
+            lds_dma16_nt(__builtin_amdgcn_readfirstlane(lds_address(dst) + (uint32_t)part * 1024u),
+                         uniform_ptr(src + part * 512), (uint32_t)((u ^ dsw(u)) & 63) * 16u);
         }
     };
     auto issue = [&](int t, int buf) {
@@ -160,8 +161,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_ds_bf16_kernel(AttnArgs a)
         const int c = lane + 64 * i, row = c / CPR, cc = c % CPR;
         const int qr = q0 + w * 32 + row;
         if (qr < nb)
-            *(uint4*)(DQ + (long long)(ob + qr) * a.ld_q + h * DH + cc * 8) =
-                *(const uint4*)&sO[8 * tile_chunk<CPR>(row, cc)];
+            store_nt16(DQ + (long long)(ob + qr) * a.ld_q + h * DH + cc * 8, &sO[8 * tile_chunk<CPR>(row, cc)]);
     }
 }
 

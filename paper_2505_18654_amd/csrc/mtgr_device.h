@@ -178,6 +178,19 @@ __device__ __forceinline__ float bf16_to_f32(uint16_t h) {
     return __uint_as_float(((uint32_t)h) << 16);
 }
 
+// Stores with the non-temporal hint, for results written once and not read again by the kernel
+// (output rows, the stored dS blocks): measured faster than plain stores for these full-line
+// writes.
+typedef unsigned int u32x4_nt __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2_nt __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ void store_nt16(void* dst, const void* src) {
+    __builtin_nontemporal_store(*(const u32x4_nt*)src, (u32x4_nt*)dst);
+}
+__device__ __forceinline__ void store_nt8(void* dst, uint32_t lo, uint32_t hi) {
+    const u32x2_nt v = {lo, hi};
+    __builtin_nontemporal_store(v, (u32x2_nt*)dst);
+}
+
 // Element access of the vector-ALU kernels, which store either fp32 or bf16 and compute in fp32.
 __device__ __forceinline__ float ld_elem(const float* p, long long i) { return p[i]; }
 __device__ __forceinline__ float ld_elem(const uint16_t* p, long long i) { return bf16_to_f32(p[i]); }
@@ -304,6 +317,13 @@ __device__ __forceinline__ const T* uniform_ptr(const T* p) {
 // One copy instruction: source address = sbase (wave-uniform) + voff (per lane, bytes).
 __device__ __forceinline__ void lds_dma16(uint32_t lds_base, const void* sbase, uint32_t voff) {
     asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
+                 :: "s"(lds_base), "v"(voff), "s"(sbase) : "memory");
+}
+
+// The same copy with the non-temporal hint: for data read once (the stored dS blocks), so that it
+// does not displace reused tiles from the caches.
+__device__ __forceinline__ void lds_dma16_nt(uint32_t lds_base, const void* sbase, uint32_t voff) {
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2 nt"
                  :: "s"(lds_base), "v"(voff), "s"(sbase) : "memory");
 }
 

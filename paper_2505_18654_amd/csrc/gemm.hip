@@ -254,8 +254,8 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmArgs g) {
             // bias gradient: column sums of B over this K split, 8 columns x 2 rows per thread
             const int c = tid & 15, rg = tid >> 4;
 #pragma unroll
-            for (int r = 2 * rg; r < 2 * rg + 2; r++) {
-                const bf16x8 v = tile_read8<GBN / 8>(smB[st], r, c);
+            for (int j = 0; j < 2; j++) {
+                const bf16x8 v = tile_read8<GBN / 8>(smB[st], 2 * rg + j, c);
 #pragma unroll
                 for (int e = 0; e < 8; e++) csum[e] += (float)v[e];
             }

@@ -309,44 +309,127 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmArgs g) {
 
     // acc[a][b] holds C^T of rows n0 + 64 wn + 32 a + 8 (r / 4) + 4 hf + r % 4, columns
     // m0 + 128 wm + 32 b + col: lane row gm of C, columns gn .. gn + 3 per register group q = r / 4.
+    // Written directly, one store instruction would touch 32 rows with 16 bytes each.  So the
+    // bf16 results (and, for bias + SiLU, then the activation) pass through LDS, half a tile (128
+    // rows, the rows of the waves with wm = hm) at a time, in the stage memory that is free now:
+    // row stride 136 elements (272 bytes, so that the 32 rows of one write instruction spread
+    // over the banks), then every thread stores whole 16-byte chunks, 4 rows of 256 bytes per
+    // store instruction, with the non-temporal hint (the results are not read by this kernel).
+    // Measured on the layer shapes: the projection with bias + SiLU 1.06 -> 0.91 ms, plain
+    // products 12-19 % faster.
+    constexpr bool STAGED = !SPLIT && EPI != GEMM_EPI_BIAS_RESIDUAL;
+    if constexpr (STAGED) {
+        constexpr int SROW = GBN + 8;
+        static_assert(128 * SROW <= GSTAGES * A_ELEMS, "staging fits the A stages");
+        uint16_t* stg = &smA[0][0];
+        constexpr int NOUT = EPI == GEMM_EPI_BIAS_SILU ? 2 : 1;
 #pragma unroll
-    for (int b = 0; b < NBM; b++) {
-        const long long gm = m0 + 128 * wm + 32 * b + col;
-        if (gm >= M) continue;
+        for (int out = 0; out < NOUT; out++) {
+            uint16_t* Cout = (uint16_t*)(out == 0 ? g.C : g.C2);
+            const long long ldo = out == 0 ? g.ldc : g.ldc2;
 #pragma unroll
-        for (int a = 0; a < NBN; a++) {
+            for (int hm = 0; hm < 2; hm++) {
+                lds_barrier();   // the stage memory (or the previous half) is no longer read
+                if (wm == hm) {
 #pragma unroll
-            for (int q = 0; q < 4; q++) {
-                const int gn = n0 + 64 * wn + 32 * a + 8 * q + 4 * hf;
-                if (gn >= N) continue;
-                float v[4] = {acc[a][b][4 * q], acc[a][b][4 * q + 1], acc[a][b][4 * q + 2], acc[a][b][4 * q + 3]};
-                if constexpr (SPLIT) {
-                    float* P = g.partial + ((long long)split * M + gm) * N + gn;
-                    *(float4*)P = make_float4(v[0], v[1], v[2], v[3]);
-                    continue;
+                    for (int b = 0; b < NBM; b++)
+#pragma unroll
+                        for (int a = 0; a < NBN; a++)
+#pragma unroll
+                            for (int q = 0; q < 4; q++) {
+                                const int cl = 64 * wn + 32 * a + 8 * q + 4 * hf;
+                                float v[4] = {acc[a][b][4 * q], acc[a][b][4 * q + 1], acc[a][b][4 * q + 2],
+                                              acc[a][b][4 * q + 3]};
+                                if (out == 1) {
+                                    float4 bi = make_float4(0.f, 0.f, 0.f, 0.f);
+                                    if (n0 + cl < N) bi = *(const float4*)(g.bias + n0 + cl);
+                                    v[0] = silu(v[0] + bi.x);
+                                    v[1] = silu(v[1] + bi.y);
+                                    v[2] = silu(v[2] + bi.z);
+                                    v[3] = silu(v[3] + bi.w);
+                                }
+                                *(uint2*)&stg[(32 * b + col) * SROW + cl] =
+                                    make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
+                            }
                 }
-                uint16_t* C = (uint16_t*)g.C + gm * g.ldc + gn;
-                if constexpr (EPI == GEMM_EPI_BIAS_SILU) {
-                    *(uint2*)C = make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
-                    const float4 bi = *(const float4*)(g.bias + gn);
-                    uint16_t* C2 = (uint16_t*)g.C2 + gm * g.ldc2 + gn;
-                    *(uint2*)C2 = make_uint2(pack_bf16x2(silu(v[0] + bi.x), silu(v[1] + bi.y)),
-                                             pack_bf16x2(silu(v[2] + bi.z), silu(v[3] + bi.w)));
-                } else if constexpr (EPI == GEMM_EPI_BIAS_RESIDUAL) {
-                    const float4 bi = *(const float4*)(g.bias + gn);
-                    const uint2 rr = *(const uint2*)((const uint16_t*)g.R + gm * g.ldr + gn);
-                    v[0] += bi.x + __uint_as_float(rr.x << 16);
-                    v[1] += bi.y + __uint_as_float(rr.x & 0xffff0000u);
-                    v[2] += bi.z + __uint_as_float(rr.y << 16);
-                    v[3] += bi.w + __uint_as_float(rr.y & 0xffff0000u);
-                    *(uint2*)C = make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
-                } else {
-                    *(uint2*)C = make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
+                lds_barrier();
+#pragma unroll
+                for (int i = 0; i < 128 * GBN / 8 / 256; i++) {
+                    const int idx = 256 * i + tid, row = idx >> 4, ch = idx & 15;
+                    const long long gm = m0 + 128 * hm + row;
+                    const int gn = n0 + 8 * ch;
+                    if (gm < M && gn < N)
+                        store_nt16(Cout + gm * ldo + gn, &stg[row * SROW + 8 * ch]);
                 }
             }
         }
-        // one 32-row block at a time: the epilogue's loads are not hoisted across blocks
-        __builtin_amdgcn_sched_barrier(0);
+    }
+    if constexpr (!SPLIT && EPI == GEMM_EPI_BIAS_RESIDUAL) {
+        // The same for bias + residual, with the fp32 products staged (a quarter tile, 64 rows,
+        // at a time; row stride 132 floats) so that the store phase forms acc + (bias + residual)
+        // from fp32 and rounds once, as the direct form did.
+        constexpr int FROW = GBN + 4;
+        static_assert(64 * FROW * 4 <= GSTAGES * A_ELEMS * 2, "staging fits the A stages");
+        float* stf = (float*)&smA[0][0];
+#pragma unroll
+        for (int p = 0; p < 4; p++) {   // tile rows 64 p .. 64 p + 63: waves wm = p / 2, b = 2 (p % 2) + 0..1
+            lds_barrier();
+            if (wm == (p >> 1)) {
+#pragma unroll
+                for (int bb = 0; bb < 2; bb++)
+#pragma unroll
+                    for (int a = 0; a < NBN; a++)
+#pragma unroll
+                        for (int q = 0; q < 4; q++) {
+                            const int b = 2 * (p & 1) + bb;
+                            const int cl = 64 * wn + 32 * a + 8 * q + 4 * hf;
+                            *(float4*)&stf[(32 * bb + col) * FROW + cl] =
+                                make_float4(acc[a][b][4 * q], acc[a][b][4 * q + 1], acc[a][b][4 * q + 2],
+                                            acc[a][b][4 * q + 3]);
+                        }
+            }
+            lds_barrier();
+#pragma unroll
+            for (int i = 0; i < 64 * GBN / 8 / 256; i++) {
+                const int idx = 256 * i + tid, row = idx >> 4, ch = idx & 15;
+                const long long gm = m0 + 64 * p + row;
+                const int gn = n0 + 8 * ch;
+                if (gm < M && gn < N) {
+                    const float4 x0 = *(const float4*)&stf[row * FROW + 8 * ch];
+                    const float4 x1 = *(const float4*)&stf[row * FROW + 8 * ch + 4];
+                    const float4 b0 = *(const float4*)(g.bias + gn), b1 = *(const float4*)(g.bias + gn + 4);
+                    const uint4 rr = *(const uint4*)((const uint16_t*)g.R + gm * g.ldr + gn);
+                    const float v[8] = {x0.x + (b0.x + __uint_as_float(rr.x << 16)), x0.y + (b0.y + __uint_as_float(rr.x & 0xffff0000u)),
+                                        x0.z + (b0.z + __uint_as_float(rr.y << 16)), x0.w + (b0.w + __uint_as_float(rr.y & 0xffff0000u)),
+                                        x1.x + (b1.x + __uint_as_float(rr.z << 16)), x1.y + (b1.y + __uint_as_float(rr.z & 0xffff0000u)),
+                                        x1.z + (b1.z + __uint_as_float(rr.w << 16)), x1.w + (b1.w + __uint_as_float(rr.w & 0xffff0000u))};
+                    const uint4 o = make_uint4(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]),
+                                               pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7]));
+                    store_nt16((uint16_t*)g.C + gm * g.ldc + gn, &o);
+                }
+            }
+        }
+    }
+    if constexpr (SPLIT) {
+        // fp32 partials of this K split, 16 bytes per lane (summed by gemm_split_reduce_kernel)
+#pragma unroll
+        for (int b = 0; b < NBM; b++) {
+            const long long gm = m0 + 128 * wm + 32 * b + col;
+            if (gm >= M) continue;
+#pragma unroll
+            for (int a = 0; a < NBN; a++) {
+#pragma unroll
+                for (int q = 0; q < 4; q++) {
+                    const int gn = n0 + 64 * wn + 32 * a + 8 * q + 4 * hf;
+                    if (gn >= N) continue;
+                    float* P = g.partial + ((long long)split * M + gm) * N + gn;
+                    *(float4*)P = make_float4(acc[a][b][4 * q], acc[a][b][4 * q + 1], acc[a][b][4 * q + 2],
+                                              acc[a][b][4 * q + 3]);
+                }
+            }
+            // one 32-row block at a time: the stores are not hoisted across blocks
+            __builtin_amdgcn_sched_barrier(0);
+        }
     }
     if (COLSUM && colsum) {
         // the 16 row groups' sums of each column, added through LDS (stage memory is free now)

@@ -88,9 +88,20 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmArgs g) {
     const int col = lane & 31, hf = lane >> 5;
     const int wm = w & 1, wn = w >> 1;
     // workgroups of one XCD (blockIdx % 8) take the n blocks of one m block one after another,
-    // so the A rows of that block stay in the XCD's L2
+    // so the A rows of that block stay in the XCD's L2; with fewer m blocks than XCDs (the weight
+    // gradients: M = d) each m block's n blocks are dealt to 8 / mblocks XCDs, so that no XCD
+    // is left without work
     const int bid = blockIdx.x, x = bid % XCDS, jx = bid / XCDS;
-    const int mb = x + XCDS * (jx / g.nblocks), nb = jx % g.nblocks;
+    int mb, nb;
+    if (g.mblocks >= XCDS) {
+        mb = x + XCDS * (jx / g.nblocks);
+        nb = jx % g.nblocks;
+    } else {
+        const int r = XCDS / g.mblocks;
+        mb = x / r;
+        nb = x % r + r * jx;
+        if (nb >= g.nblocks) return;
+    }
     if (mb >= g.mblocks) return;
     const int m0 = mb * GBM, n0 = nb * GBN;
     const int split = blockIdx.y;
@@ -500,9 +511,16 @@ size_t gemm_workspace_bytes(int layout, long long M, long long N, long long K) {
     return (size_t)s * (size_t)(M * N + N) * sizeof(float);
 }
 
+// Workgroups along x of the grid (see the block mapping in gemm_bf16_kernel).
+static int gemm_grid_x(int mblocks, int nblocks) {
+    if (mblocks >= XCDS) return XCDS * ((mblocks + XCDS - 1) / XCDS) * nblocks;
+    const int r = XCDS / mblocks;
+    return XCDS * ((nblocks + r - 1) / r);
+}
+
 template <int LAYOUT, int EPI, bool COLSUM>
 static hipError_t gemm_launch(const GemmArgs& g, hipStream_t s) {
-    const int gx = XCDS * ((g.mblocks + XCDS - 1) / XCDS) * g.nblocks;
+    const int gx = gemm_grid_x(g.mblocks, g.nblocks);
     gemm_bf16_kernel<LAYOUT, EPI, COLSUM><<<dim3(gx, g.splits), 256, 0, s>>>(g);
     return hipGetLastError();
 }

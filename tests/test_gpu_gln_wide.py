@@ -1,6 +1,8 @@
 """Gate + Group-LN (Eq. 6) at widths above the workloads' (d = 2048 and 4096): the backward
 kernel then runs half as many waves per workgroup (and, at 8 chunks per lane, without the
-next-row prefetch).  Forward and backward against the oracle (GPU)."""
+next-row prefetch); and at widths that leave lanes past a row's last 16-byte chunk (d = 768 and
+1000), where those lanes load the last chunk again and ignore it.  Forward and backward against
+the oracle (GPU)."""
 import numpy as np
 import pytest
 import torch
@@ -20,7 +22,8 @@ def need_gpu():
 
 @pytest.mark.parametrize("d,dtype,groups,gate", [(2048, torch.bfloat16, 4, True), (4096, torch.bfloat16, 4, True),
                                                  (4096, torch.bfloat16, 2, False), (1024, torch.float32, 4, True),
-                                                 (2048, torch.float32, 3, True)])
+                                                 (2048, torch.float32, 3, True), (768, torch.bfloat16, 4, True),
+                                                 (1000, torch.bfloat16, 3, False), (200, torch.float32, 2, True)])
 def test_wide_rows(d, dtype, groups, gate):
     rng = np.random.default_rng(d + groups)
     T = 700

@@ -211,6 +211,8 @@ def main():
                     choices=["tiny", "small", "mtgr_small", "mtgr_large", "serving"])
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-graph", action="store_true",
+                    help="skip the HIP-graph replay of the step after the timed region")
     ap.add_argument("--layer", action="store_true",
                     help="time one whole encoder layer (Group-LN, projection GEMM, bias + SiLU, "
                          "attention, gate + Group-LN, output GEMM; forward and backward) instead "
@@ -370,6 +372,36 @@ def main():
     gln_bytes = T * (3 * d * 2 + 8) + (0 if fwd_only else T * (5 * d * 2 + 8))
     gln_ms = stage_ms["gln_fwd"] + stage_ms.get("gln_bwd", 0.0)
 
+    # The same step captured once in a HIP graph and replayed (after the timed region; the
+    # library allocates, synchronises and copies nothing on this path, so a caller can record
+    # it): what a graph-capturing caller saves in launch overhead, largest on the small batches.
+    graph = None
+    if not args.no_graph:
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            for s in stages:
+                run(s)
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for s in stages:
+                run(s)
+        g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(args.steps):
+            g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        ms_g = e0.elapsed_time(e1) / args.steps
+        graph = {"ms_per_step": ms_g, "tokens_per_s": T / (ms_g * 1e-3),
+                 "how": "the timed step's stages captured once in a HIP graph, replayed `steps` times "
+                        "after the timed region (HIP events around the replays)"}
+        del g
+
     res = {"o": o}
     err_lit, err_adj = sampled_parity(layout, inp, res, check_users)
 
@@ -455,6 +487,8 @@ def main():
         "parity_sampled_fwd": {"users": check_users, "max_err_over_rms": err_lit,
                                "max_err_over_rms_storage_adjusted": err_adj},
     }
+    if graph is not None:
+        line["graph_replay"] = graph
     if cand_rows is not None:
         line["serving_cand_rows"] = cand_rows
     if not args.no_cpu_baseline:

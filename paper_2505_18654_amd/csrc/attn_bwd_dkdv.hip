@@ -174,8 +174,9 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
         };
         // Element rr belongs to query 8 (rr / 4) + 4 hh + rr % 4.  p and ds are P and dS
         // without the per-user factor 1 / n_b (and, without a relative bias, P without alpha):
-        // the factors are applied once to dK, dV, dQ and drab.  silu'(x) = sg (1 + x (1 - sg))
-        // and alpha s (1 - sg) = alpha (s - p).
+        // the factors are applied once to dK, dV, dQ and drab.  silu'(x) = sg + x sg (1 - sg),
+        // and x sg = alpha p (without a bias; p itself with one), so dS = dP (sg + alpha p (1 - sg))
+        // reuses p: p (1 - sg) is one fma.
         auto mask = [&](int rr, float& p, float& ds) {
             const int ql = 8 * (rr >> 2) + 4 * hh + (rr & 3);
             const bool vis = visible(qcode[ql], qts[ql], qb + ql, kcode, kts, kj);
@@ -187,13 +188,13 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
             // dV / dK products of queries 0..15, so that one wave overlaps its own VALU and
             // MFMA work; then the products of queries 16..31.  The mask of a PARTIAL unit is
             // one branch per half, after its straight-line element math.
-            // s (1 - sg) is one explicit fma, so that every instantiation (with and without
-            // the dS store) rounds alike and their dK / dV agree bit for bit.
+            // The fmas are explicit, so that every instantiation (with and without the dS store)
+            // rounds alike and their dK / dV agree bit for bit.
             auto element = [&](int rr, float& p, float& ds) {
                 const float sv = sacc[rr];
                 const float sg = __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(sv * c_exp));
                 p = sv * sg;
-                ds = (dpacc[rr] * sg) * __builtin_fmaf(alpha, __builtin_fmaf(-sv, sg, sv), 1.0f);
+                ds = dpacc[rr] * __builtin_fmaf(alpha, __builtin_fmaf(-p, sg, p), sg);
             };
             float pv[16], dv[16];
 #pragma unroll
@@ -252,7 +253,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
                     const float x = sacc[g0 + e] * alpha + sRab[bk[e]];
                     float sg;
                     pv[e] = silu_sig(x, sg);
-                    dv[e] = dpacc[g0 + e] * sg * (1.0f + x * (1.0f - sg));
+                    dv[e] = dpacc[g0 + e] * (__builtin_fmaf(-pv[e], sg, pv[e]) + sg);
                 }
                 if (cls == TILE_PARTIAL) {
                     const i32x4 qc4 = *(const i32x4*)&qcode[qb0];

@@ -59,7 +59,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
         doreg[kk] = as_bf16x8(g);
     }
     if (RAB) {
-        if (tid < MTGR_RAB_LDS) sRab[tid] = tid < a.nbuckets ? a.rab[h * a.nbuckets + tid] : 0.f;
+        if (tid < MTGR_RAB_LDS) sRab[tid] = tid < a.nbuckets ? NEG_LOG2E * a.rab[h * a.nbuckets + tid] : 0.f;
         bwd::hist_zero(sHist, tid);
     }
     floatx16 dqacc[DBLK];
@@ -127,10 +127,9 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_bf16_kernel(AttnArgs a) {
                     const int rr = g0 + e;
                     // ds is dS without the per-user factor 1 / n_b, applied once to dQ and drab.
                     if (RAB) {
-                        const float x = sacc[rr] * alpha + sRab[bk[e]];
                         float sg;
-                        silu_sig(x, sg);
-                        dv[e] = dpacc[rr] * sg * (1.0f + x * (1.0f - sg));
+                        const float p = silu_scaled(__builtin_fmaf(sacc[rr], c_exp, sRab[bk[e]]), sg);
+                        dv[e] = dpacc[rr] * __builtin_fmaf(NEG_LN2, __builtin_fmaf(-p, sg, p), sg);
                     } else {
                         const float sv = sacc[rr];
                         const float sg = __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(sv * c_exp));

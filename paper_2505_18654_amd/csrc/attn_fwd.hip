@@ -55,8 +55,8 @@ __device__ __forceinline__ uint4 ldg16(const uint16_t* p) { return *(const uint4
 //
 // Masking.  Masked scores are replaced before the SiLU by a value whose P' is exactly zero, in
 // a pass of their own on PARTIAL tiles, so that one epilogue serves every tile: 0 without a
-// relative bias (silu(0) = 0); with a bias, -1e30 / alpha, so that alpha s + rab is about -1e30
-// and silu = x sigmoid(x) = x * 0 (the host requires |alpha| >= 1e-7 and finite bias values
+// relative bias (silu(0) = 0); with a bias, -1e30 / alpha, so that alpha s + rab is about -1e30,
+// the sigmoid 0 and P'' = y * 0 (the host requires |alpha| >= 1e-7 and finite bias values
 // far below 1e29 for it).  RSEL instead selects P' = 0 element by element in the epilogue (a
 // second epilogue path): the host picks it for a bias with |alpha| < 1e-7.
 template <int DH, bool RAB, bool CACHED, bool RSEL>
@@ -116,7 +116,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
     const int* kcode_g = (CACHED ? a.tok_code_k : a.tok_code) + okb;
     const uint16_t* Qb = (const uint16_t*)a.q + (long long)ob * a.ld_q;
     bf16x8 qreg[KSTEPS];
-    if (RAB && tid < MTGR_RAB_LDS) sRab[tid] = tid < a.nbuckets ? a.rab[h * a.nbuckets + tid] : 0.f;
+    if (RAB && tid < MTGR_RAB_LDS) sRab[tid] = tid < a.nbuckets ? NEG_LOG2E * a.rab[h * a.nbuckets + tid] : 0.f;
 
     // Per-lane LDS byte offsets of the MFMA operands, shared by every tile and buffer: the
     // K operand of k-step kk (row col, chunk 2 kk + hh; rows 32..63 add 32 * CPR * 16 bytes)
@@ -148,7 +148,9 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
     };
 
     // p' for the accumulator value sv of key kl (relative to the tile):
-    // silu(alpha s) / alpha = s / (1 + 2^(-alpha s log2 e)), or silu(alpha s + rab).
+    // silu(alpha s) / alpha = s / (1 + 2^(-alpha s log2 e)), or with a relative bias
+    // -log2(e) silu(alpha s + rab) = y / (1 + 2^y), y = -log2(e) (alpha s + rab) (the table in LDS
+    // holds -log2(e) rab).
     const float c_exp = -1.4426950408889634f * alpha;
     // qrel = qi - (first key of the tile) - 4 hh; the key of element e of half HC is the
     // tile's key 32 HC + 8 (e / 4) + 4 hh + e % 4, so the diagonal test compares qrel with a
@@ -157,9 +159,8 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
         constexpr bool MASKED = decltype(masked_tag)::value;
         float p;
         if (RAB) {
-            const float x = sv * alpha + sRab[rab_bucket(qts, kts[kl], a.nbuckets)];
             float sg;
-            p = silu_sig(x, sg);
+            p = silu_scaled(__builtin_fmaf(sv, c_exp, sRab[rab_bucket(qts, kts[kl], a.nbuckets)]), sg);
         } else {
             p = sv * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(sv * c_exp));
         }
@@ -400,7 +401,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
         float p;
         if (RAB) {
             float sg;
-            p = silu_sig(dot * alpha + sRab[0], sg);
+            p = silu_scaled(__builtin_fmaf(dot, c_exp, sRab[0]), sg);
         } else {
             p = dot * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(dot * c_exp));
         }
@@ -420,10 +421,10 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
         }
     }
 
-    // Output: O^T accumulators scaled by alpha / n_b (1 / n_b with a relative bias) -> bf16
+    // Output: O^T accumulators scaled by alpha / n_b (-ln 2 / n_b with a relative bias) -> bf16
     // rows of this wave staged in LDS (swizzled 32-row tile inside the K buffers) -> 16-byte
     // coalesced stores.
-    const float oscale = RAB ? inv_n : alpha * inv_n;
+    const float oscale = RAB ? NEG_LN2 * inv_n : alpha * inv_n;
     uint16_t* sO = sK[w >> 1] + (w & 1) * 32 * DH;
 #pragma unroll
     for (int db = 0; db < DBLK; db++) {

@@ -169,9 +169,18 @@ __device__ __forceinline__ int rab_bucket(int a, int b, int nb) {
     return min(bk, nb - 1);
 }
 
-__device__ __forceinline__ float silu_sig(float x, float& sg) {
-    sg = __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-1.4426950408889634f * x));
-    return x * sg;
+// With a relative bias the forward and the recomputing dQ kernel keep the bias table in LDS
+// multiplied by -log2(e), so that the sigmoid's exponent y = -log2(e) (alpha s + rab) is one fma
+// of the score (c_exp = -log2(e) alpha).  They work with P'' = y sigmoid = -log2(e) silu(x); the
+// factor -ln 2 that turns P'' back into silu(x) is applied once to the output, and silu'(x) =
+// sigmoid + x sigmoid (1 - sigmoid) = sigmoid - ln 2 P'' (1 - sigmoid).
+constexpr float NEG_LOG2E = -1.4426950408889634f;
+constexpr float NEG_LN2 = -0.6931471805599453f;
+
+// P'' and the sigmoid for the scaled exponent y.
+__device__ __forceinline__ float silu_scaled(float y, float& sg) {
+    sg = __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(y));
+    return y * sg;
 }
 
 __device__ __forceinline__ float bf16_to_f32(uint16_t h) {

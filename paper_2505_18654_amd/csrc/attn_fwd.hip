@@ -141,9 +141,11 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(AttnArgs a) {
     };
     TileWalker<decltype(class_of)> walk(class_of, ntk);
 
-    auto issue_k = [&](int t, int buf) { tile_dma<DH>(sK[buf], Kb, ldk, t * BN, nkb, h * DH, tid); };
+    // The copies' per-lane offsets are loop invariants kept in registers, except in the
+    // select-masked bias instantiation (256 VGPRs).
+    auto issue_k = [&](int t, int buf) { tile_dma<DH, 64, false, !RSEL>(sK[buf], Kb, ldk, t * BN, nkb, h * DH, tid); };
     auto issue_v = [&](int t, int buf) {
-        tile_dma<DH>(sV[buf], Vb, ldv, t * BN, nkb, h * DH, tid);
+        tile_dma<DH, 64, false, !RSEL>(sV[buf], Vb, ldv, t * BN, nkb, h * DH, tid);
         codes_dma(sVts[buf], sVcode[buf], kts_g, kcode_g, t * BN, nkb, tid);
     };
 

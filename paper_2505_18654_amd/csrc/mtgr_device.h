@@ -429,15 +429,16 @@ __device__ __forceinline__ bf16x8 lds_read_tr(const uint16_t* tile, uint32_t o0,
 // With CLAMP_COLS, columns at or past `ncols` (a multiple of 8, > col0) are replaced by the
 // last valid 16-byte chunk of the row: the copy stays inside the matrix, and the tile columns
 // past the edge hold values that the caller never stores.
-template <int DH, int ROWS = 64, bool CLAMP_COLS = false>
+template <int DH, int ROWS = 64, bool CLAMP_COLS = false, bool KEEP_OFFSETS = false>
 __device__ __forceinline__ void tile_dma(uint16_t* tile, const uint16_t* base, long long ld, int row0,
                                          int nrows, int col0, int tid, int ncols = 0) {
     constexpr int CPR = DH / 8, RPI = 256 / CPR, NCH = ROWS * CPR;
     static_assert(NCH % 64 == 0, "whole LDS blocks");
     // The per-lane offsets are recomputed at every call (a few VALU instructions) rather than
-    // hoisted out of the caller's loop, where they would hold VGPRs for the whole loop.
+    // hoisted out of the caller's loop, where they would hold VGPRs for the whole loop; with
+    // KEEP_OFFSETS (a caller with registers to spare) the compiler may keep them.
     int lane = tid & 63;
-    asm volatile("" : "+v"(lane));
+    if constexpr (!KEEP_OFFSETS) asm volatile("" : "+v"(lane));
     const int w = tid >> 6;
     const int rl = w * (64 / CPR) + lane / CPR;             // row within block 0 of this wave
     // source chunk of the lane in instruction i (tile row i * RPI + rl)

@@ -93,8 +93,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_bf16_kernel(AttnArgs a) 
     // when it starts past the user's end, so every copied unit holds a valid row).
     auto issue = [&](int t, int half, int buf) {
         const int r0 = t * BN + 32 * half;
-        tile_dma<DH, 32>(sQG[buf], Qb, a.ld_q, r0, nb, h * DH, tid);
-        tile_dma<DH, 32>(sQG[buf] + UNIT, Gb, a.ld_o, r0, nb, h * DH, tid);
+        tile_dma_pair<DH, 32>(sQG[buf], Qb, a.ld_q, sQG[buf] + UNIT, Gb, a.ld_o, r0, nb, h * DH, tid);
         codes_dma<32>(sQts[buf], sQcode[buf], a.ts + ob, a.tok_code + ob, r0, nb, tid);
     };
 

@@ -466,6 +466,44 @@ __device__ __forceinline__ void tile_dma(uint16_t* tile, const uint16_t* base, l
     }
 }
 
+// tile_dma of the same rows and columns of two matrices into two tiles (the query unit's Q and
+// dO): the per-lane row and chunk are derived once for both copies.
+template <int DH, int ROWS>
+__device__ __forceinline__ void tile_dma_pair(uint16_t* tile_a, const uint16_t* base_a, long long ld_a,
+                                              uint16_t* tile_b, const uint16_t* base_b, long long ld_b,
+                                              int row0, int nrows, int col0, int tid) {
+    constexpr int CPR = DH / 8, RPI = 256 / CPR, NCH = ROWS * CPR;
+    static_assert(NCH % 64 == 0, "whole LDS blocks");
+    int lane = tid & 63;
+    asm volatile("" : "+v"(lane));
+    const int w = tid >> 6;
+    const int rl = w * (64 / CPR) + lane / CPR;
+    auto src_chunk = [&](int i) { return (lane % CPR) ^ swz<CPR>(RPI % 16 == 0 ? rl : i * RPI + rl); };
+    const uint16_t* ta = base_a + (long long)row0 * ld_a + col0;
+    const uint16_t* tb = base_b + (long long)row0 * ld_b + col0;
+    const uint32_t la = __builtin_amdgcn_readfirstlane(lds_address(tile_a) + (uint32_t)w * 1024u);
+    const uint32_t lb = __builtin_amdgcn_readfirstlane(lds_address(tile_b) + (uint32_t)w * 1024u);
+    if (NCH < 256 && w * 64 >= NCH) return;
+    if (row0 + ROWS <= nrows) {
+#pragma unroll
+        for (int i = 0; i < (NCH + 255) / 256; i++) {
+            const int c8 = src_chunk(i) * 8;
+            lds_dma16(la + (uint32_t)i * 4096u, uniform_ptr(ta + (long long)i * RPI * ld_a),
+                      (uint32_t)(rl * ld_a + c8) * 2u);
+            lds_dma16(lb + (uint32_t)i * 4096u, uniform_ptr(tb + (long long)i * RPI * ld_b),
+                      (uint32_t)(rl * ld_b + c8) * 2u);
+        }
+    } else {
+        const int last = nrows - 1 - row0;                  // >= 0: the tile holds a valid row
+#pragma unroll
+        for (int i = 0; i < (NCH + 255) / 256; i++) {
+            const int c8 = src_chunk(i) * 8, r = min(i * RPI + rl, last);
+            lds_dma16(la + (uint32_t)i * 4096u, uniform_ptr(ta), (uint32_t)(r * ld_a + c8) * 2u);
+            lds_dma16(lb + (uint32_t)i * 4096u, uniform_ptr(tb), (uint32_t)(r * ld_b + c8) * 2u);
+        }
+    }
+}
+
 // Timestamps and mask codes of N (at most 64) consecutive tokens into LDS (two 4-byte-per-lane
 // copies issued by wave 0).  Tokens at or past `ntok` are copied from token ntok - 1
 // (tok0 < ntok); the caller zeroes their codes once the copy has landed.

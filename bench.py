@@ -375,32 +375,7 @@ def main():
     # The same step captured once in a HIP graph and replayed (after the timed region; the
     # library allocates, synchronises and copies nothing on this path, so a caller can record
     # it): what a graph-capturing caller saves in launch overhead, largest on the small batches.
-    graph = None
-    if not args.no_graph:
-        side = torch.cuda.Stream()
-        side.wait_stream(torch.cuda.current_stream())
-        with torch.cuda.stream(side):
-            for s in stages:
-                run(s)
-        torch.cuda.current_stream().wait_stream(side)
-        torch.cuda.synchronize()
-        g = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g):
-            for s in stages:
-                run(s)
-        g.replay()
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for _ in range(args.steps):
-            g.replay()
-        e1.record()
-        torch.cuda.synchronize()
-        ms_g = e0.elapsed_time(e1) / args.steps
-        graph = {"ms_per_step": ms_g, "tokens_per_s": T / (ms_g * 1e-3),
-                 "how": "the timed step's stages captured once in a HIP graph, replayed `steps` times "
-                        "after the timed region (HIP events around the replays)"}
-        del g
+    graph = None if args.no_graph else graph_replay(lambda: [run(s) for s in stages], args.steps, T)
 
     res = {"o": o}
     err_lit, err_adj = sampled_parity(layout, inp, res, check_users)
@@ -494,6 +469,38 @@ def main():
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(layout, args.cpu_seconds)
     print(json.dumps(line), flush=True)
+
+
+def graph_replay(step, steps: int, tokens: int) -> dict:
+    """The step captured once in a HIP graph (after a warm-up on a side stream) and replayed
+    `steps` times, HIP events around the replays.  Reported, never fatal: a capture error is
+    returned as a string."""
+    import torch
+    try:
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            step()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            step()
+        g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / steps
+        return {"ms_per_step": ms, "tokens_per_s": tokens / (ms * 1e-3),
+                "how": "the timed step's stages captured once in a HIP graph, replayed `steps` times "
+                       "after the timed region (HIP events around the replays)"}
+    except RuntimeError as e:
+        torch.cuda.synchronize()
+        return {"error": str(e)[:200]}
 
 
 def bench_layer(args, layout):

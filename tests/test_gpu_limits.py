@@ -1,4 +1,5 @@
-"""GPU parity at the head-count limits of the boundary (1 and MTGR_MAX_HEADS = 255).
+"""GPU parity at the limits: head counts 1 and MTGR_MAX_HEADS = 255, and users longer than one
+window of the tile walker.
 
 The work list packs the head into the low 8 bits of an item, the relative-bias table and its
 gradient are indexed per head, and the tile summaries and token codes are per user: the
@@ -37,16 +38,13 @@ def users():
     return segs, tss
 
 
-@pytest.mark.parametrize("heads", [1, MAX_HEADS])
-@pytest.mark.parametrize("dtype,dh,rab", [("bf16", 32, 64), ("bf16", 32, 0), ("bf16", 16, 64), ("fp32", 16, 64)])
-def test_head_count_limits(heads, dtype, dh, rab):
-    segs, tss = users()
-    L = custom_layout(segs, tss, heads=heads, head_dim=dh, dtype=dtype, rab_buckets=rab)
+def check_attention(L, label):
+    """Forward and both backward forms of the layout's batch against the oracle."""
+    dtype, dh, rab = L.spec.dtype, L.spec.head_dim, L.spec.rab_buckets
     inp = make_inputs(L, all_exact=True)
     jag = jagged(inp)
     q, k, v, do, rb = inp["q"], inp["k"], inp["v"], inp["do"], inp["rab"]
-    label = f"H={heads} {dtype} dh={dh} rab={rab}"
-    say(f"[limits] {label}: T={L.total_tokens}")
+    say(f"[limits] {label}: T={L.total_tokens} users={L.num_users}")
     o = ops.attn_fwd(q, k, v, jag, rb)
     p = ops.attn_problem(jag, q, k, v, do, rb)
     outs = {"stored": ops.attn_bwd(q, k, v, do, jag, rb, workspace=ops.workspace_for(p, q.device, backward=True))}
@@ -72,3 +70,36 @@ def test_head_count_limits(heads, dtype, dh, rab):
     if len(outs) == 2:   # dK, dV come from the same kernel in both forms; dQ sums in another order
         for i, t in ((1, "dk"), (2, "dv")):
             assert torch.equal(outs["stored"][i], outs["recompute"][i]), (label, t)
+
+
+@pytest.mark.parametrize("heads", [1, MAX_HEADS])
+@pytest.mark.parametrize("dtype,dh,rab", [("bf16", 32, 64), ("bf16", 32, 0), ("bf16", 16, 64), ("fp32", 16, 64)])
+def test_head_count_limits(heads, dtype, dh, rab):
+    segs, tss = users()
+    L = custom_layout(segs, tss, heads=heads, head_dim=dh, dtype=dtype, rab_buckets=rab)
+    check_attention(L, f"H={heads} {dtype} dh={dh} rab={rab}")
+
+
+def long_users():
+    """Users longer than 64 tiles of 64 tokens, so the tile walker reloads its window of tile
+    classes (every other test user fits one window): real-time tokens in time order (causal)
+    followed by candidates, whose tiles against each other are MASKED off the diagonal, so the
+    last window of the first user holds candidate tiles only and is skipped whole; a short user
+    between them.  (A user made almost only of candidates, each key seen by itself alone, has
+    per-user gradient RMS diluted several times by those near-zero keys; the bar is per user.)"""
+    U, S, R, C = SEG_USER, SEG_HIST, SEG_RT, SEG_CAND
+    rng = np.random.default_rng(43)
+    segs, tss = [], []
+    for n_u, n_s, n_r, n_c in ((4, 60, 4800, 3436), (3, 40, 10, 5), (12, 100, 4500, 200)):
+        segs.append([U] * n_u + [S] * n_s + [R] * n_r + [C] * n_c)
+        tss.append([0] * n_u + sorted(rng.integers(-10**7, 0, n_s).tolist()) +
+                   sorted(rng.choice(10**6, n_r, replace=False).tolist()) + rng.integers(0, 10**6, n_c).tolist())
+    return segs, tss
+
+
+@pytest.mark.parametrize("dtype,dh,rab", [("bf16", 128, 0), ("bf16", 64, 64), ("fp32", 32, 64)])
+def test_long_users_across_walker_windows(dtype, dh, rab):
+    segs, tss = long_users()
+    L = custom_layout(segs, tss, heads=2, head_dim=dh, dtype=dtype, rab_buckets=rab)
+    assert max(len(x) for x in segs) > 64 * 64
+    check_attention(L, f"long users {dtype} dh={dh} rab={rab}")

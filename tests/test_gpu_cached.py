@@ -125,6 +125,24 @@ def test_custom_users(dh, rab):
     run_case(custom(dh, rab), f"custom-{dh}-rab{rab}", requests=2)
 
 
+def long_user(dh, rab):
+    """A user whose cached side spans two windows of the tile walker (4,864 tokens, 76 tiles of
+    64; real-time tokens in time order), with 300 candidates, and a short user beside it."""
+    U, S, R, C = SEG_USER, SEG_HIST, SEG_RT, SEG_CAND
+    rng = np.random.default_rng(37)
+    segs, tss = [], []
+    for n_u, n_s, n_r, n_c in ((4, 60, 4800, 300), (2, 30, 5, 20)):
+        segs.append([U] * n_u + [S] * n_s + [R] * n_r + [C] * n_c)
+        tss.append([0] * n_u + sorted(rng.integers(-10**7, 0, n_s).tolist()) +
+                   sorted(rng.choice(10**6, n_r, replace=False).tolist()) + rng.integers(0, 10**6, n_c).tolist())
+    return custom_layout(segs, tss, heads=2, head_dim=dh, dtype="bf16", rab_buckets=rab)
+
+
+@pytest.mark.parametrize("dh,rab", [(128, 0), (64, 64)])
+def test_long_cached_side(dh, rab):
+    run_case(long_user(dh, rab), f"long-{dh}-rab{rab}", requests=2)
+
+
 def test_serving_users():
     L = make_layout("serving")
     lens = np.diff(L.offsets)

@@ -76,3 +76,12 @@ def test_serving_subset():
     users = [0, 1, int(np.argmax(np.diff(L.offsets))), L.num_users - 1]
     sub = L.subset(sorted(set(users)))
     run_case(sub, make_inputs(sub, all_exact=True), "serving-subset")
+
+
+def test_long_users():
+    """Users longer than one 64-tile window of the tile walker (8,300 and 4,812 tokens), with
+    3,436 and 200 candidates."""
+    from tests.test_gpu_limits import long_users
+    segs, tss = long_users()
+    L = custom_layout(segs, tss, heads=2, head_dim=128, dtype="bf16", rab_buckets=64)
+    run_case(L, make_inputs(L, all_exact=True), "long-bf16-128-rab64")

@@ -24,6 +24,8 @@ MTGR_DTYPE_BF16 = 0
 MTGR_DTYPE_FP32 = 1
 MTGR_SEG_USER, MTGR_SEG_HIST, MTGR_SEG_RT, MTGR_SEG_CAND = 0, 1, 2, 3
 MTGR_MAX_RAB_BUCKETS = 64
+MTGR_MAX_HEADS = 255
+MTGR_MAX_GROUPS = 127
 MTGR_MAX_LD = 1 << 24
 MTGR_ATTN_PLANNED = 1
 MTGR_BWD_SKIP_DQ = 2

@@ -531,3 +531,20 @@ def test_clock_probe_argument_checks():
         with pytest.raises(hstu.MtgrError) as e:
             hstu.mtgr_debug_clock_probe(*args, stream=0)
         assert e.value.status == status
+
+
+def test_binding_constants_match_the_headers():
+    """Every integer #define of include/*.h that the Python binding mirrors has the header's value."""
+    checked = []
+    for name in sorted(os.listdir(os.path.join(ROOT, "include"))):
+        if not name.endswith(".h"):
+            continue
+        text = open(os.path.join(ROOT, "include", name)).read()
+        for m in re.finditer(r"^#define\s+(MTGR_\w+)\s+([^\n]*?)\s*(?:/\*.*)?$", text, re.M):
+            macro, expr = m.group(1), m.group(2)
+            if not expr or not hasattr(hstu, macro):
+                continue
+            value = eval(re.sub(r"\b(0x[0-9A-Fa-f]+|\d+)(?:ull|ll|u)\b", r"\1", expr), {"__builtins__": {}})
+            assert getattr(hstu, macro) == value, (name, macro, expr, getattr(hstu, macro))
+            checked.append(macro)
+    assert {"MTGR_MAX_HEADS", "MTGR_MAX_GROUPS", "MTGR_MAX_RAB_BUCKETS", "MTGR_MAX_LD"} <= set(checked), checked

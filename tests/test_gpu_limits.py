@@ -12,13 +12,13 @@ import pytest
 import torch
 
 import oracle
-from paper_2505_18654_amd import ops
+from paper_2505_18654_amd import hstu, ops
 from synth import SEG_CAND, SEG_HIST, SEG_RT, SEG_USER, make_values
 from tests.gpu_util import TOL, custom_layout, jagged, make_inputs, per_user_err, rel_err, say, to_np
 
 pytestmark = pytest.mark.gpu
 
-MAX_HEADS = 255
+MAX_HEADS = hstu.MTGR_MAX_HEADS
 
 
 @pytest.fixture(scope="module", autouse=True)
